@@ -1,0 +1,469 @@
+"""Pins for the CPU oracle: checks that tie it to the paper's definitions
+through something other than itself (hand-worked fixtures, closed forms,
+invariants, special cases that reduce to a library routine, brute force on
+tiny inputs).
+
+Every pin takes an `oracle.Oracle` instance so the same checks run on the
+real oracle (tests/test_oracle_pins.py) and on copies of it with planted
+mistakes (tests/test_oracle_mutants.py), where at least one pin of the
+group must fail.  Each pin raises AssertionError on failure.
+"""
+import itertools
+import math
+import os
+
+import numpy as np
+import torch
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+# ------------------------------------------------------------- test helpers
+def bits_to_f64(u16):
+    return (np.asarray(u16, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def f64_to_bits(x):
+    """Exact bf16 values -> bit patterns (asserts exactness)."""
+    x32 = np.asarray(x, dtype=np.float32)
+    u = x32.view(np.uint32)
+    assert np.all((u & 0xFFFF) == 0), "value not exactly representable in bf16"
+    return (u >> 16).astype(np.uint16)
+
+
+def rand_bf16(shape, seed, scale=1.0):
+    g = torch.Generator().manual_seed(seed)
+    x = torch.randn(*shape, generator=g) * scale
+    return x.to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def make_records(Kbits, Vbits):
+    """Kbits, Vbits: uint16 [..., nblk, blk, d] -> records uint16 [..., nblk, 2*blk*d]
+    (K tile row-major, V tile channel-major)."""
+    Kbits = np.asarray(Kbits, dtype=np.uint16)
+    Vbits = np.asarray(Vbits, dtype=np.uint16)
+    *lead, blk, d = Kbits.shape
+    kpart = Kbits.reshape(*lead, blk * d)
+    vpart = np.swapaxes(Vbits, -1, -2).reshape(*lead, d * blk)
+    return np.ascontiguousarray(np.concatenate([kpart, vpart], axis=-1))
+
+
+def dense_offsets(units, nblk_max, blk, d):
+    return (np.arange(units, dtype=np.int64) * nblk_max * 2 * blk * d * 2)
+
+
+def read_fixture(name):
+    rows = {}
+    for line in open(os.path.join(GOLDEN, name)):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        key, *vals = line.split()
+        rows[key] = vals
+    return rows
+
+
+# ------------------------------------------------------------------ O0 meta
+def pin_meta_bruteforce(O):
+    """lo/hi equal numpy's channel-wise min/max over each block's tokens,
+    and lo <= K <= hi for every token (the cuboid bounds every key)."""
+    B, Hkv, nblk, blk, d = 2, 3, 5, 4, 8
+    K = rand_bf16((B, Hkv, nblk, blk, d), 11)
+    V = rand_bf16((B, Hkv, nblk, blk, d), 12)
+    rec = make_records(K, V)
+    meta = O.build_metadata(rec, dense_offsets(B * Hkv, nblk, blk, d), np.full(B, nblk, np.int32),
+                            B, Hkv, nblk, blk, d)
+    Kf = bits_to_f64(K)
+    lo = bits_to_f64(meta[..., 0, :])
+    hi = bits_to_f64(meta[..., 1, :])
+    assert np.array_equal(lo, Kf.min(axis=3)), "lo is not the channel-wise minimum"
+    assert np.array_equal(hi, Kf.max(axis=3)), "hi is not the channel-wise maximum"
+    assert np.all(lo[:, :, :, None, :] <= Kf) and np.all(Kf <= hi[:, :, :, None, :])
+
+
+def pin_meta_ragged_untouched(O):
+    """Blocks past a sequence's length are not written; shorter sequences
+    still get the right metadata."""
+    B, Hkv, nblk_max, blk, d = 3, 2, 6, 2, 4
+    nblk = np.array([6, 2, 0], np.int32)
+    K = rand_bf16((B, Hkv, nblk_max, blk, d), 21)
+    rec = make_records(K, K)
+    sentinel = np.full((B, Hkv, nblk_max, 2, d), 0x7777, np.uint16)
+    meta = O.build_metadata(rec, dense_offsets(B * Hkv, nblk_max, blk, d), nblk, B, Hkv, nblk_max, blk, d,
+                            meta=sentinel.copy())
+    Kf = bits_to_f64(K)
+    for b in range(B):
+        n = nblk[b]
+        assert np.all(meta[b, :, n:] == 0x7777), "wrote past the sequence's blocks"
+        assert np.array_equal(bits_to_f64(meta[b, :, :n, 0]), Kf[b, :, :n].min(axis=2))
+        assert np.array_equal(bits_to_f64(meta[b, :, :n, 1]), Kf[b, :, :n].max(axis=2))
+
+
+def pin_meta_signed_zero(O):
+    """Hand-worked fixture: -0 < +0 in the min/max (totalOrder reading)."""
+    fx = read_fixture("metadata_signed_zero.txt")
+    K = np.array([[int(x, 16) for x in fx[f"key_t{t}"]] for t in range(3)], np.uint16)
+    rec = make_records(K[None, None, None], K[None, None, None])
+    meta = O.build_metadata(rec, np.zeros(1, np.int64), np.array([1], np.int32), 1, 1, 1, 3, 3)
+    assert [int(x) for x in meta[0, 0, 0, 0]] == [int(x, 16) for x in fx["lo"]]
+    assert [int(x) for x in meta[0, 0, 0, 1]] == [int(x, 16) for x in fx["hi"]]
+
+
+def pin_meta_record_offsets(O):
+    """Units placed at arbitrary (non-dense, reversed) byte offsets."""
+    Hkv, nblk, blk, d = 3, 4, 2, 4
+    K = rand_bf16((1, Hkv, nblk, blk, d), 31)
+    rec = make_records(K, K)[0]  # [Hkv][nblk][rec]
+    rb = rec.shape[-1] * 2
+    buf = np.zeros((Hkv + 1) * nblk * rec.shape[-1], np.uint16)
+    offs = np.array([(Hkv - g) * nblk * rb for g in range(Hkv)], np.int64)
+    for g in range(Hkv):
+        w = offs[g] // 2
+        buf[w:w + nblk * rec.shape[-1]] = rec[g].reshape(-1)
+    meta = O.build_metadata(buf, offs, np.array([nblk], np.int32), 1, Hkv, nblk, blk, d)
+    Kf = bits_to_f64(K)
+    assert np.array_equal(bits_to_f64(meta[0, :, :, 0]), Kf[0].min(axis=2))
+    assert np.array_equal(bits_to_f64(meta[0, :, :, 1]), Kf[0].max(axis=2))
+
+
+# ----------------------------------------------------------------- O1 score
+def _meta_from_keys(Kf):
+    """[..., blk, d] exact bf16 values -> metadata bits [..., 2, d] via numpy min/max."""
+    return np.stack([f64_to_bits(Kf.min(axis=-2)), f64_to_bits(Kf.max(axis=-2))], axis=-2)
+
+
+def pin_score_fixture(O):
+    """Hand-worked fixture (golden/score_box.txt)."""
+    fx = read_fixture("score_box.txt")
+    K = np.array([[float(x) for x in fx["key_t0"]], [float(x) for x in fx["key_t1"]]])
+    q = np.array([[float(x) for x in fx["q_h0"]], [float(x) for x in fx["q_h1"]]])
+    meta = _meta_from_keys(K)[None, None, None]
+    S = O.score(f64_to_bits(q)[None], meta, np.array([1], np.int32), 2, 1, 1, 4)
+    assert S[0, 0, 0] == float(fx["score"][0]), S
+    # each head alone (G = 1 views of the same data)
+    for h in range(2):
+        S1 = O.score(f64_to_bits(q[h:h + 1])[None], meta, np.array([1], np.int32), 1, 1, 1, 4)
+        assert S1[0, 0, 0] == float(fx[f"s_h{h}"][0]), (h, S1)
+
+
+def pin_score_upper_bound(O):
+    """Every token's q_h.k_t is <= the block score, for every head of the
+    group (the cuboid contains all keys of the block)."""
+    B, Hq, Hkv, nblk, blk, d = 2, 6, 2, 7, 5, 16
+    K = rand_bf16((B, Hkv, nblk, blk, d), 41, 1.5)
+    q = rand_bf16((B, Hq, d), 42)
+    meta = _meta_from_keys(bits_to_f64(K))
+    S = O.score(q, meta, np.full(B, nblk, np.int32), Hq, Hkv, nblk, d)
+    qf, Kf = bits_to_f64(q), bits_to_f64(K)
+    G = Hq // Hkv
+    for b, g in itertools.product(range(B), range(Hkv)):
+        dots = np.einsum("hc,jtc->hjt", qf[b, g * G:(g + 1) * G], Kf[b, g])
+        assert np.all(dots.max(axis=(0, 2)) <= S[b, g] + 1e-12 * np.abs(S[b, g])), "not an upper bound"
+
+
+def pin_score_point_block(O):
+    """blk = 1: the cuboid is a point, so the score equals max_h q_h.k exactly
+    (up to fp64 rounding of a 32-term sum)."""
+    B, Hq, Hkv, nblk, d = 2, 8, 2, 9, 32
+    K = rand_bf16((B, Hkv, nblk, 1, d), 51)
+    q = rand_bf16((B, Hq, d), 52)
+    meta = _meta_from_keys(bits_to_f64(K))
+    S = O.score(q, meta, np.full(B, nblk, np.int32), Hq, Hkv, nblk, d)
+    qf, Kf = bits_to_f64(q), bits_to_f64(K)
+    G = Hq // Hkv
+    for b, g in itertools.product(range(B), range(Hkv)):
+        ref = (qf[b, g * G:(g + 1) * G] @ Kf[b, g, :, 0].T).max(axis=0)
+        assert np.allclose(S[b, g], ref, rtol=1e-13, atol=1e-13), (S[b, g], ref)
+
+
+def pin_score_corner_tight(O):
+    """A block that contains the cuboid corner favoured by q (hi where q >= 0,
+    lo where q < 0) has score exactly q.corner: the bound is attained."""
+    d, blk, nblk = 16, 6, 5
+    rng = np.random.default_rng(61)
+    q = rand_bf16((1, 1, d), 62)
+    qf = bits_to_f64(q)[0, 0]
+    K = bits_to_f64(rand_bf16((1, 1, nblk, blk, d), 63))
+    lo, hi = K.min(axis=3), K.max(axis=3)
+    corner = np.where(qf >= 0, hi, lo)  # [1,1,nblk,d]
+    for j in range(nblk):
+        K[0, 0, j, rng.integers(blk)] = corner[0, 0, j]
+    meta = _meta_from_keys(K)
+    S = O.score(q, meta, np.array([nblk], np.int32), 1, 1, nblk, d)
+    ref = corner[0, 0] @ qf
+    assert np.allclose(S[0, 0], ref, rtol=1e-13, atol=1e-13), (S[0, 0], ref)
+
+
+def pin_score_ragged(O):
+    """Blocks past a sequence's length score -inf; earlier blocks unaffected."""
+    B, Hq, Hkv, nblk_max, d = 2, 2, 1, 5, 8
+    K = bits_to_f64(rand_bf16((B, Hkv, nblk_max, 1, d), 71))
+    q = rand_bf16((B, Hq, d), 72)
+    meta = _meta_from_keys(K)
+    S = O.score(q, meta, np.array([5, 3], np.int32), Hq, Hkv, nblk_max, d)
+    assert np.all(np.isneginf(S[1, 0, 3:])) and np.all(np.isfinite(S[1, 0, :3]))
+    ref = (bits_to_f64(q)[1] @ K[1, 0, :3, 0].T).max(axis=0)
+    assert np.allclose(S[1, 0, :3], ref, rtol=1e-13)
+
+
+# ---------------------------------------------------------------- O2 select
+def _brute_select(S_row, n, k):
+    order = sorted(range(n), key=lambda j: (-S_row[j], j))[:k]
+    out = sorted(order)
+    return out + [-1] * (k - len(out))
+
+
+def pin_select_fixture(O):
+    fx = read_fixture("select_ties.txt")
+    s = np.array([float(x) for x in fx["scores"]])
+    for k in (1, 2, 3, 4, 6, 8):
+        sel = O.select(s[None, None], np.array([6], np.int32), k)
+        assert sel[0, 0].tolist() == [int(x) for x in fx[f"k{k}"]], (k, sel)
+
+
+def pin_select_bruteforce(O):
+    """Random scores with many exact ties vs a full stable sort."""
+    rng = np.random.default_rng(81)
+    B, Hkv, nblk_max = 3, 2, 40
+    nblk = np.array([40, 17, 3], np.int32)
+    for trial in range(20):
+        S = rng.integers(0, 6, size=(B, Hkv, nblk_max)).astype(np.float64) * 0.5 - 1.0
+        k = int(rng.integers(1, 45))
+        sel = O.select(S, nblk, k)
+        for b, g in itertools.product(range(B), range(Hkv)):
+            assert sel[b, g].tolist() == _brute_select(S[b, g], int(nblk[b]), k), (trial, b, g, k)
+
+
+def pin_select_all_when_k_large(O):
+    """k >= number of blocks selects every block, in order."""
+    S = np.random.default_rng(91).standard_normal((1, 1, 10))
+    sel = O.select(S, np.array([10], np.int32), 10)
+    assert sel[0, 0].tolist() == list(range(10))
+
+
+# ------------------------------------------------------------------ O3 LRU
+class ListLRU:
+    """Brute-force reference for one unit: an explicit recency list of
+    (last_use, slot) entries scanned in order."""
+
+    def __init__(self, cap):
+        self.cap = cap
+        self.block = [-1] * cap
+        self.last = [0] * cap
+
+    def step(self, t, sel):
+        sel = [j for j in sel if j >= 0]
+        slots = {}
+        for j in sel:
+            if j in self.block:
+                s = self.block.index(j)
+                self.last[s] = t
+                slots[j] = s
+        misses = []
+        for j in sel:
+            if j in slots:
+                continue
+            empty = [s for s in range(self.cap) if self.block[s] < 0]
+            if empty:
+                s = empty[0]
+            else:
+                recency = sorted((self.last[s], s) for s in range(self.cap) if self.block[s] not in sel)
+                s = recency[0][1]
+            self.block[s] = j
+            self.last[s] = t
+            slots[j] = s
+            misses.append((j, s))
+        return [slots[j] for j in sel], misses
+
+
+def pin_lru_fixture(O):
+    rows = []
+    final = None
+    for line in open(os.path.join(GOLDEN, "lru_trace.txt")):
+        line = line.strip()
+        if line.startswith("step"):
+            parts = [p.strip() for p in line.split("|")]
+            t = int(parts[0].split()[1])
+            sel = [int(x) for x in parts[1].split()]
+            slots = [int(x) for x in parts[2].split()]
+            miss = [tuple(int(y) for y in x.split(":")) for x in parts[3].split()] if len(parts) > 3 else []
+            rows.append((t, sel, slots, miss))
+        elif line.startswith("final"):
+            final = [tuple(int(y) for y in x.split(":")) for x in line.split()[1:]]
+    c = O.lru(1, 1, np.array([8], np.int32), np.array([3], np.int32))
+    for t, sel, slots, miss in rows:
+        got_slots, got_miss = c.step(t, np.array(sel, np.int32)[None, None])
+        assert got_slots[0, 0].tolist() == slots, (t, got_slots)
+        assert [(int(m[2]), int(m[3])) for m in got_miss] == miss, (t, got_miss)
+        assert all(int(m[0]) == 0 and int(m[1]) == 0 for m in got_miss)
+    blocks, last = c.export()
+    assert [(s, int(blocks[s]), int(last[s])) for s in range(3)] == final
+
+
+def pin_lru_bruteforce(O):
+    """Random selection streams with locality vs the recency-list reference,
+    plus the cache invariants."""
+    rng = np.random.default_rng(101)
+    for trial in range(6):
+        B, Hkv = 2, 2
+        nblk = rng.integers(6, 30, size=B).astype(np.int32)
+        k = int(rng.integers(1, 6))
+        cap = np.array([[int(rng.integers(k, k + 6)) for _ in range(Hkv)] for _ in range(B)], np.int32)
+        c = O.lru(B, Hkv, nblk, cap)
+        refs = [[ListLRU(int(cap[b, g])) for g in range(Hkv)] for b in range(B)]
+        prev = [[None] * Hkv for _ in range(B)]
+        cached = [[set() for _ in range(Hkv)] for _ in range(B)]
+        for t in range(25):
+            sel = np.full((B, Hkv, k), -1, np.int32)
+            for b, g in itertools.product(range(B), range(Hkv)):
+                m = min(k, int(nblk[b])) - (1 if rng.random() < 0.2 and k > 1 else 0)
+                base = prev[b][g] if prev[b][g] is not None and rng.random() < 0.7 else []
+                keep = [j for j in base if rng.random() < 0.6][:m]
+                rest = [j for j in rng.permutation(int(nblk[b])).tolist() if j not in keep]
+                chosen = sorted(keep + rest[: m - len(keep)])
+                sel[b, g, :len(chosen)] = chosen
+                prev[b][g] = chosen
+            slots, miss = c.step(t, sel)
+            by_unit = {}
+            for mb, mg, j, s in miss.tolist():
+                by_unit.setdefault((mb, mg), []).append((j, s))
+            for b, g in itertools.product(range(B), range(Hkv)):
+                chosen = [j for j in sel[b, g] if j >= 0]
+                rslots, rmiss = refs[b][g].step(t, chosen)
+                assert slots[b, g, :len(chosen)].tolist() == rslots, (trial, t, b, g)
+                assert by_unit.get((b, g), []) == rmiss, (trial, t, b, g)
+                # invariants
+                assert len(set(rslots)) == len(rslots)
+                assert len(rmiss) == len(set(chosen) - cached[b][g])
+                cached[b][g] = set(j for j in refs[b][g].block if j >= 0)
+                assert set(chosen) <= cached[b][g]
+
+
+def pin_lru_repeated_step(O):
+    """Two resolves with the same step number (e.g. a second pass in one
+    decode step): blocks selected by the second call are never evicted by it,
+    even when their last use ties with unselected blocks."""
+    rng = np.random.default_rng(105)
+    for trial in range(10):
+        nblk, cap, k = 12, 4, 3
+        c = O.lru(1, 1, np.array([nblk], np.int32), np.array([cap], np.int32))
+        ref = ListLRU(cap)
+        t = 0
+        for call in range(12):
+            t += int(rng.integers(0, 2))  # nondecreasing, often repeated
+            chosen = sorted(rng.choice(nblk, size=k, replace=False).tolist())
+            slots, miss = c.step(t, np.array(chosen, np.int32)[None, None])
+            rslots, rmiss = ref.step(t, chosen)
+            assert slots[0, 0].tolist() == rslots, (trial, call)
+            assert [(int(m[2]), int(m[3])) for m in miss] == rmiss, (trial, call)
+
+
+def pin_lru_capacity_error(O):
+    c = O.lru(1, 1, np.array([10], np.int32), np.array([2], np.int32))
+    try:
+        c.step(0, np.array([[[1, 2, 3]]], np.int32))
+    except OverflowError:
+        return
+    raise AssertionError("capacity error not raised")
+
+
+# ---------------------------------------------------------------- O4 gather
+def pin_gather_bytes(O):
+    """Each reported miss copies exactly its source record into its slot;
+    nothing else in the cache image changes."""
+    rng = np.random.default_rng(111)
+    B, Hkv, nblk, rb = 2, 3, 7, 64
+    pool = rng.integers(0, 256, size=B * Hkv * nblk * rb, dtype=np.uint8)
+    pool_off = np.arange(B * Hkv, dtype=np.int64) * nblk * rb
+    cap = 4
+    cache = rng.integers(0, 256, size=B * Hkv * cap * rb, dtype=np.uint8)
+    before = cache.copy()
+    cache_off = np.arange(B * Hkv, dtype=np.int64)[::-1].copy() * cap * rb
+    miss = np.array([[0, 0, 3, 1], [1, 2, 6, 0], [1, 0, 0, 3], [0, 2, 5, 2]], np.int32)
+    O.gather(miss, pool, pool_off, cache, cache_off, rb, Hkv)
+    touched = np.zeros_like(cache, dtype=bool)
+    for b, g, j, s in miss.tolist():
+        u = b * Hkv + g
+        dst = slice(cache_off[u] + s * rb, cache_off[u] + (s + 1) * rb)
+        src = slice(pool_off[u] + j * rb, pool_off[u] + (j + 1) * rb)
+        assert np.array_equal(cache[dst], pool[src]), (b, g, j, s)
+        touched[dst] = True
+    assert np.array_equal(cache[~touched], before[~touched])
+
+
+# ------------------------------------------------------------- O5 attention
+def _torch_attention(q, Ksel, Vsel, scale):
+    """Library-routine reference in fp64: softmax(q K^T * scale) V."""
+    qt = torch.from_numpy(q)
+    p = torch.softmax(torch.from_numpy(Ksel) @ qt * scale, dim=0)
+    return (p @ torch.from_numpy(Vsel)).numpy()
+
+
+def pin_attention_fixture(O):
+    fx = read_fixture("attention_two_tokens.txt")
+    q = np.array([[[float(x) for x in fx["q"]]]])
+    K = np.array([[float(x) for x in fx["k0"]], [float(x) for x in fx["k1"]]])
+    V = np.array([[float(x) for x in fx["v0"]], [float(x) for x in fx["v1"]]])
+    rec = make_records(f64_to_bits(K)[None], f64_to_bits(V)[None])
+    out = O.attention(f64_to_bits(q), rec, np.zeros(1, np.int64), np.array([[[0]]], np.int32), 1, 2)
+    ref = np.array([float(x) for x in fx["out"]])
+    assert np.allclose(out[0, 0], ref, rtol=0, atol=1e-6), (out, ref)
+
+
+def pin_attention_dense(O):
+    """Selecting every block reproduces dense softmax attention (torch fp64)."""
+    B, Hq, Hkv, nblk, blk, d = 2, 8, 2, 6, 4, 16
+    K = rand_bf16((B, Hkv, nblk, blk, d), 121, 1.5)
+    V = rand_bf16((B, Hkv, nblk, blk, d), 122)
+    q = rand_bf16((B, Hq, d), 123)
+    rec = make_records(K, V)
+    slots = np.broadcast_to(np.arange(nblk, dtype=np.int32), (B, Hkv, nblk)).copy()
+    out = O.attention(q, rec, dense_offsets(B * Hkv, nblk, blk, d), slots, Hkv, blk)
+    G = Hq // Hkv
+    qf, Kf, Vf = bits_to_f64(q), bits_to_f64(K), bits_to_f64(V)
+    for b, h in itertools.product(range(B), range(Hq)):
+        g = h // G
+        ref = _torch_attention(qf[b, h], Kf[b, g].reshape(-1, d), Vf[b, g].reshape(-1, d), 1 / math.sqrt(d))
+        assert np.allclose(out[b, h], ref, rtol=1e-6, atol=1e-6), (b, h)
+
+
+def pin_attention_subset(O):
+    """Attention over selected slots equals dense attention over just the
+    tokens of those blocks; -1 entries are skipped; slot order is the
+    order listed."""
+    B, Hq, Hkv, nblk, blk, d = 1, 4, 2, 9, 3, 8
+    K = rand_bf16((B, Hkv, nblk, blk, d), 131, 2.0)
+    V = rand_bf16((B, Hkv, nblk, blk, d), 132)
+    q = rand_bf16((B, Hq, d), 133)
+    rec = make_records(K, V)
+    slots = np.array([[[7, 1, 4, -1], [0, 8, -1, -1]]], np.int32)
+    out = O.attention(q, rec, dense_offsets(B * Hkv, nblk, blk, d), slots, Hkv, blk)
+    qf, Kf, Vf = bits_to_f64(q), bits_to_f64(K), bits_to_f64(V)
+    for h in range(Hq):
+        g = h // 2
+        js = [j for j in slots[0, g] if j >= 0]
+        ref = _torch_attention(qf[0, h], Kf[0, g, js].reshape(-1, d), Vf[0, g, js].reshape(-1, d), 1 / math.sqrt(d))
+        assert np.allclose(out[0, h], ref, rtol=1e-6, atol=1e-6), h
+        lo = Vf[0, g, js].reshape(-1, d).min(axis=0)
+        hi = Vf[0, g, js].reshape(-1, d).max(axis=0)
+        assert np.all(out[0, h] >= lo - 1e-6) and np.all(out[0, h] <= hi + 1e-6), "outside the convex hull of V"
+
+
+def pin_attention_empty(O):
+    """No selected token -> zero output."""
+    q = rand_bf16((1, 2, 4), 141)
+    rec = make_records(rand_bf16((1, 2, 2, 4), 142), rand_bf16((1, 2, 2, 4), 143))
+    out = O.attention(q, rec, np.zeros(1, np.int64), np.full((1, 1, 2), -1, np.int32), 1, 2)
+    assert np.all(out == 0)
+
+
+GROUPS = {
+    "meta": [pin_meta_bruteforce, pin_meta_ragged_untouched, pin_meta_signed_zero, pin_meta_record_offsets],
+    "score": [pin_score_fixture, pin_score_upper_bound, pin_score_point_block, pin_score_corner_tight,
+              pin_score_ragged],
+    "select": [pin_select_fixture, pin_select_bruteforce, pin_select_all_when_k_large],
+    "lru": [pin_lru_fixture, pin_lru_bruteforce, pin_lru_repeated_step, pin_lru_capacity_error],
+    "gather": [pin_gather_bytes],
+    "attention": [pin_attention_fixture, pin_attention_dense, pin_attention_subset, pin_attention_empty],
+}
+ALL_PINS = [p for ps in GROUPS.values() for p in ps]

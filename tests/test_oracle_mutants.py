@@ -1,0 +1,99 @@
+"""Planted mistakes in the oracle must fail its pins.
+
+Each case copies oracle/oracle.c, applies one small edit of the kind a
+mistake would make (a dropped term, a wrong sign, index or tie-break, a
+transposed operand), compiles the copy on the CPU and runs the pins of the
+affected group against it: at least one pin must fail.  The real oracle is
+never modified.
+"""
+import multiprocessing
+import os
+import tempfile
+
+import pytest
+
+import oracle
+import oracle.build as obuild
+import pins
+
+MUTANTS = [
+    # (id, group, pattern, replacement)
+    ("meta-min-is-max", "meta", "if (vx < vmn ||", "if (vx > vmn ||"),
+    ("meta-drops-last-token", "meta", "for (int t = 1; t < blk; ++t)", "for (int t = 1; t < blk - 1; ++t)"),
+    ("meta-zero-tie-reversed", "meta", "(vx == vmn && sign_bit(x) && !sign_bit(mn))",
+     "(vx == vmn && !sign_bit(x) && sign_bit(mn))"),
+    ("meta-k-transposed", "meta", "uint16_t x = rec[t * d + c];", "uint16_t x = rec[c * blk + t];"),
+    ("meta-ignores-offsets", "meta", "((const char *)base + unit_off[u]\n",
+     "((const char *)base + (int64_t)u * nblk_max * (int64_t)record_bytes\n"),
+    ("score-min-corner", "score", "s += (a > e ? a : e);", "s += (a < e ? a : e);"),
+    ("score-drops-lo", "score", "s += (a > e ? a : e);", "s += e;"),
+    ("score-first-head-only", "score", "if (s > best)", "if (i == 0)"),
+    ("score-sum-of-heads", "score", "double best = -INFINITY;\n                if (j < n) {",
+     "double best = 0.0;\n                if (j < n) {"),
+    ("score-interleaved-heads", "score", "int h = g * G + i;\n                        const uint16_t *qh",
+     "int h = g + i * Hkv;\n                        const uint16_t *qh"),
+    ("score-ragged-ignored", "score", "if (j < n) {", "if (j < nblk_max) {"),
+    ("select-tie-to-higher", "select", "    if (sa < sb) return 1;\n    return (a > b) - (a < b);",
+     "    if (sa < sb) return 1;\n    return (a < b) - (a > b);"),
+    ("select-unsorted-output", "select", "qsort(order, (size_t)m, sizeof(int), ascending_int);", ""),
+    ("select-smallest", "select", "if (sa > sb) return -1;\n    if (sa < sb) return 1;",
+     "if (sa < sb) return -1;\n    if (sa > sb) return 1;"),
+    ("lru-highest-free-slot", "lru", "if (blocks[s] < 0) { chosen = s; break; }", "if (blocks[s] < 0) { chosen = s; }"),
+    ("lru-evicts-mru", "lru", "last[s] < last[chosen]", "last[s] > last[chosen]"),
+    ("lru-tie-to-higher-slot", "lru", "last[s] < last[chosen]", "last[s] <= last[chosen]"),
+    ("lru-evicts-selected", "lru", "if (is_selected(sel_u, k, blocks[s])) continue;", ""),
+    ("lru-hit-no-refresh", "lru", "                    last[s] = step;\n                    out_u[i] = s;",
+     "                    out_u[i] = s;"),
+    ("gather-slot-as-source", "gather", "pool_off[u] + (int64_t)j * (int64_t)record_bytes;",
+     "pool_off[u] + (int64_t)s * (int64_t)record_bytes;"),
+    ("gather-unit-swap", "gather", "int u = b * Hkv + g;\n        const char *src",
+     "int u = g * Hkv + b;\n        const char *src"),
+    ("attn-no-scale", "attention", "z[i] = scale * dot;", "z[i] = dot;"),
+    ("attn-v-row-major", "attention", "acc[c] += p * bf(Vt[c * blk + t]);", "acc[c] += p * bf(Vt[t * d + c]);"),
+    ("attn-head-mod", "attention", "int g = h / G;\n            int u = b * Hkv + g;\n            const uint16_t *qh",
+     "int g = h % Hkv;\n            int u = b * Hkv + g;\n            const uint16_t *qh"),
+    ("attn-unnormalised", "attention", "double p = z[i] / denom;", "double p = z[i];"),
+    ("attn-drops-last-entry", "attention", "for (int i = 0; i < k; ++i) {\n                int32_t s = slots",
+     "for (int i = 0; i < k - 1; ++i) {\n                int32_t s = slots"),
+    ("attn-drops-first-token", "attention", "for (int t = 0; t < blk; ++t) {\n                    kv_of[n] = rec;",
+     "for (int t = 1; t < blk; ++t) {\n                    kv_of[n] = rec;"),
+]
+
+
+@pytest.fixture(scope="module")
+def src():
+    return open(obuild.SRC).read()
+
+
+@pytest.mark.parametrize("mid,group,pattern,repl", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_mutant_is_caught(mid, group, pattern, repl, src):
+    assert src.count(pattern) == 1, f"mutation pattern for {mid} must occur exactly once"
+    mutated = src.replace(pattern, repl)
+    with tempfile.TemporaryDirectory() as tmp:
+        path = os.path.join(tmp, f"oracle_{mid}.c")
+        open(path, "w").write(mutated)
+        lib = obuild.build(path, os.path.join(tmp, f"liboracle_{mid}.so"), extra=("-Wno-unused-function",
+                                                                                 "-Wno-unused-variable",
+                                                                                 "-Wno-unused-parameter"))
+        # run the pins in a forked child so that a mutant that crashes
+        # (an out-of-bounds index) counts as caught instead of ending pytest
+        ctx = multiprocessing.get_context("fork")
+        child = ctx.Process(target=_run_group, args=(lib, group))
+        child.start()
+        child.join(120)
+        if child.is_alive():
+            child.kill()
+            child.join()
+        assert child.exitcode != 0, f"planted mistake {mid} passed every {group} pin"
+
+
+def _run_group(lib, group):
+    import faulthandler
+    faulthandler.disable()  # a crashing mutant is an expected outcome here
+    O = oracle.Oracle(oracle.load(lib))
+    for pin in pins.GROUPS[group]:
+        try:
+            pin(O)
+        except (AssertionError, RuntimeError, OverflowError, ValueError):
+            os._exit(1)
+    os._exit(0)
