@@ -1,0 +1,208 @@
+/*
+ * sparseserve.h -- C ABI of the MI355X (gfx950) decode-step hot path of
+ * SparseServe's dynamic sparse attention over a hierarchical HBM/DRAM KV
+ * cache (arXiv 2509.24626).
+ *
+ * One decode step of one layer is:
+ *   ss_score_topk        criticality of every KV block from its metadata and
+ *                        top-k block selection per (sequence, KV head)
+ *   ss_cache_resolve     the KV cache manager maps the selected blocks to
+ *                        HBM cache slots and lists the misses (host side)
+ *   ss_gather_blocks     one fused kernel loads every missed block record
+ *                        from pinned, device-mapped DRAM into its slot
+ *   ss_sparse_attention  attention of the decode query over the selected
+ *                        blocks only
+ * plus ss_build_metadata, run when blocks fill.
+ *
+ * Conventions for every call
+ *   - Plain C types only.  `stream` is a hipStream_t passed as void*; NULL
+ *     means the null stream.  GPU calls only enqueue work on `stream` and
+ *     return without synchronising; host calls (ss_cache_*) are synchronous.
+ *   - "device" pointers are GPU-accessible addresses: HBM allocations or the
+ *     device address of pinned, mapped host memory (ss_host_alloc_mapped).
+ *     "host" pointers are ordinary CPU memory.
+ *   - The caller owns every buffer it passes.  The library owns only
+ *     ss_cache handles and memory from ss_host_alloc_mapped.  No GPU call
+ *     allocates memory; workspaces are passed in by the caller.
+ *   - Arguments are validated before anything is enqueued; on failure the
+ *     call returns a non-zero ss_status, enqueues nothing and sets a
+ *     per-thread message readable with ss_last_error().  HIP launch errors
+ *     return SS_ERR_HIP.  Nothing throws across this boundary.
+ *   - Values read by a kernel from device arrays (lengths, selections,
+ *     slots, miss entries) are range-checked by the kernel; out-of-range
+ *     entries are skipped, never dereferenced.
+ *
+ * Shapes and notation: B sequences, Hq query heads, Hkv KV heads with
+ * G = Hq / Hkv query heads per KV head (query head h uses KV head h / G),
+ * d = head dim, blk = tokens per block, nblk_max = block capacity per
+ * sequence in the metadata and score arrays, nblk[b] = blocks of sequence b,
+ * k = blocks selected per (sequence, KV head).  A (sequence b, KV head g)
+ * pair is a "unit" u = b * Hkv + g.
+ * Supported: d == 128, blk in {8, 16, 32}, 1 <= G <= 16, 1 <= k,
+ * nblk_max <= 65536; other values return SS_ERR_UNSUPPORTED.
+ *
+ * Block record (bf16, 2*blk*d*2 bytes; the KV cache block of one KV head,
+ * Section 3.2's (H,N,D) layout: the tokens of one head are contiguous):
+ *     K tile: blk rows of d channels, element (t, c) at bf16 index t*d + c
+ *     V tile: channel-major, element (t, c) at bf16 index blk*d + c*blk + t
+ * The channel-major V tile lets the attention kernel load V^T operand
+ * fragments as 16-byte vectors.
+ */
+#ifndef SPARSESERVE_H
+#define SPARSESERVE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int ss_status;
+#define SS_OK 0
+#define SS_ERR_INVALID_ARG 1 /* null pointer, negative size, inconsistent shape */
+#define SS_ERR_UNSUPPORTED 2 /* outside the supported set above */
+#define SS_ERR_CAPACITY 3    /* a unit selects more blocks than it has cache slots */
+#define SS_ERR_OOM 4         /* host allocation failed, or a caller buffer is too small */
+#define SS_ERR_HIP 5         /* a HIP runtime call or kernel launch failed */
+
+#define SS_ABI_VERSION 1
+
+int ss_abi_version(void);
+const char *ss_status_string(ss_status status);
+/* Message of the last failing call on this thread ("" if none). */
+const char *ss_last_error(void);
+
+/* ---------------------------------------------------------------- memory
+ * Pinned host memory mapped into the GPU's address space: the DRAM tier of
+ * the KV cache that GPU kernels read directly over the host link
+ * (Section 3.2.1, GPU-direct loading).
+ * flags: 0 = coherent (fine-grained), 1 = non-coherent (coarse-grained).
+ * On success *host_ptr is the CPU address and *dev_ptr the GPU address of
+ * the same bytes.  Free with ss_host_free(host_ptr). */
+ss_status ss_host_alloc_mapped(size_t bytes, unsigned flags, void **host_ptr, void **dev_ptr);
+ss_status ss_host_free(void *host_ptr);
+
+/* --------------------------------------------------------------- metadata
+ * Block metadata is the bounding cuboid of the block's keys: the
+ * channel-wise minimum (lo) and maximum (hi) of K over the blk tokens
+ * (Section 2.2; created when a block fills, Section 3.1).  Minimum and
+ * maximum follow IEEE-754 totalOrder (-0 < +0), so every entry is one of the
+ * input values.
+ *   kv_base, unit_off: device; block j of unit u is the record at
+ *       kv_base + unit_off[u] + j * record_bytes (unit_off: device int64
+ *       [B*Hkv], byte offsets; kv_base may be HBM or mapped host memory)
+ *   nblk: device int32 [B], clamped to [0, nblk_max]
+ *   meta: device bf16 [B][Hkv][nblk_max][2][d]: lo[d] then hi[d]; entries
+ *       with j >= nblk[b] are not written. */
+ss_status ss_build_metadata(const void *kv_base, const int64_t *unit_off, const int32_t *nblk,
+                            int B, int Hkv, int nblk_max, int blk, int d, void *meta, void *stream);
+
+/* ------------------------------------------------------ scoring, selection
+ * Criticality of block j for KV head g of sequence b (Section 2.2, the dot
+ * product of the query with the block metadata, taken as the largest value
+ * q.k can reach inside the cuboid), maximised over the G query heads that
+ * share g:
+ *     S(b,g,j) = max_{h in group g} sum_c max(q[b,h,c]*lo[c], q[b,h,c]*hi[c])
+ * computed with exact bf16 products and fp32 accumulation.
+ *   q: device bf16 [B][Hq][d]; meta as produced by ss_build_metadata;
+ *   nblk: device int32 [B]
+ *   scores: device fp32 [B][Hkv][nblk_max]; entries j >= nblk[b] are not
+ *       written. */
+ss_status ss_score_blocks(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv,
+                          int nblk_max, int d, float *scores, void *stream);
+
+/* Top-k block selection per unit (Section 2.2: the k most critical blocks,
+ * chosen per head).  Order: higher score first, equal scores -> lower block
+ * index first (-0.0 and +0.0 are equal).  Output per unit: the first
+ * min(k, nblk[b]) blocks in that order, listed in ascending block index,
+ * then -1 padding.  Scores must not be NaN.
+ *   scores: device fp32 [B][Hkv][nblk_max]; sel: device int32 [B][Hkv][k]. */
+ss_status ss_select_topk(const float *scores, const int32_t *nblk, int B, int Hkv, int nblk_max, int k,
+                         int32_t *sel, void *stream);
+
+/* ss_score_blocks followed by ss_select_topk; `scores` is the caller's
+ * fp32 [B][Hkv][nblk_max] buffer and holds the scores afterwards. */
+ss_status ss_score_topk(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv,
+                        int nblk_max, int d, int k, float *scores, int32_t *sel, void *stream);
+
+/* ------------------------------------------------------------ block cache
+ * The HBM tier of the KV cache manager (Section 3.1): per unit, a region of
+ * capacity[u] fixed-size block slots, managed per head; least-recently-used
+ * eviction.  Host-side state only; the slots' bytes live in the caller's
+ * HBM cache buffer at cache_base + region_off[u] + slot * record_bytes.
+ * Not thread-safe per handle; use one handle per layer.
+ *   nblk: host int32 [B] blocks per sequence; capacity: host int32 [B*Hkv]
+ *   (>= 0).  Regions are laid out unit after unit. */
+typedef struct ss_cache ss_cache;
+ss_status ss_cache_create(int B, int Hkv, const int32_t *nblk, const int32_t *capacity, size_t record_bytes,
+                          ss_cache **out);
+void ss_cache_destroy(ss_cache *cache);
+/* total slots over all units (the HBM cache holds total * record_bytes) */
+int64_t ss_cache_total_slots(const ss_cache *cache);
+/* off: host int64 [B*Hkv], byte offset of each unit's region */
+ss_status ss_cache_region_offsets(const ss_cache *cache, int64_t *off);
+/* Host threads used by ss_cache_resolve (default: hardware concurrency, at most 16). */
+ss_status ss_cache_set_threads(ss_cache *cache, int n_threads);
+
+/* Resolve one step's selection.  Per unit, with sel[u][*] strictly
+ * ascending then -1 padded:
+ *   1. every selected block already cached (a hit) gets last_use = step;
+ *   2. every other selected block (a miss), in ascending block order, takes
+ *      the lowest-numbered empty slot, else the slot whose block is not
+ *      selected in this call and has the smallest last_use (ties: lowest
+ *      slot), evicting that block; the slot gets last_use = step.
+ *   sel: host int32 [B][Hkv][k]
+ *   slots: host int32 [B][Hkv][k], the slot of each selected block (-1 for
+ *       -1 entries)
+ *   miss: host int32 [miss_cap][4] rows (b, g, block, slot), units in order,
+ *       ascending block within a unit; *n_miss rows are written.
+ * Errors (state unchanged): SS_ERR_INVALID_ARG for a malformed selection,
+ * SS_ERR_CAPACITY if a unit selects more blocks than it has slots,
+ * SS_ERR_OOM if miss_cap rows are not enough. */
+ss_status ss_cache_resolve(ss_cache *cache, int64_t step, const int32_t *sel, int k, int32_t *slots,
+                           int32_t *miss, int64_t miss_cap, int64_t *n_miss);
+/* State dump for tests: per slot (units in order) the block it holds (-1
+ * empty) and its last use.  Arrays hold ss_cache_total_slots entries. */
+ss_status ss_cache_export(const ss_cache *cache, int32_t *slot_block, int64_t *slot_last);
+
+/* ----------------------------------------------------------------- gather
+ * FlashH2D-style loading (Section 3.2.1): one kernel copies every missed
+ * block record from the DRAM pool into its HBM cache slot:
+ *     cache_base + cache_off[u] + slot*record_bytes
+ *         <- pool_base + pool_off[u] + block*record_bytes,   u = b*Hkv + g
+ * for each row (b, g, block, slot) of `miss`.
+ *   miss: device (or mapped host) int32 [n_miss][4]
+ *   pool_base: device address of the pool (mapped host memory or HBM)
+ *   pool_off, cache_off: device int64 [B*Hkv] byte offsets
+ *   nblk: device int32 [B]; capacity: device int32 [B*Hkv]
+ * Rows with b, g, block or slot out of range are skipped. */
+ss_status ss_gather_blocks(const int32_t *miss, int64_t n_miss, const void *pool_base, const int64_t *pool_off,
+                           void *cache_base, const int64_t *cache_off, const int32_t *nblk,
+                           const int32_t *capacity, int B, int Hkv, size_t record_bytes, void *stream);
+
+/* ------------------------------------------------------ sparse attention
+ * Attention of each sequence's decode query over the tokens of its selected
+ * blocks only (Section 2.1's S = QK^T/sqrt(d), P = softmax(S), O = PV,
+ * restricted as in Section 2.2):
+ *     z_t = scale * q[b,h] . K_t,  p = softmax(z),  out[b,h] = sum_t p_t V_t
+ * over the tokens t of the records at kv_base + region_off[u] +
+ * slots[u][i]*record_bytes, i < k; entries < 0 or >= slot_limit are
+ * skipped.  With no token the output is 0.  fp32 accumulation; the
+ * probabilities enter the PV product as a bf16 hi/lo pair, so they are
+ * carried to about 16 significant bits.
+ *   q: device bf16 [B][Hq][d]; region_off: device int64 [B*Hkv];
+ *   slots: device int32 [B][Hkv][k]; out: device fp32 [B][Hq][d]
+ *   workspace: device, at least ss_sparse_attention_workspace(...) bytes
+ *   (the call fails with SS_ERR_OOM if ws_bytes is smaller).
+ * All-HBM layouts pass slots = the selection and region_off = the units'
+ * block arrays. */
+size_t ss_sparse_attention_workspace(int B, int Hq, int Hkv, int d, int blk, int k);
+ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t *region_off, const int32_t *slots,
+                              int32_t slot_limit, int B, int Hq, int Hkv, int d, int blk, int k, float scale,
+                              float *out, void *workspace, size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPARSESERVE_H */

@@ -1,0 +1,193 @@
+"""ctypes binding of libsparseserve.so (include/sparseserve.h).
+
+Argument marshalling only: every function here has the name of the C entry
+point it calls and does no computation of its own.  Buffers may be torch
+tensors (device or host), numpy arrays or raw integer addresses; streams
+are torch streams, raw hipStream_t integers, or None for torch's current
+stream.  A failing call raises SparseServeError with the library's message.
+The library must be built (paper_2509_24626_amd/build.py); there is no
+fallback path.
+"""
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "libsparseserve.so")
+
+_lib = None
+
+SS_OK = 0
+SS_ERR_INVALID_ARG = 1
+SS_ERR_UNSUPPORTED = 2
+SS_ERR_CAPACITY = 3
+SS_ERR_OOM = 4
+SS_ERR_HIP = 5
+
+
+class SparseServeError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"[{status}] {message}")
+        self.status = status
+
+
+_vp, _i32, _i64, _sz, _f32 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
+
+_SIGNATURES = {
+    "ss_abi_version": (_i32, []),
+    "ss_status_string": (ctypes.c_char_p, [_i32]),
+    "ss_last_error": (ctypes.c_char_p, []),
+    "ss_host_alloc_mapped": (_i32, [_sz, ctypes.c_uint, _vp, _vp]),
+    "ss_host_free": (_i32, [_vp]),
+    "ss_build_metadata": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),
+    "ss_score_blocks": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),
+    "ss_select_topk": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp]),
+    "ss_score_topk": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp]),
+    "ss_cache_create": (_i32, [_i32, _i32, _vp, _vp, _sz, _vp]),
+    "ss_cache_destroy": (None, [_vp]),
+    "ss_cache_total_slots": (_i64, [_vp]),
+    "ss_cache_region_offsets": (_i32, [_vp, _vp]),
+    "ss_cache_set_threads": (_i32, [_vp, _i32]),
+    "ss_cache_resolve": (_i32, [_vp, _i64, _vp, _i32, _vp, _vp, _i64, _vp]),
+    "ss_cache_export": (_i32, [_vp, _vp, _vp]),
+    "ss_gather_blocks": (_i32, [_vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _sz, _vp]),
+    "ss_sparse_attention_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32]),
+    "ss_sparse_attention": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
+                                   _sz, _vp]),
+}
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: run paper_2509_24626_amd/build.py (no fallback exists)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def exported_names():
+    return list(_SIGNATURES)
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if hasattr(x, "data_ptr"):  # torch.Tensor
+        return x.data_ptr()
+    if hasattr(x, "ctypes"):  # numpy.ndarray
+        return x.ctypes.data
+    raise TypeError(f"cannot pass {type(x)} as a buffer")
+
+
+def _stream(s):
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def _check(status):
+    if status != SS_OK:
+        raise SparseServeError(status, lib().ss_last_error().decode())
+
+
+def ss_abi_version():
+    return lib().ss_abi_version()
+
+
+def ss_status_string(status):
+    return lib().ss_status_string(status).decode()
+
+
+def ss_last_error():
+    return lib().ss_last_error().decode()
+
+
+def ss_host_alloc_mapped(nbytes, flags=0):
+    """Returns (host_address, device_address)."""
+    h, d = ctypes.c_void_p(), ctypes.c_void_p()
+    _check(lib().ss_host_alloc_mapped(nbytes, flags, ctypes.byref(h), ctypes.byref(d)))
+    return h.value or 0, d.value or 0
+
+
+def ss_host_free(host_address):
+    _check(lib().ss_host_free(host_address))
+
+
+def ss_build_metadata(kv_base, unit_off, nblk, B, Hkv, nblk_max, blk, d, meta, stream=None):
+    _check(lib().ss_build_metadata(_ptr(kv_base), _ptr(unit_off), _ptr(nblk), B, Hkv, nblk_max, blk, d, _ptr(meta),
+                                   _stream(stream)))
+
+
+def ss_score_blocks(q, meta, nblk, B, Hq, Hkv, nblk_max, d, scores, stream=None):
+    _check(lib().ss_score_blocks(_ptr(q), _ptr(meta), _ptr(nblk), B, Hq, Hkv, nblk_max, d, _ptr(scores),
+                                 _stream(stream)))
+
+
+def ss_select_topk(scores, nblk, B, Hkv, nblk_max, k, sel, stream=None):
+    _check(lib().ss_select_topk(_ptr(scores), _ptr(nblk), B, Hkv, nblk_max, k, _ptr(sel), _stream(stream)))
+
+
+def ss_score_topk(q, meta, nblk, B, Hq, Hkv, nblk_max, d, k, scores, sel, stream=None):
+    _check(lib().ss_score_topk(_ptr(q), _ptr(meta), _ptr(nblk), B, Hq, Hkv, nblk_max, d, k, _ptr(scores), _ptr(sel),
+                               _stream(stream)))
+
+
+def ss_cache_create(B, Hkv, nblk, capacity, record_bytes):
+    """nblk: host int32 [B]; capacity: host int32 [B*Hkv]. Returns a handle."""
+    h = ctypes.c_void_p()
+    _check(lib().ss_cache_create(B, Hkv, _ptr(nblk), _ptr(capacity), record_bytes, ctypes.byref(h)))
+    return h.value
+
+
+def ss_cache_destroy(handle):
+    lib().ss_cache_destroy(handle)
+
+
+def ss_cache_total_slots(handle):
+    return lib().ss_cache_total_slots(handle)
+
+
+def ss_cache_region_offsets(handle, off):
+    _check(lib().ss_cache_region_offsets(handle, _ptr(off)))
+
+
+def ss_cache_set_threads(handle, n):
+    _check(lib().ss_cache_set_threads(handle, n))
+
+
+def ss_cache_resolve(handle, step, sel, k, slots, miss, miss_cap):
+    """Host arrays; returns the number of miss rows written."""
+    n = ctypes.c_int64(0)
+    _check(lib().ss_cache_resolve(handle, step, _ptr(sel), k, _ptr(slots), _ptr(miss), miss_cap, ctypes.byref(n)))
+    return n.value
+
+
+def ss_cache_export(handle, slot_block, slot_last):
+    _check(lib().ss_cache_export(handle, _ptr(slot_block), _ptr(slot_last)))
+
+
+def ss_gather_blocks(miss, n_miss, pool_base, pool_off, cache_base, cache_off, nblk, capacity, B, Hkv, record_bytes,
+                     stream=None):
+    _check(lib().ss_gather_blocks(_ptr(miss), n_miss, _ptr(pool_base), _ptr(pool_off), _ptr(cache_base),
+                                  _ptr(cache_off), _ptr(nblk), _ptr(capacity), B, Hkv, record_bytes, _stream(stream)))
+
+
+def ss_sparse_attention_workspace(B, Hq, Hkv, d, blk, k):
+    return lib().ss_sparse_attention_workspace(B, Hq, Hkv, d, blk, k)
+
+
+def ss_sparse_attention(q, kv_base, region_off, slots, slot_limit, B, Hq, Hkv, d, blk, k, scale, out, workspace,
+                        ws_bytes, stream=None):
+    _check(lib().ss_sparse_attention(_ptr(q), _ptr(kv_base), _ptr(region_off), _ptr(slots), slot_limit, B, Hq, Hkv,
+                                     d, blk, k, float(scale), _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))

@@ -1,0 +1,410 @@
+// Host side of the KV cache manager's HBM tier (Section 3.1): per
+// (sequence, KV head) unit, a region of fixed-size block slots with
+// least-recently-used replacement.  The selected blocks of a step are
+// resolved to slots here; the misses go to the GPU gather.
+//
+// Per unit: block -> slot map (O(1) hit test), slot -> block, last use, and
+// an intrusive doubly linked list of the cached slots in (last_use, slot)
+// order, so the eviction victim is always the list head.  Hits and misses of
+// a call are unlinked while they are processed (a block selected in this
+// call can never be the victim) and re-appended at the tail in slot order,
+// merged with any tail entries already stamped with the same step.  Empty
+// slots are only ever the top range [used, capacity): slots never empty
+// again, so "lowest empty slot" is a counter.
+//
+// Units are independent; ss_cache_resolve validates every unit, sizes the
+// miss list with a prefix sum, then updates the units in parallel on a
+// small persistent thread pool.  Output order does not depend on threading.
+#include <algorithm>
+#include <atomic>
+#include <condition_variable>
+#include <cstring>
+#include <functional>
+#include <mutex>
+#include <new>
+#include <thread>
+#include <vector>
+
+#include "internal.hpp"
+
+namespace {
+
+class pool {
+  public:
+    explicit pool(int n) { resize(n); }
+    ~pool() { stop(); }
+
+    void resize(int n)
+    {
+        stop();
+        n = std::max(1, std::min(n, 64));
+        quit_.store(false);
+        const uint64_t start = gen_.load(std::memory_order_acquire);  // no job is pending now
+        for (int i = 1; i < n; ++i) workers_.emplace_back([this, i, start] { loop(i, start); });
+        size_ = n;
+    }
+    int size() const { return size_; }
+
+    // run f(worker_index) on every worker (the caller is worker 0), wait for all
+    void run(const std::function<void(int)> &f)
+    {
+        if (size_ == 1) {
+            f(0);
+            return;
+        }
+        {
+            std::lock_guard<std::mutex> g(mu_);
+            job_ = &f;
+            pending_.store(size_ - 1, std::memory_order_relaxed);
+            gen_.fetch_add(1, std::memory_order_release);
+        }
+        cv_.notify_all();
+        f(0);
+        while (pending_.load(std::memory_order_acquire) != 0) std::this_thread::yield();
+        job_ = nullptr;
+    }
+
+  private:
+    void loop(int idx, uint64_t seen)
+    {
+        for (;;) {
+            // spin briefly (a decode step resolves every layer), then sleep
+            uint64_t g = gen_.load(std::memory_order_acquire);
+            for (int spin = 0; g == seen && spin < 20000; ++spin) {
+                std::this_thread::yield();
+                g = gen_.load(std::memory_order_acquire);
+            }
+            if (g == seen) {
+                std::unique_lock<std::mutex> lk(mu_);
+                cv_.wait(lk, [&] { return quit_.load() || gen_.load(std::memory_order_acquire) != seen; });
+                if (quit_.load()) return;
+                g = gen_.load(std::memory_order_acquire);
+            }
+            if (quit_.load()) return;
+            seen = g;
+            (*job_)(idx);
+            pending_.fetch_sub(1, std::memory_order_acq_rel);
+        }
+    }
+    void stop()
+    {
+        {
+            std::lock_guard<std::mutex> g(mu_);
+            quit_.store(true);
+        }
+        cv_.notify_all();
+        for (auto &t : workers_) t.join();
+        workers_.clear();
+        size_ = 1;
+    }
+
+    std::vector<std::thread> workers_;
+    std::mutex mu_;
+    std::condition_variable cv_;
+    std::atomic<uint64_t> gen_{0};
+    std::atomic<int> pending_{0};
+    const std::function<void(int)> *job_ = nullptr;
+    std::atomic<bool> quit_{false};
+    int size_ = 1;
+};
+
+struct unit_state {
+    int32_t cap = 0, nblk = 0, used = 0;
+    int32_t head = -1, tail = -1;  // LRU list of cached slots
+    int64_t slot_base = 0;         // first slot of this unit in the slot arrays
+    int64_t block_base = 0;        // first entry of this unit in block_slot
+};
+
+int default_threads()
+{
+    unsigned n = std::thread::hardware_concurrency();
+    if (n == 0) n = 1;
+    return (int)std::min(16u, n);
+}
+
+// One pool for the process: resolves on different handles take turns.
+std::mutex g_pool_mu;
+pool &shared_pool()
+{
+    static pool p(default_threads());
+    return p;
+}
+
+}  // namespace
+
+struct ss_cache {
+    int B = 0, Hkv = 0;
+    size_t record_bytes = 0;
+    int64_t total_slots = 0;
+    int64_t last_step = INT64_MIN;
+    std::vector<unit_state> units;
+    std::vector<int32_t> block_slot;  // [sum nblk] slot holding the block, -1
+    std::vector<int32_t> slot_block;  // [total] block held, -1 empty
+    std::vector<int64_t> slot_last;   // [total]
+    std::vector<int32_t> prev, next;  // [total] LRU links, slot indices local to the unit
+    std::vector<int64_t> miss_count;  // [units] scratch
+    int threads = 1;                          // workers used by resolve
+    std::vector<std::vector<uint64_t>> mark;  // per worker: slot bitmap for ordering
+    std::vector<std::vector<int32_t>> touched;  // per worker
+};
+
+namespace {
+
+// validates one unit's selection; returns count of valid entries or -1 / -2
+int check_unit(const unit_state &st, const int32_t *sel, int k)
+{
+    int count = 0;
+    int32_t prev = -1;
+    bool padding = false;
+    for (int i = 0; i < k; ++i) {
+        const int32_t j = sel[i];
+        if (j < 0) {
+            if (j != -1) return -1;
+            padding = true;
+            continue;
+        }
+        if (padding || j <= prev || j >= st.nblk) return -1;
+        prev = j;
+        ++count;
+    }
+    if (count > st.cap) return -2;
+    return count;
+}
+
+inline void unlink(ss_cache *c, unit_state &st, int32_t s)
+{
+    int32_t *pv = c->prev.data() + st.slot_base, *nx = c->next.data() + st.slot_base;
+    const int32_t p = pv[s], n = nx[s];
+    if (p >= 0) nx[p] = n; else st.head = n;
+    if (n >= 0) pv[n] = p; else st.tail = p;
+    pv[s] = nx[s] = -1;
+}
+
+void resolve_unit(ss_cache *c, int worker, int u, int64_t step, const int32_t *sel, int k, int32_t *slots,
+                  int32_t *miss_rows, int b, int g)
+{
+    unit_state &st = c->units[u];
+    int32_t *bs = c->block_slot.data() + st.block_base;
+    int32_t *sb = c->slot_block.data() + st.slot_base;
+    int64_t *last = c->slot_last.data() + st.slot_base;
+    int32_t *pv = c->prev.data() + st.slot_base, *nx = c->next.data() + st.slot_base;
+    std::vector<int32_t> &touched = c->touched[worker];
+    touched.clear();
+
+    // 1. hits
+    for (int i = 0; i < k; ++i) {
+        const int32_t j = sel[i];
+        slots[i] = -1;
+        if (j < 0) continue;
+        const int32_t s = bs[j];
+        if (s >= 0) {
+            last[s] = step;
+            unlink(c, st, s);
+            touched.push_back(s);
+            slots[i] = s;
+        }
+    }
+    // 2. misses, ascending block order
+    int64_t nm = 0;
+    for (int i = 0; i < k; ++i) {
+        const int32_t j = sel[i];
+        if (j < 0 || slots[i] >= 0) continue;
+        int32_t s;
+        if (st.used < st.cap) {
+            s = st.used++;
+        } else {
+            s = st.head;  // least recently used, lowest slot among equals
+            unlink(c, st, s);
+            bs[sb[s]] = -1;
+        }
+        sb[s] = j;
+        bs[j] = s;
+        last[s] = step;
+        touched.push_back(s);
+        slots[i] = s;
+        int32_t *row = miss_rows + 4 * nm++;
+        row[0] = b;
+        row[1] = g;
+        row[2] = j;
+        row[3] = s;
+    }
+    if (touched.empty()) return;
+    // 3. re-append the touched slots in slot order, merged with the tail run
+    //    already stamped with this step
+    while (st.tail >= 0 && last[st.tail] == step) {
+        const int32_t s = st.tail;
+        unlink(c, st, s);
+        touched.push_back(s);
+    }
+    std::vector<uint64_t> &bits = c->mark[worker];
+    const size_t words = ((size_t)st.cap + 63) / 64;
+    if (bits.size() < words) bits.resize(words);
+    std::fill(bits.begin(), bits.begin() + words, 0ull);
+    for (int32_t s : touched) bits[s >> 6] |= 1ull << (s & 63);
+    for (size_t w = 0; w < words; ++w) {
+        uint64_t x = bits[w];
+        while (x) {
+            const int32_t s = (int32_t)(w * 64 + __builtin_ctzll(x));
+            x &= x - 1;
+            pv[s] = st.tail;
+            nx[s] = -1;
+            if (st.tail >= 0) nx[st.tail] = s; else st.head = s;
+            st.tail = s;
+        }
+    }
+}
+
+}  // namespace
+
+extern "C" {
+
+ss_status ss_cache_create(int B, int Hkv, const int32_t *nblk, const int32_t *capacity, size_t record_bytes,
+                          ss_cache **out)
+{
+    SS_CHECK_ARG(out, "ss_cache_create: null out");
+    *out = nullptr;
+    SS_CHECK_ARG(B >= 0 && Hkv > 0, "ss_cache_create: bad shape B=%d Hkv=%d", B, Hkv);
+    SS_CHECK_ARG(record_bytes > 0, "ss_cache_create: record_bytes=0");
+    if (B > 0) SS_CHECK_ARG(nblk && capacity, "ss_cache_create: null pointer");
+    ss_cache *c = new (std::nothrow) ss_cache;
+    if (!c) return ss::fail(SS_ERR_OOM, "ss_cache_create: out of memory");
+    try {
+        c->B = B;
+        c->Hkv = Hkv;
+        c->record_bytes = record_bytes;
+        const int units = B * Hkv;
+        c->units.resize(units);
+        int64_t slots = 0, blocks = 0;
+        for (int u = 0; u < units; ++u) {
+            const int32_t n = nblk[u / Hkv], cap = capacity[u];
+            if (n < 0 || cap < 0) {
+                delete c;
+                return ss::fail(SS_ERR_INVALID_ARG, "ss_cache_create: negative nblk or capacity at unit %d", u);
+            }
+            unit_state &st = c->units[u];
+            st.cap = cap;
+            st.nblk = n;
+            st.slot_base = slots;
+            st.block_base = blocks;
+            slots += cap;
+            blocks += n;
+        }
+        c->total_slots = slots;
+        c->block_slot.assign(blocks, -1);
+        c->slot_block.assign(slots, -1);
+        c->slot_last.assign(slots, 0);
+        c->prev.assign(slots, -1);
+        c->next.assign(slots, -1);
+        c->miss_count.assign(units, 0);
+        c->threads = default_threads();
+        c->mark.resize(64);
+        c->touched.resize(64);
+    } catch (const std::bad_alloc &) {
+        delete c;
+        return ss::fail(SS_ERR_OOM, "ss_cache_create: out of memory");
+    }
+    *out = c;
+    return SS_OK;
+}
+
+void ss_cache_destroy(ss_cache *c) { delete c; }
+
+int64_t ss_cache_total_slots(const ss_cache *c) { return c ? c->total_slots : 0; }
+
+ss_status ss_cache_region_offsets(const ss_cache *c, int64_t *off)
+{
+    SS_CHECK_ARG(c && off, "ss_cache_region_offsets: null pointer");
+    for (size_t u = 0; u < c->units.size(); ++u) off[u] = c->units[u].slot_base * (int64_t)c->record_bytes;
+    return SS_OK;
+}
+
+ss_status ss_cache_set_threads(ss_cache *c, int n)
+{
+    SS_CHECK_ARG(c && n > 0, "ss_cache_set_threads: bad argument");
+    c->threads = std::min(n, 64);
+    return SS_OK;
+}
+
+ss_status ss_cache_resolve(ss_cache *c, int64_t step, const int32_t *sel, int k, int32_t *slots, int32_t *miss,
+                           int64_t miss_cap, int64_t *n_miss)
+{
+    SS_CHECK_ARG(c && n_miss && k > 0 && miss_cap >= 0, "ss_cache_resolve: bad argument");
+    *n_miss = 0;
+    const int units = (int)c->units.size();
+    if (units == 0) return SS_OK;
+    SS_CHECK_ARG(sel && slots && (miss || miss_cap == 0), "ss_cache_resolve: null pointer");
+    SS_CHECK_ARG(step >= c->last_step, "ss_cache_resolve: step %lld precedes the previous step %lld",
+                 (long long)step, (long long)c->last_step);
+
+    std::lock_guard<std::mutex> pool_lock(g_pool_mu);
+    pool &workers = shared_pool();
+    if (workers.size() < c->threads) {
+        try {
+            workers.resize(c->threads);
+        } catch (const std::exception &) {
+            return ss::fail(SS_ERR_OOM, "ss_cache_resolve: could not start %d threads", c->threads);
+        }
+    }
+    const int nt = std::min(c->threads, workers.size());
+    // pass 1 (parallel, read-only): validate and count misses per unit
+    std::atomic<int> bad_unit{-1}, bad_kind{0};
+    workers.run([&](int w) {
+        if (w >= nt) return;
+        const int lo = (int)((int64_t)units * w / nt), hi = (int)((int64_t)units * (w + 1) / nt);
+        for (int u = lo; u < hi; ++u) {
+            const unit_state &st = c->units[u];
+            const int32_t *su = sel + (int64_t)u * k;
+            const int cnt = check_unit(st, su, k);
+            if (cnt < 0) {
+                int expect = -1;
+                if (bad_unit.compare_exchange_strong(expect, u)) bad_kind.store(cnt);
+                c->miss_count[u] = 0;
+                continue;
+            }
+            const int32_t *bs = c->block_slot.data() + st.block_base;
+            int64_t m = 0;
+            for (int i = 0; i < k; ++i)
+                if (su[i] >= 0 && bs[su[i]] < 0) ++m;
+            c->miss_count[u] = m;
+        }
+    });
+    if (bad_unit.load() >= 0) {
+        const int u = bad_unit.load();
+        if (bad_kind.load() == -2)
+            return ss::fail(SS_ERR_CAPACITY, "ss_cache_resolve: unit %d selects more blocks than its %d slots", u,
+                            c->units[u].cap);
+        return ss::fail(SS_ERR_INVALID_ARG,
+                        "ss_cache_resolve: unit %d selection is not strictly ascending in [0, nblk) then -1", u);
+    }
+    int64_t total = 0;
+    for (int u = 0; u < units; ++u) {
+        const int64_t m = c->miss_count[u];
+        c->miss_count[u] = total;  // becomes the unit's first output row
+        total += m;
+    }
+    if (total > miss_cap)
+        return ss::fail(SS_ERR_OOM, "ss_cache_resolve: %lld misses > miss_cap %lld", (long long)total,
+                        (long long)miss_cap);
+
+    // pass 2 (parallel): update the units
+    workers.run([&](int w) {
+        if (w >= nt) return;
+        const int lo = (int)((int64_t)units * w / nt), hi = (int)((int64_t)units * (w + 1) / nt);
+        for (int u = lo; u < hi; ++u)
+            resolve_unit(c, w, u, step, sel + (int64_t)u * k, k, slots + (int64_t)u * k, miss + 4 * c->miss_count[u],
+                         u / c->Hkv, u % c->Hkv);
+    });
+    c->last_step = step;
+    *n_miss = total;
+    return SS_OK;
+}
+
+ss_status ss_cache_export(const ss_cache *c, int32_t *slot_block, int64_t *slot_last)
+{
+    SS_CHECK_ARG(c && slot_block && slot_last, "ss_cache_export: null pointer");
+    std::memcpy(slot_block, c->slot_block.data(), sizeof(int32_t) * c->total_slots);
+    std::memcpy(slot_last, c->slot_last.data(), sizeof(int64_t) * c->total_slots);
+    return SS_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,101 @@
+// GPU-direct loading of missed KV blocks (Section 3.2.1, FlashH2D): a single
+// kernel copies every missed block record from the pinned, device-mapped
+// DRAM pool into its HBM cache slot, instead of one memcpy per block.
+//
+// Each workgroup copies whole records (4, 8 or 16 KiB).  Every thread issues
+// all of its 16-byte loads for RPI records before the first store, so each
+// wave keeps RPI*CH KiB of host-link reads in flight; workgroups stride over
+// the miss list.
+#include "internal.hpp"
+
+namespace {
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+template <int CH, int RPI>  // 16-byte chunks per thread per record; records per iteration
+__global__ __launch_bounds__(256) void gather_kernel(const int4 *__restrict__ miss, int64_t n_miss,
+                                                     const uint8_t *__restrict__ pool,
+                                                     const int64_t *__restrict__ pool_off,
+                                                     uint8_t *__restrict__ cache,
+                                                     const int64_t *__restrict__ cache_off,
+                                                     const int32_t *__restrict__ nblk,
+                                                     const int32_t *__restrict__ capacity, int B, int Hkv)
+{
+    constexpr int64_t REC = 4096LL * CH;
+    const int t = threadIdx.x;
+    for (int64_t m0 = (int64_t)blockIdx.x * RPI; m0 < n_miss; m0 += (int64_t)gridDim.x * RPI) {
+        const u32x4_t *src[RPI];
+        u32x4_t *dst[RPI];
+        bool ok[RPI];
+#pragma unroll
+        for (int r = 0; r < RPI; ++r) {
+            ok[r] = false;
+            src[r] = nullptr;
+            dst[r] = nullptr;
+            const int64_t mi = m0 + r;
+            if (mi < n_miss) {
+                const int4 e = miss[mi];  // (b, g, block, slot)
+                if (e.x >= 0 && e.x < B && e.y >= 0 && e.y < Hkv) {
+                    const int64_t u = (int64_t)e.x * Hkv + e.y;
+                    if (e.z >= 0 && e.z < nblk[e.x] && e.w >= 0 && e.w < capacity[u]) {
+                        ok[r] = true;
+                        src[r] = reinterpret_cast<const u32x4_t *>(pool + pool_off[u] + (int64_t)e.z * REC);
+                        dst[r] = reinterpret_cast<u32x4_t *>(cache + cache_off[u] + (int64_t)e.w * REC);
+                    }
+                }
+            }
+        }
+        u32x4_t v[RPI][CH];
+#pragma unroll
+        for (int r = 0; r < RPI; ++r)
+            if (ok[r]) {
+#pragma unroll
+                for (int c = 0; c < CH; ++c) v[r][c] = __builtin_nontemporal_load(src[r] + c * 256 + t);
+            }
+#pragma unroll
+        for (int r = 0; r < RPI; ++r)
+            if (ok[r]) {
+#pragma unroll
+                for (int c = 0; c < CH; ++c) dst[r][c * 256 + t] = v[r][c];
+            }
+    }
+}
+
+template <int CH>
+void launch(const int4 *miss, int64_t n_miss, const uint8_t *pool, const int64_t *pool_off, uint8_t *cache,
+            const int64_t *cache_off, const int32_t *nblk, const int32_t *cap, int B, int Hkv, hipStream_t s)
+{
+    constexpr int RPI = 2;
+    int64_t blocks = (n_miss + RPI - 1) / RPI;
+    const int64_t max_blocks = 2048;
+    if (blocks > max_blocks) blocks = max_blocks;
+    gather_kernel<CH, RPI><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(miss, n_miss, pool, pool_off, cache,
+                                                                         cache_off, nblk, cap, B, Hkv);
+}
+
+}  // namespace
+
+extern "C" ss_status ss_gather_blocks(const int32_t *miss, int64_t n_miss, const void *pool_base,
+                                      const int64_t *pool_off, void *cache_base, const int64_t *cache_off,
+                                      const int32_t *nblk, const int32_t *capacity, int B, int Hkv,
+                                      size_t record_bytes, void *stream)
+{
+    SS_CHECK_ARG(n_miss >= 0 && B >= 0 && Hkv > 0, "ss_gather_blocks: bad shape n_miss=%lld B=%d Hkv=%d",
+                 (long long)n_miss, B, Hkv);
+    SS_CHECK_SUPPORTED(record_bytes == 4096 || record_bytes == 8192 || record_bytes == 16384,
+                       "ss_gather_blocks: record_bytes=%zu (blk 8/16/32 at d=128)", record_bytes);
+    if (n_miss == 0) return SS_OK;
+    SS_CHECK_ARG(miss && pool_base && pool_off && cache_base && cache_off && nblk && capacity,
+                 "ss_gather_blocks: null pointer");
+    SS_CHECK_ARG((reinterpret_cast<uintptr_t>(miss) & 15) == 0, "ss_gather_blocks: miss list not 16-byte aligned");
+    hipStream_t s = ss::as_stream(stream);
+    const int4 *m = reinterpret_cast<const int4 *>(miss);
+    const uint8_t *p = static_cast<const uint8_t *>(pool_base);
+    uint8_t *c = static_cast<uint8_t *>(cache_base);
+    switch (record_bytes) {
+    case 4096: launch<1>(m, n_miss, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, s); break;
+    case 8192: launch<2>(m, n_miss, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, s); break;
+    default: launch<4>(m, n_miss, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, s); break;
+    }
+    return ss::check_launch("ss_gather_blocks");
+}

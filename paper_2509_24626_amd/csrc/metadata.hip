@@ -1,0 +1,120 @@
+// Block metadata: the bounding cuboid (channel-wise min and max) of the keys
+// of each KV block (Section 2.2; built when a block fills, Section 3.1).
+//
+// One wave per block record.  A K tile is blk rows of 128 bf16 channels
+// (256 B per row); each lane loads 16 B (8 channels) of one row per step, so
+// one wave-wide load covers 4 rows.  Min and max run on 16-bit totalOrder
+// keys, two channels per 32-bit word, then across the four row groups of
+// the wave.  Lanes 0..15 write lo and hi.
+#include "internal.hpp"
+
+namespace {
+
+// bf16 bits -> 16-bit key with unsigned order equal to IEEE totalOrder,
+// two lanes per word: negative values flip all bits, others set the sign.
+__device__ __forceinline__ uint32_t to_key2(uint32_t w)
+{
+    uint32_t s = (w >> 15) & 0x00010001u;
+    return w ^ (0x80008000u | (s * 0x7FFFu));
+}
+
+__device__ __forceinline__ uint32_t from_key2(uint32_t k)
+{
+    uint32_t s = (k >> 15) & 0x00010001u;  // set for non-negative values
+    return k ^ (0xFFFFFFFFu ^ (s * 0x7FFFu));
+}
+
+typedef unsigned short u16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t min2(uint32_t a, uint32_t b)
+{
+    u16x2_t r = __builtin_elementwise_min(__builtin_bit_cast(u16x2_t, a), __builtin_bit_cast(u16x2_t, b));
+    return __builtin_bit_cast(uint32_t, r);
+}
+
+__device__ __forceinline__ uint32_t max2(uint32_t a, uint32_t b)
+{
+    u16x2_t r = __builtin_elementwise_max(__builtin_bit_cast(u16x2_t, a), __builtin_bit_cast(u16x2_t, b));
+    return __builtin_bit_cast(uint32_t, r);
+}
+
+template <int BLK>
+__global__ __launch_bounds__(256) void meta_kernel(const uint8_t *__restrict__ kv_base,
+                                                   const int64_t *__restrict__ unit_off,
+                                                   const int32_t *__restrict__ nblk, int Hkv, int nblk_max,
+                                                   int64_t total_blocks, uint16_t *__restrict__ meta)
+{
+    constexpr int D = ss::kHeadDim;
+    constexpr int64_t REC = 2LL * BLK * D * 2;
+    const int lane = threadIdx.x & 63;
+    const int64_t id = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (id >= total_blocks) return;
+    const int64_t u = id / nblk_max;
+    const int j = (int)(id - u * nblk_max);
+    int n = nblk[u / Hkv];
+    n = n < 0 ? 0 : (n > nblk_max ? nblk_max : n);
+    if (j >= n) return;
+
+    const uint8_t *rec = kv_base + unit_off[u] + (int64_t)j * REC;
+    const int row0 = lane >> 4;         // 0..3
+    const int cbyte = (lane & 15) * 16;  // 8 channels
+    uint32_t lo[4], hi[4];
+    {
+        uint4 v = *reinterpret_cast<const uint4 *>(rec + row0 * (D * 2) + cbyte);
+        lo[0] = hi[0] = to_key2(v.x);
+        lo[1] = hi[1] = to_key2(v.y);
+        lo[2] = hi[2] = to_key2(v.z);
+        lo[3] = hi[3] = to_key2(v.w);
+    }
+#pragma unroll
+    for (int r = 4; r < BLK; r += 4) {
+        uint4 v = *reinterpret_cast<const uint4 *>(rec + (r + row0) * (D * 2) + cbyte);
+        uint32_t k0 = to_key2(v.x), k1 = to_key2(v.y), k2 = to_key2(v.z), k3 = to_key2(v.w);
+        lo[0] = min2(lo[0], k0); hi[0] = max2(hi[0], k0);
+        lo[1] = min2(lo[1], k1); hi[1] = max2(hi[1], k1);
+        lo[2] = min2(lo[2], k2); hi[2] = max2(hi[2], k2);
+        lo[3] = min2(lo[3], k3); hi[3] = max2(hi[3], k3);
+    }
+#pragma unroll
+    for (int x = 16; x <= 32; x <<= 1) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            lo[i] = min2(lo[i], (uint32_t)__shfl_xor((int)lo[i], x));
+            hi[i] = max2(hi[i], (uint32_t)__shfl_xor((int)hi[i], x));
+        }
+    }
+    if (lane < 16) {
+        uint16_t *m = meta + ((int64_t)u * nblk_max + j) * (2 * D);
+        uint4 l4 = make_uint4(from_key2(lo[0]), from_key2(lo[1]), from_key2(lo[2]), from_key2(lo[3]));
+        uint4 h4 = make_uint4(from_key2(hi[0]), from_key2(hi[1]), from_key2(hi[2]), from_key2(hi[3]));
+        *reinterpret_cast<uint4 *>(m + lane * 8) = l4;
+        *reinterpret_cast<uint4 *>(m + D + lane * 8) = h4;
+    }
+}
+
+}  // namespace
+
+extern "C" ss_status ss_build_metadata(const void *kv_base, const int64_t *unit_off, const int32_t *nblk, int B,
+                                       int Hkv, int nblk_max, int blk, int d, void *meta, void *stream)
+{
+    SS_CHECK_ARG(B >= 0 && Hkv > 0 && nblk_max >= 0, "ss_build_metadata: bad shape B=%d Hkv=%d nblk_max=%d", B,
+                 Hkv, nblk_max);
+    SS_CHECK_SUPPORTED(d == ss::kHeadDim, "ss_build_metadata: d=%d (only 128)", d);
+    SS_CHECK_SUPPORTED(ss::supported_blk(blk), "ss_build_metadata: blk=%d (8, 16 or 32)", blk);
+    SS_CHECK_SUPPORTED(nblk_max <= ss::kMaxBlocks, "ss_build_metadata: nblk_max=%d > %d", nblk_max,
+                       ss::kMaxBlocks);
+    const int64_t total = (int64_t)B * Hkv * nblk_max;
+    if (total == 0) return SS_OK;
+    SS_CHECK_ARG(kv_base && unit_off && nblk && meta, "ss_build_metadata: null pointer");
+    const int64_t grid = (total + 3) / 4;
+    SS_CHECK_SUPPORTED(grid <= 0x7FFFFFFF, "ss_build_metadata: too many blocks");
+    hipStream_t s = ss::as_stream(stream);
+    const uint8_t *kv = static_cast<const uint8_t *>(kv_base);
+    uint16_t *m = static_cast<uint16_t *>(meta);
+    switch (blk) {
+    case 8: meta_kernel<8><<<dim3((unsigned)grid), dim3(256), 0, s>>>(kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
+    case 16: meta_kernel<16><<<dim3((unsigned)grid), dim3(256), 0, s>>>(kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
+    default: meta_kernel<32><<<dim3((unsigned)grid), dim3(256), 0, s>>>(kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
+    }
+    return ss::check_launch("ss_build_metadata");
+}

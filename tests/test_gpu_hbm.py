@@ -1,0 +1,234 @@
+"""GPU parity, all KV resident in HBM: metadata, block scores, top-k
+selection and sparse attention against the CPU oracle, through the C ABI.
+
+Cases span several tiles with ragged tails, sequences shorter than k, an
+empty sequence, GQA groups of 1, 4, 7 and 16, blocks of 8, 16 and 32
+tokens, k equal to and above the block count (dense attention), exact score
+ties, and the tiny and Llama-3-8B-shaped workloads at their full sizes.
+"""
+import math
+import zlib
+
+import numpy as np
+import pytest
+import torch
+
+import gpu_util as gu
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def ss():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    from paper_2509_24626_amd import binding
+    binding.lib()
+    return binding
+
+
+CASES = {
+    # name: B, Hq, Hkv, blk, nblk_max, k, n_plant, nblk
+    "tiny-b2-h8kv2-ctx4k": (2, 8, 2, 16, 256, 16, 8, None),
+    "ragged-short-empty": (3, 8, 2, 16, 40, 16, 0, [40, 7, 0]),
+    "gqa7-blk8-ragged": (2, 28, 4, 8, 300, 24, 0, [300, 123]),
+    "gqa1-blk32": (2, 4, 4, 32, 64, 8, 0, None),
+    "gqa16-blk16": (1, 32, 2, 16, 100, 10, 0, None),
+    "k-equals-blocks": (2, 8, 2, 16, 20, 20, 0, None),
+    "k-above-blocks": (2, 8, 2, 16, 20, 32, 0, [20, 13]),
+}
+
+_cache = {}
+
+
+def workload(name):
+    if name not in _cache:
+        B, Hq, Hkv, blk, nmax, k, npl, nblk = CASES[name]
+        print(f"[gpu] workload {name}: B={B} Hq={Hq} Hkv={Hkv} blk={blk} nblk_max={nmax} k={k}", flush=True)
+        _cache[name] = gu.HbmWorkload(B, Hq, Hkv, blk, nmax, k, seed=zlib.crc32(name.encode()) % 1000, n_plant=npl, nblk=nblk)
+    return _cache[name]
+
+
+def oracle_meta(oracle_impl, w):
+    return oracle_impl.build_metadata(w.kv_host, w.unit_off_host, w.nblk_host, w.B, w.Hkv, w.nblk_max, w.blk, w.d)
+
+
+def valid_rows_equal(a, b, nblk):
+    for bb in range(a.shape[0]):
+        n = int(nblk[bb])
+        np.testing.assert_array_equal(a[bb, :, :n], b[bb, :, :n])
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_metadata_bitexact(ss, oracle_impl, name):
+    w = workload(name)
+    meta = gu.run_metadata(ss, w)
+    torch.cuda.synchronize()
+    valid_rows_equal(gu.u16(meta), oracle_meta(oracle_impl, w), w.nblk_host)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_scores_and_selection(ss, oracle_impl, name):
+    w = workload(name)
+    meta = gu.run_metadata(ss, w)
+    scores = torch.empty(w.B, w.Hkv, w.nblk_max, dtype=torch.float32, device="cuda")
+    sel = torch.empty(w.B, w.Hkv, w.k, dtype=torch.int32, device="cuda")
+    ss.ss_score_topk(w.q, meta, w.nblk, w.B, w.Hq, w.Hkv, w.nblk_max, w.d, w.k, scores, sel)
+    torch.cuda.synchronize()
+    om = oracle_meta(oracle_impl, w)
+    S = oracle_impl.score(w.q_host, om, w.nblk_host, w.Hq, w.Hkv, w.nblk_max, w.d)
+    osel = oracle_impl.select(S, w.nblk_host, w.k)
+    worst = gu.check_scores(scores.cpu().numpy(), S, w.q_host, om, w.nblk_host, w.Hq // w.Hkv)
+    diff = gu.check_selection(sel.cpu().numpy(), osel, S, w.nblk_host, w.k)
+    print(f"[gpu] {name}: worst relative score error {worst:.2e}; units with tie-band differences {len(diff)}")
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_attention_on_oracle_selection(ss, oracle_impl, name):
+    w = workload(name)
+    om = oracle_meta(oracle_impl, w)
+    S = oracle_impl.score(w.q_host, om, w.nblk_host, w.Hq, w.Hkv, w.nblk_max, w.d)
+    osel = oracle_impl.select(S, w.nblk_host, w.k)
+    out = gu.run_attention(ss, w, torch.from_numpy(osel).cuda())
+    torch.cuda.synchronize()
+    ref = oracle_impl.attention(w.q_host, w.kv_host, w.unit_off_host, osel, w.Hkv, w.blk)
+    err = np.abs(out.cpu().numpy() - ref).max()
+    print(f"[gpu] {name}: attention max abs error {err:.2e}")
+    assert err <= gu.ATTN_TOL
+
+
+@pytest.mark.parametrize("name", ["tiny-b2-h8kv2-ctx4k", "gqa7-blk8-ragged", "ragged-short-empty"])
+def test_end_to_end_step(ss, oracle_impl, name):
+    """GPU selection feeds GPU attention; units whose selection equals the
+    oracle's must match the oracle's attention."""
+    w = workload(name)
+    meta = gu.run_metadata(ss, w)
+    scores = torch.empty(w.B, w.Hkv, w.nblk_max, dtype=torch.float32, device="cuda")
+    sel = torch.empty(w.B, w.Hkv, w.k, dtype=torch.int32, device="cuda")
+    ss.ss_score_topk(w.q, meta, w.nblk, w.B, w.Hq, w.Hkv, w.nblk_max, w.d, w.k, scores, sel)
+    out = gu.run_attention(ss, w, sel).cpu().numpy()
+    om = oracle_meta(oracle_impl, w)
+    S = oracle_impl.score(w.q_host, om, w.nblk_host, w.Hq, w.Hkv, w.nblk_max, w.d)
+    osel = oracle_impl.select(S, w.nblk_host, w.k)
+    ref = oracle_impl.attention(w.q_host, w.kv_host, w.unit_off_host, osel, w.Hkv, w.blk)
+    gsel = sel.cpu().numpy()
+    G = w.Hq // w.Hkv
+    compared = 0
+    for b in range(w.B):
+        for g in range(w.Hkv):
+            if np.array_equal(gsel[b, g], osel[b, g]):
+                compared += 1
+                assert np.abs(out[b, g * G:(g + 1) * G] - ref[b, g * G:(g + 1) * G]).max() <= gu.ATTN_TOL
+    assert compared >= w.units - 1
+
+
+def test_planted_blocks_are_selected(ss):
+    """Sanity (not parity): on the tiny workload every planted block is
+    among the selected blocks of its KV head."""
+    B, Hq, Hkv, blk, nmax, k, npl, _ = CASES["tiny-b2-h8kv2-ctx4k"]
+    seed = zlib.crc32(b"tiny-b2-h8kv2-ctx4k") % 1000
+    w = workload("tiny-b2-h8kv2-ctx4k")
+    meta = gu.run_metadata(ss, w)
+    scores = torch.empty(B, Hkv, nmax, dtype=torch.float32, device="cuda")
+    sel = torch.empty(B, Hkv, k, dtype=torch.int32, device="cuda")
+    ss.ss_score_topk(w.q, meta, w.nblk, B, Hq, Hkv, nmax, 128, k, scores, sel)
+    gsel = sel.cpu().numpy()
+    for b in range(B):
+        for g in range(Hkv):
+            planted = synth.gen.planted_blocks(nmax, npl, seed, 0, b, g, "cuda").cpu().numpy()
+            assert set(planted.tolist()) <= set(gsel[b, g].tolist())
+
+
+def test_topk_exact_ties(ss, oracle_impl):
+    """Scores drawn from a handful of values (massive exact ties, +0 and -0,
+    negatives): the GPU selection must equal the oracle's bit for bit."""
+    rng = np.random.default_rng(5)
+    for B, Hkv, nmax, k, nblk in [(2, 3, 1000, 37, [1000, 999]), (1, 2, 5000, 512, [5000]),
+                                  (2, 2, 300, 300, [300, 17]), (1, 1, 16384, 512, [16384]),
+                                  (3, 1, 64, 1, [64, 1, 2])]:
+        vals = np.array([-3.5, -0.0, 0.0, 1.25, 1.25000012, 7.0, 246.0], np.float32)
+        sc = vals[rng.integers(0, len(vals), size=(B, Hkv, nmax))]
+        sel = torch.empty(B, Hkv, k, dtype=torch.int32, device="cuda")
+        ss.ss_select_topk(torch.from_numpy(sc).cuda(), torch.tensor(nblk, dtype=torch.int32, device="cuda"), B, Hkv,
+                          nmax, k, sel)
+        ref = oracle_impl.select(sc.astype(np.float64), np.array(nblk, np.int32), k)
+        np.testing.assert_array_equal(sel.cpu().numpy(), ref)
+
+
+def test_topk_random_scores_match(ss, oracle_impl):
+    """Continuous random scores (no ties) at the workloads' block counts."""
+    rng = np.random.default_rng(6)
+    for nmax, k in [(256, 16), (2048, 128), (8192, 128), (16384, 512), (700, 699)]:
+        sc = (246 + 21 * rng.standard_normal((2, 2, nmax))).astype(np.float32)
+        sel = torch.empty(2, 2, k, dtype=torch.int32, device="cuda")
+        ss.ss_select_topk(torch.from_numpy(sc).cuda(), torch.full((2,), nmax, dtype=torch.int32, device="cuda"), 2, 2,
+                          nmax, k, sel)
+        ref = oracle_impl.select(sc.astype(np.float64), np.full(2, nmax, np.int32), k)
+        np.testing.assert_array_equal(sel.cpu().numpy(), ref)
+
+
+def test_attention_skips_invalid_slots(ss, oracle_impl):
+    """-1 entries anywhere and slots >= slot_limit are skipped."""
+    w = workload("gqa1-blk32")  # B=2, Hq=Hkv=4, blk 32, 64 blocks, k=8
+    slots = np.array([[[3, -1, 7, 70, 0, -1, 63, 5],
+                       [-1, -1, -1, -1, -1, -1, -1, -1],
+                       [64, 65, 1000, -1, 2, -1, -1, -1],
+                       [10, 11, 12, 13, 14, 15, 16, 17]],
+                      [[1, 2, 3, 4, 5, 6, 64, 65],
+                       [10, -1, 11, -1, 12, -1, 13, -1],
+                       [-1, -1, -1, -1, -1, -1, -1, 9],
+                       [63, 62, 61, 60, 59, 58, 57, 56]]], np.int32)
+    out = gu.run_attention(ss, w, torch.from_numpy(slots).cuda(), slot_limit=64).cpu().numpy()
+    ora_slots = np.where(slots >= 64, -1, slots)
+    ref = oracle_impl.attention(w.q_host, w.kv_host, w.unit_off_host, ora_slots, w.Hkv, w.blk)
+    assert np.abs(out - ref).max() <= gu.ATTN_TOL
+    assert np.all(out[0, 1] == 0)  # every entry skipped -> zero output
+
+
+def test_runs_are_bitwise_deterministic(ss):
+    w = workload("gqa7-blk8-ragged")
+    meta = gu.run_metadata(ss, w)
+    res = []
+    for _ in range(2):
+        scores = torch.empty(w.B, w.Hkv, w.nblk_max, dtype=torch.float32, device="cuda")
+        sel = torch.empty(w.B, w.Hkv, w.k, dtype=torch.int32, device="cuda")
+        ss.ss_score_topk(w.q, meta, w.nblk, w.B, w.Hq, w.Hkv, w.nblk_max, w.d, w.k, scores, sel)
+        out = gu.run_attention(ss, w, sel)
+        res.append((sel.cpu().numpy(), out.cpu().numpy()))
+    np.testing.assert_array_equal(res[0][0], res[1][0])
+    np.testing.assert_array_equal(res[0][1].view(np.uint32), res[1][1].view(np.uint32))
+
+
+def test_llama3_8b_shape_full_size(ss, oracle_impl):
+    """The Llama-3-8B-shaped single layer at full size (B=32, 32/8 heads,
+    32k context, blk 16, k=128, 64 planted blocks per head), every unit
+    checked against the oracle."""
+    cfg = synth.get(1)
+    print(f"[gpu] {cfg.name}: generating", flush=True)
+    w = gu.HbmWorkload(cfg.B, cfg.Hq, cfg.Hkv, cfg.blk, cfg.nblk_max, cfg.k, seed=0, n_plant=cfg.n_plant)
+    meta = gu.run_metadata(ss, w)
+    scores = torch.empty(w.B, w.Hkv, w.nblk_max, dtype=torch.float32, device="cuda")
+    sel = torch.empty(w.B, w.Hkv, w.k, dtype=torch.int32, device="cuda")
+    ss.ss_score_topk(w.q, meta, w.nblk, w.B, w.Hq, w.Hkv, w.nblk_max, w.d, w.k, scores, sel)
+    out = gu.run_attention(ss, w, sel).cpu().numpy()
+    gmeta = gu.u16(meta)
+    print(f"[gpu] {cfg.name}: oracle", flush=True)
+    om = oracle_meta(oracle_impl, w)
+    np.testing.assert_array_equal(gmeta, om)
+    S = oracle_impl.score(w.q_host, om, w.nblk_host, w.Hq, w.Hkv, w.nblk_max, w.d)
+    osel = oracle_impl.select(S, w.nblk_host, w.k)
+    gu.check_scores(scores.cpu().numpy(), S, w.q_host, om, w.nblk_host, w.Hq // w.Hkv)
+    diff = gu.check_selection(sel.cpu().numpy(), osel, S, w.nblk_host, w.k)
+    ref = oracle_impl.attention(w.q_host, w.kv_host, w.unit_off_host, osel, w.Hkv, w.blk)
+    G = w.Hq // w.Hkv
+    worst = 0.0
+    for b in range(w.B):
+        for g in range(w.Hkv):
+            if (b, g) not in diff:
+                worst = max(worst, float(np.abs(out[b, g * G:(g + 1) * G] - ref[b, g * G:(g + 1) * G]).max()))
+    # attention on the oracle's own selection covers every unit
+    out2 = gu.run_attention(ss, w, torch.from_numpy(osel).cuda()).cpu().numpy()
+    worst2 = float(np.abs(out2 - ref).max())
+    print(f"[gpu] {cfg.name}: tie-band units {len(diff)}, attention err {worst:.2e} / {worst2:.2e}")
+    assert worst <= gu.ATTN_TOL and worst2 <= gu.ATTN_TOL
