@@ -202,6 +202,50 @@ ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t 
                               int32_t slot_limit, int B, int Hq, int Hkv, int d, int blk, int k, float scale,
                               float *out, void *workspace, size_t ws_bytes, void *stream);
 
+/* ------------------------------------------------------- one layer's step
+ * The decode step of one layer over the HBM/DRAM hierarchy (Section 3.1's
+ * executor / cache-manager exchange): score and select on the GPU, copy the
+ * selection to the host, resolve it in the block cache, copy slots and the
+ * miss list back, gather the misses, attend.  The only host wait is for the
+ * selection; everything after it is enqueued on `stream` and the call
+ * returns without waiting for it.
+ * All pointers below are caller-owned.  Device buffers: scores fp32
+ * [B][Hkv][nblk_max]; sel_dev and slots_dev int32 [B][Hkv][k]; miss_dev
+ * int32 [miss_cap][4] (16-byte aligned); attn_ws of attn_ws_bytes >=
+ * ss_sparse_attention_workspace(...).  Host buffers (pinned, for
+ * asynchronous copies): sel_host, slots_host int32 [B][Hkv][k]; miss_host
+ * int32 [miss_cap][4].  miss_cap >= B*Hkv*k always suffices.
+ * slot_limit: the largest per-unit capacity (slots at or above it are never
+ * read).  The cache regions of `cache` index cache_base through
+ * cache_off_dev (= ss_cache_region_offsets, copied to the device).
+ * events: NULL, or 5 hipEvent_t recorded on `stream` before scoring, after
+ * selection, before the gather, after the gather and after attention (for
+ * per-stage timing).
+ * On error nothing further is enqueued; a resolve error leaves the cache
+ * unchanged. */
+typedef struct ss_layer_buffers {
+    int B, Hq, Hkv, d, blk, nblk_max, k;
+    float scale;
+    const void *meta;           /* device bf16 [B][Hkv][nblk_max][2][d] */
+    const int32_t *nblk_dev;    /* device int32 [B] */
+    const void *pool;           /* device address of the DRAM pool */
+    const int64_t *pool_off_dev; /* device int64 [B*Hkv] */
+    ss_cache *cache;
+    void *cache_base;           /* HBM cache, ss_cache_total_slots records */
+    const int64_t *cache_off_dev; /* device int64 [B*Hkv] */
+    const int32_t *capacity_dev;  /* device int32 [B*Hkv] */
+    int32_t slot_limit;
+    float *scores;
+    int32_t *sel_dev, *slots_dev, *miss_dev;
+    int32_t *sel_host, *slots_host, *miss_host;
+    int64_t miss_cap;
+    void *attn_ws;
+    size_t attn_ws_bytes;
+} ss_layer_buffers;
+
+ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, const void *q, float *out, void *stream,
+                          void *const *events, int64_t *n_miss);
+
 #ifdef __cplusplus
 }
 #endif

@@ -32,6 +32,16 @@ class SparseServeError(RuntimeError):
 
 _vp, _i32, _i64, _sz, _f32 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_size_t, ctypes.c_float
 
+
+class ss_layer_buffers(ctypes.Structure):
+    """Mirror of the C struct ss_layer_buffers (include/sparseserve.h)."""
+    _fields_ = [("B", _i32), ("Hq", _i32), ("Hkv", _i32), ("d", _i32), ("blk", _i32), ("nblk_max", _i32),
+                ("k", _i32), ("scale", _f32), ("meta", _vp), ("nblk_dev", _vp), ("pool", _vp),
+                ("pool_off_dev", _vp), ("cache", _vp), ("cache_base", _vp), ("cache_off_dev", _vp),
+                ("capacity_dev", _vp), ("slot_limit", _i32), ("scores", _vp), ("sel_dev", _vp),
+                ("slots_dev", _vp), ("miss_dev", _vp), ("sel_host", _vp), ("slots_host", _vp),
+                ("miss_host", _vp), ("miss_cap", _i64), ("attn_ws", _vp), ("attn_ws_bytes", _sz)]
+
 _SIGNATURES = {
     "ss_abi_version": (_i32, []),
     "ss_status_string": (ctypes.c_char_p, [_i32]),
@@ -53,6 +63,7 @@ _SIGNATURES = {
     "ss_sparse_attention_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32]),
     "ss_sparse_attention": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
                                    _sz, _vp]),
+    "ss_decode_layer": (_i32, [ctypes.POINTER(ss_layer_buffers), _i64, _vp, _vp, _vp, _vp, _vp]),
 }
 
 
@@ -191,3 +202,15 @@ def ss_sparse_attention(q, kv_base, region_off, slots, slot_limit, B, Hq, Hkv, d
                         ws_bytes, stream=None):
     _check(lib().ss_sparse_attention(_ptr(q), _ptr(kv_base), _ptr(region_off), _ptr(slots), slot_limit, B, Hq, Hkv,
                                      d, blk, k, float(scale), _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def ss_decode_layer(buffers, step, q, out, stream=None, events=None):
+    """buffers: an ss_layer_buffers; events: None or 5 raw hipEvent_t
+    handles.  Returns the number of blocks gathered."""
+    n = ctypes.c_int64(0)
+    ev = None
+    if events is not None:
+        ev = (ctypes.c_void_p * 5)(*events)
+    _check(lib().ss_decode_layer(ctypes.byref(buffers), step, _ptr(q), _ptr(out), _stream(stream), ev,
+                                 ctypes.byref(n)))
+    return n.value

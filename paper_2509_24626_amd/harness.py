@@ -1,0 +1,204 @@
+"""Composition of the C-ABI calls into decode-step layers, with torch used
+only to hold device memory and streams.
+
+HbmLayer   all KV blocks resident in HBM: score/top-k, then attention with
+           the selection as the slot list.
+HierLayer  KV blocks in a pinned, device-mapped DRAM pool and an LRU HBM
+           block cache per (sequence, KV head): one ss_decode_layer call
+           per step (score/top-k, resolve, gather, attention).
+
+build_hbm_layer / build_hier_layer draw a seeded synthetic layer (synth)
+on the GPU, build its metadata with ss_build_metadata, and for the
+hierarchical case copy the records into the DRAM pool.  Nothing here
+computes any part of the method itself.
+"""
+import ctypes
+import math
+
+import numpy as np
+import torch
+
+import synth
+from synth import gen
+
+from . import binding as ss
+
+D = 128
+
+
+def _dev(a, dtype):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=dtype)).cuda()
+
+
+class HostPool:
+    """Pinned, device-mapped host memory from ss_host_alloc_mapped."""
+
+    def __init__(self, nbytes, flags=0):
+        self.nbytes = nbytes
+        self.host, self.dev = ss.ss_host_alloc_mapped(nbytes, flags)
+        # CPU views of the same bytes (no copy)
+        buf = (ctypes.c_uint8 * nbytes).from_address(self.host)
+        self.u8 = np.frombuffer(buf, dtype=np.uint8)
+        self.t = torch.from_numpy(self.u8)
+
+    def close(self):
+        if self.host:
+            self.t = None
+            self.u8 = None
+            ss.ss_host_free(self.host)
+            self.host = 0
+
+
+class HbmLayer:
+    def __init__(self, cfg, kv, nblk_host, meta=None):
+        self.cfg = cfg
+        B, Hkv = cfg.B, cfg.Hkv
+        self.units = B * Hkv
+        self.kv = kv
+        self.nblk_host = np.asarray(nblk_host, np.int32)
+        self.nblk = _dev(self.nblk_host, np.int32)
+        self.unit_off = _dev(np.arange(self.units, dtype=np.int64) * cfg.nblk_max * cfg.record_bytes, np.int64)
+        self.meta = meta if meta is not None else torch.empty(B, Hkv, cfg.nblk_max, 2, D, dtype=torch.int16,
+                                                              device="cuda")
+        self.scores = torch.empty(B, Hkv, cfg.nblk_max, dtype=torch.float32, device="cuda")
+        self.sel = torch.empty(B, Hkv, cfg.k, dtype=torch.int32, device="cuda")
+        self.out = torch.empty(B, cfg.Hq, D, dtype=torch.float32, device="cuda")
+        self.ws_bytes = ss.ss_sparse_attention_workspace(B, cfg.Hq, Hkv, D, cfg.blk, cfg.k)
+        self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device="cuda")
+
+    def build_metadata(self):
+        c = self.cfg
+        ss.ss_build_metadata(self.kv, self.unit_off, self.nblk, c.B, c.Hkv, c.nblk_max, c.blk, D, self.meta)
+
+    def select(self, q):
+        c = self.cfg
+        ss.ss_score_topk(q, self.meta, self.nblk, c.B, c.Hq, c.Hkv, c.nblk_max, D, c.k, self.scores, self.sel)
+
+    def attend(self, q, slots=None):
+        c = self.cfg
+        ss.ss_sparse_attention(q, self.kv, self.unit_off, self.sel if slots is None else slots, c.nblk_max, c.B,
+                               c.Hq, c.Hkv, D, c.blk, c.k, 1.0 / math.sqrt(D), self.out, self.ws, self.ws_bytes)
+
+    def step(self, q):
+        self.select(q)
+        self.attend(q)
+        return self.out
+
+
+def build_hbm_layer(cfg, seed, layer=0):
+    """Draws a synthetic HBM-resident layer; returns (HbmLayer, q fp32, q bf16)."""
+    q32, q = gen.query(cfg.B, cfg.Hq, D, seed, "cuda", layer)
+    sK, sV = gen.channel_scales(cfg.Hkv, D, seed, layer, "cuda")
+    kv = torch.empty(cfg.B, cfg.Hkv, cfg.nblk_max, cfg.record_bytes // 2, dtype=torch.bfloat16, device="cuda")
+    for b in range(cfg.B):
+        kv[b], _ = gen.kv_records_seq(b, cfg.Hkv, cfg.nblk_max, cfg.blk, D, sK, sV, seed, layer, "cuda",
+                                      q_bf16_b=q[b], n_plant=cfg.n_plant, shift=cfg.plant_shift)
+    lens = gen.lengths(cfg, seed)
+    L = HbmLayer(cfg, kv, (lens // cfg.blk).astype(np.int32))
+    L.build_metadata()
+    return L, q32, q
+
+
+class HierLayer:
+    """One layer of the hierarchical workload: its DRAM pool slice, HBM
+    metadata, HBM block cache and step buffers."""
+
+    def __init__(self, cfg, nblk_host, capacity, pool, pool_off_host, meta):
+        self.cfg = cfg
+        B, Hkv, k = cfg.B, cfg.Hkv, cfg.k
+        self.units = B * Hkv
+        self.nblk_host = np.asarray(nblk_host, np.int32)
+        self.capacity = np.ascontiguousarray(capacity, np.int32).reshape(-1)
+        self.pool = pool
+        self.pool_off_host = np.asarray(pool_off_host, np.int64)
+        self.meta = meta
+        self.handle = ss.ss_cache_create(B, Hkv, self.nblk_host, self.capacity, cfg.record_bytes)
+        self.total_slots = ss.ss_cache_total_slots(self.handle)
+        off = np.empty(self.units, np.int64)
+        ss.ss_cache_region_offsets(self.handle, off)
+        self.cache_off_host = off
+        self.cache = torch.empty(max(self.total_slots, 1) * cfg.record_bytes, dtype=torch.uint8, device="cuda")
+        self.cache_off = _dev(off, np.int64)
+        self.cap_dev = _dev(self.capacity, np.int32)
+        self.nblk = _dev(self.nblk_host, np.int32)
+        self.pool_off = _dev(self.pool_off_host, np.int64)
+        self.scores = torch.empty(B, Hkv, cfg.nblk_max, dtype=torch.float32, device="cuda")
+        self.sel = torch.empty(B, Hkv, k, dtype=torch.int32, device="cuda")
+        self.slots = torch.empty(B, Hkv, k, dtype=torch.int32, device="cuda")
+        self.miss_cap = self.units * k
+        self.miss = torch.empty(self.miss_cap, 4, dtype=torch.int32, device="cuda")
+        self.sel_h = torch.empty(B, Hkv, k, dtype=torch.int32, pin_memory=True)
+        self.slots_h = torch.empty(B, Hkv, k, dtype=torch.int32, pin_memory=True)
+        self.miss_h = torch.empty(self.miss_cap, 4, dtype=torch.int32, pin_memory=True)
+        self.out = torch.empty(B, cfg.Hq, D, dtype=torch.float32, device="cuda")
+        self.ws_bytes = ss.ss_sparse_attention_workspace(B, cfg.Hq, Hkv, D, cfg.blk, k)
+        self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device="cuda")
+        p = ss._ptr
+        self.buffers = ss.ss_layer_buffers(
+            B=B, Hq=cfg.Hq, Hkv=Hkv, d=D, blk=cfg.blk, nblk_max=cfg.nblk_max, k=k, scale=1.0 / math.sqrt(D),
+            meta=p(meta), nblk_dev=p(self.nblk), pool=pool.dev, pool_off_dev=p(self.pool_off), cache=self.handle,
+            cache_base=p(self.cache), cache_off_dev=p(self.cache_off), capacity_dev=p(self.cap_dev),
+            slot_limit=int(self.capacity.max()) if self.units else 0, scores=p(self.scores), sel_dev=p(self.sel),
+            slots_dev=p(self.slots), miss_dev=p(self.miss), sel_host=p(self.sel_h), slots_host=p(self.slots_h),
+            miss_host=p(self.miss_h), miss_cap=self.miss_cap, attn_ws=p(self.ws), attn_ws_bytes=self.ws_bytes)
+        self.last_n_miss = 0
+
+    def step(self, t, q, events=None):
+        self.last_n_miss = ss.ss_decode_layer(self.buffers, t, q, self.out, None, events)
+        return self.out
+
+    def close(self):
+        if self.handle:
+            ss.ss_cache_destroy(self.handle)
+            self.handle = None
+
+
+def cache_capacity(cfg, nblk):
+    """Slots per unit: floor(cache_frac * blocks of the sequence)."""
+    per_seq = np.floor(cfg.cache_frac * np.asarray(nblk, np.float64)).astype(np.int32)
+    return np.repeat(per_seq, cfg.Hkv)
+
+
+def pool_layout(cfg, nblk):
+    """Byte offsets of each unit's block array in a compact DRAM pool."""
+    per_unit = np.repeat(np.asarray(nblk, np.int64), cfg.Hkv) * cfg.record_bytes
+    off = np.concatenate([[0], np.cumsum(per_unit)[:-1]]).astype(np.int64)
+    return off, int(per_unit.sum())
+
+
+def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None):
+    """Draws one layer's KV per sequence on the GPU, builds its metadata in
+    HBM and copies the records into `pool` at pool_base_off.  Returns the
+    HierLayer (its pool offsets are relative to the pool base)."""
+    nblk = np.asarray(nblk, np.int32)
+    sK, sV = gen.channel_scales(cfg.Hkv, D, seed, layer, "cuda")
+    off, total = pool_layout(cfg, nblk)
+    off = off + pool_base_off
+    meta = torch.empty(cfg.B, cfg.Hkv, cfg.nblk_max, 2, D, dtype=torch.int16, device="cuda")
+    for b in range(cfg.B):
+        n = int(nblk[b])
+        if n == 0:
+            continue
+        rec, _ = gen.kv_records_seq(b, cfg.Hkv, n, cfg.blk, D, sK, sV, seed, layer, "cuda")
+        rec = rec.contiguous()
+        # metadata of this sequence, from the HBM copy of its records
+        unit_off = _dev(np.arange(cfg.Hkv, dtype=np.int64) * n * cfg.record_bytes, np.int64)
+        ss.ss_build_metadata(rec, unit_off, _dev([n], np.int32), 1, cfg.Hkv, cfg.nblk_max, cfg.blk, D, meta[b])
+        start = int(off[b * cfg.Hkv])
+        nbytes = cfg.Hkv * n * cfg.record_bytes
+        pool.t[start:start + nbytes].copy_(rec.view(torch.uint8).reshape(-1))
+        if progress and b % 16 == 15:
+            progress(f"layer {layer}: {b + 1}/{cfg.B} sequences in the DRAM pool")
+    torch.cuda.synchronize()
+    L = HierLayer(cfg, nblk, cache_capacity(cfg, nblk), pool, off, meta)
+    return L
+
+
+def query_stream(cfg, seed, layer, steps, device="cuda"):
+    """q for the warm-up step (index 0) and `steps` drifting steps after it."""
+    q32, q = gen.query(cfg.B, cfg.Hq, D, seed, device, layer)
+    qs = [(q32, q)]
+    for s in range(1, steps + 1):
+        q32, q = gen.drift(q32, cfg.drift, seed, layer, s)
+        qs.append((q32, q))
+    return qs
