@@ -1,0 +1,267 @@
+#!/usr/bin/env python3
+"""Sparse decode-step throughput on one MI355X.
+
+Default workload: the hierarchical 128k-context layer (B=64, 32 query / 8
+KV heads, head_dim 128, 8192 blocks of 16 tokens per sequence, top-k 128
+blocks, all KV in a pinned DRAM pool, an HBM block cache of 25% of each
+sequence's blocks, queries drifting 0.3 per step).  One step is the whole
+decode path of that layer: block scoring, top-k selection, the host-side
+cache resolve, the gather of missed blocks from DRAM and sparse attention.
+Inputs are resident (pool in pinned DRAM, metadata and cache in HBM) when
+timing starts; the warm-up step fills the cold cache.
+
+Prints one JSON line on stdout (progress goes to stderr):
+  value      = B * steps / wall time of the timed steps (tokens/s)
+  roofline   = the step's dominant kernel against its bound (HBM 8 TB/s, or
+               the PCIe 5.0 x16 host link at 63.0 GB/s per direction)
+  rooflines  = every kernel of the step, each with its algorithmic bytes
+  cpu_baseline = the CPU oracle on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0
+LINK_PEAK_GBS = 32.0 * 16 * 128 / 130 / 8  # PCIe 5.0 x16, one direction: 63.0 GB/s
+D = 128
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's)")
+    ap.add_argument("--warmup", type=int, default=1, help="untimed steps first (the first fills the cache)")
+    ap.add_argument("--config", default="2", help="workload index or name (see synth/configs.py)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seqs", type=int, default=16, help="sequences in the CPU-oracle sample")
+    ap.add_argument("--cpu-steps", type=int, default=8, help="timed steps in the CPU-oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--pool-flags", type=int, default=0, help="0 coherent, 1 non-coherent pinned pool")
+    return ap.parse_args()
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU: the decode path has no cross-GPU step (every (sequence, KV head) "
+              f"unit is independent); got --gpus {args.gpus}, WORLD_SIZE {world}.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import synth
+    from paper_2509_24626_amd import binding as ss
+    from paper_2509_24626_amd import harness as H
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    ss.lib()
+    cfg = synth.get(int(args.config)) if args.config.isdigit() else synth.get(args.config)
+    steps = args.steps if args.steps is not None else cfg.steps
+    warmup = max(args.warmup, 1)
+    if cfg.placement != "host":
+        print("bench.py times the hierarchical workloads (2, 3, 4); the all-HBM ones are parity cases",
+              file=sys.stderr)
+        sys.exit(2)
+
+    # ------------------------------------------------------------ setup
+    lens = synth.gen.lengths(cfg, args.seed)
+    nblk = (lens // cfg.blk).astype(np.int32)
+    _, per_layer = H.pool_layout(cfg, nblk)
+    total = per_layer * cfg.layers
+    log(f"workload {cfg.name}: {cfg.layers} layer(s), pool {total / 2**30:.2f} GiB pinned")
+    pool = H.HostPool(total, args.pool_flags)
+    layers, qstreams = [], []
+    meta_ms = []
+    for l in range(cfg.layers):
+        t0 = time.perf_counter()
+        L = H.build_hier_layer(cfg, args.seed, l, pool, l * per_layer, nblk, progress=log)
+        layers.append(L)
+        qstreams.append(H.query_stream(cfg, args.seed, l, warmup + steps - 1))
+    # metadata build (setup path), timed on its own for one layer
+    L0 = layers[0]
+    kv_one = torch.empty(cfg.Hkv * int(nblk[0]) * cfg.record_bytes, dtype=torch.uint8, device="cuda")
+    kv_one.copy_(pool.t[int(L0.pool_off_host[0]):int(L0.pool_off_host[0]) + kv_one.numel()])
+    off1 = torch.from_numpy(np.arange(cfg.Hkv, dtype=np.int64) * int(nblk[0]) * cfg.record_bytes).cuda()
+    n1 = torch.tensor([int(nblk[0])], dtype=torch.int32, device="cuda")
+    meta1 = torch.empty(cfg.Hkv, cfg.nblk_max, 2, D, dtype=torch.int16, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(3):
+        e0.record()
+        ss.ss_build_metadata(kv_one, off1, n1, 1, cfg.Hkv, cfg.nblk_max, cfg.blk, D, meta1)
+        e1.record()
+        torch.cuda.synchronize()
+        meta_ms.append(e0.elapsed_time(e1))
+    meta_bytes = cfg.Hkv * int(nblk[0]) * (cfg.blk * D * 2 + 2 * D * 2)
+    del kv_one
+
+    # ----------------------------------------------------------- warm-up
+    for s in range(warmup):
+        for l, L in enumerate(layers):
+            L.step(s, qstreams[l][s][1])
+    torch.cuda.synchronize()
+    log(f"warm-up done ({warmup} step(s)); timing {steps} step(s)")
+
+    # ------------------------------------------------------------ timed
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in layers] for _ in range(steps)]
+    for row in ev:  # create the underlying events before timing
+        for es in row:
+            for e in es:
+                e.record()
+    torch.cuda.synchronize()
+    n_miss = np.zeros((steps, len(layers)), np.int64)
+    valid_sel = []
+    t0 = time.perf_counter()
+    for i in range(steps):
+        s = warmup + i
+        for l, L in enumerate(layers):
+            L.step(s, qstreams[l][s][1], events=[e.cuda_event for e in ev[i][l]])
+            n_miss[i, l] = L.last_n_miss
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    for L in layers:
+        valid_sel.append(int((L.sel >= 0).sum().item()))
+
+    # ------------------------------------------------------- accounting
+    stage = {k: [] for k in ("score", "topk", "host", "gather", "attention")}
+    for i in range(steps):
+        for l in range(len(layers)):
+            e = ev[i][l]
+            stage["score"].append(e[0].elapsed_time(e[1]))
+            stage["topk"].append(e[1].elapsed_time(e[2]))
+            stage["host"].append(e[2].elapsed_time(e[3]))
+            stage["gather"].append(e[3].elapsed_time(e[4]))
+            stage["attention"].append(e[4].elapsed_time(e[5]))
+    avg = {k: float(np.mean(v)) for k, v in stage.items()}
+    units = cfg.B * cfg.Hkv
+    blocks = int(nblk.sum()) * cfg.Hkv
+    q_bytes = cfg.B * cfg.Hq * D * 2
+    algo = {
+        # metadata rows (lo, hi: 512 B per block) + fp32 scores written + q
+        "score": blocks * (2 * D * 2 + 4) + q_bytes,
+        # scores read + selection written
+        "topk": blocks * 4 + units * cfg.k * 4,
+        # missed block records over the host link (mean over the timed steps)
+        "gather": float(n_miss.mean()) * cfg.record_bytes,
+        # selected K and V records + q + fp32 output
+        "attention": float(np.mean(valid_sel)) * cfg.record_bytes + q_bytes + cfg.B * cfg.Hq * D * 4,
+    }
+    roof = {}
+    for k, bound, peak in (("score", "hbm", HBM_PEAK_GBS), ("topk", "hbm", HBM_PEAK_GBS),
+                           ("gather", "host-link", LINK_PEAK_GBS), ("attention", "hbm", HBM_PEAK_GBS)):
+        ach = algo[k] / (avg[k] * 1e-3) / 1e9 if avg[k] > 0 else 0.0
+        roof[k] = {"bound": bound, "achieved": round(ach, 2), "peak": round(peak, 2), "unit": "GB/s",
+                   "frac": round(ach / peak, 4), "bytes_per_launch": int(algo[k]), "ms_per_launch": round(avg[k], 4),
+                   "traffic": None}
+    dominant = max(("score", "topk", "gather", "attention"), key=lambda k: avg[k])
+    tokens = cfg.B * steps
+    value = tokens / wall
+    miss_rate = float(n_miss.mean()) / (units * cfg.k)
+
+    # ------------------------------------------------------ CPU baseline
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, pool, layers[0], qstreams[0], nblk, args, warmup)
+
+    result = {
+        "metric": "sparse decode-step tokens/sec at 1 GPU; % HBM roofline; gather host-link GB/s",
+        "value": round(value, 2),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": round(wall / steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "batch": cfg.B, "q_heads": cfg.Hq, "kv_heads": cfg.Hkv, "head_dim": D,
+                   "context": int(lens.max()), "block": cfg.blk, "topk_blocks": cfg.k, "cache_frac": cfg.cache_frac,
+                   "layers": cfg.layers, "drift": cfg.drift, "seed": args.seed},
+        "roofline": dict(kernel=dominant, **roof[dominant]),
+        "rooflines": roof,
+        "stages_ms": {k: round(v, 4) for k, v in avg.items()},
+        "miss_rate": round(miss_rate, 4),
+        "gather_GBps": roof["gather"]["achieved"],
+        "hbm_frac": {"score": roof["score"]["frac"], "attention": roof["attention"]["frac"]},
+        "metadata_build": {"ms": round(float(np.median(meta_ms)), 4), "bytes": meta_bytes,
+                           "GBps": round(meta_bytes / (np.median(meta_ms) * 1e-3) / 1e9, 1),
+                           "note": "setup path (when blocks fill), one sequence, not in the step"},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+    for L in layers:
+        L.close()
+    pool.close()
+
+
+def cpu_baseline(cfg, pool, L, qs, nblk, args, warmup):
+    """The oracle on the first `cpu_seqs` sequences of layer 0: its own
+    metadata (untimed), a cache-fill step (untimed), then `cpu_steps` timed
+    steps of score, select, LRU resolve, gather and attention, one thread
+    per sequence."""
+    import oracle
+    from synth import gen
+    O = oracle.Oracle()
+    nseq = min(args.cpu_seqs, cfg.B)
+    nsteps = min(args.cpu_steps, len(qs) - 1)
+    threads = min(16, os.cpu_count() or 1, nseq)
+    rb, Hkv = cfg.record_bytes, cfg.Hkv
+    qh = [gen.to_u16(qs[s][1]) for s in range(nsteps + 1)]
+    log(f"cpu baseline: oracle on {nseq} sequences x {nsteps} steps, {threads} threads")
+
+    def prepare(b):
+        units = np.arange(b * Hkv, (b + 1) * Hkv)
+        nb = nblk[b:b + 1]
+        meta = O.build_metadata(pool.host, L.pool_off_host[units], nb, 1, Hkv, cfg.nblk_max, cfg.blk, D)
+        cap = L.capacity[units]
+        lru = O.lru(1, Hkv, nb, cap)
+        img_off = np.concatenate([[0], np.cumsum(cap.astype(np.int64))[:-1]]) * rb
+        img = np.zeros(int(cap.sum()) * rb + rb, np.uint8)
+        state = dict(meta=meta, lru=lru, img=img, img_off=img_off, off=L.pool_off_host[units], nb=nb)
+        step(b, state, 0)
+        return state
+
+    def step(b, st, s):
+        q = qh[s][b:b + 1]
+        S = O.score(q, st["meta"], st["nb"], cfg.Hq, Hkv, cfg.nblk_max, D)
+        sel = O.select(S, st["nb"], cfg.k)
+        slots, miss = st["lru"].step(s, sel)
+        O.gather(miss, pool.host, st["off"], st["img"], st["img_off"], rb, Hkv)
+        O.attention(q, st["img"], st["img_off"], slots, Hkv, cfg.blk)
+
+    with ThreadPoolExecutor(threads) as ex:
+        states = list(ex.map(prepare, range(nseq)))
+        t0 = time.perf_counter()
+        list(ex.map(lambda b: [step(b, states[b], s) for s in range(1, nsteps + 1)], range(nseq)))
+        wall = time.perf_counter() - t0
+    cpu_model = ""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"value": round(nseq * nsteps / wall, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{nseq} of {cfg.B} sequences (all {Hkv} KV heads each) x {nsteps} decode steps of layer 0 "
+                      f"after an untimed cache-fill step; score, select, LRU resolve, gather, attention; "
+                      f"{wall:.2f} s wall, {threads} threads, one sequence per thread",
+            "cpu": cpu_model}
+
+
+if __name__ == "__main__":
+    main()

@@ -218,9 +218,9 @@ ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t 
  * slot_limit: the largest per-unit capacity (slots at or above it are never
  * read).  The cache regions of `cache` index cache_base through
  * cache_off_dev (= ss_cache_region_offsets, copied to the device).
- * events: NULL, or 5 hipEvent_t recorded on `stream` before scoring, after
- * selection, before the gather, after the gather and after attention (for
- * per-stage timing).
+ * events: NULL, or 6 hipEvent_t recorded on `stream` before scoring, after
+ * scoring, after selection, before the gather, after the gather and after
+ * attention (for per-stage timing).
  * On error nothing further is enqueued; a resolve error leaves the cache
  * unchanged. */
 typedef struct ss_layer_buffers {

@@ -205,12 +205,12 @@ def ss_sparse_attention(q, kv_base, region_off, slots, slot_limit, B, Hq, Hkv, d
 
 
 def ss_decode_layer(buffers, step, q, out, stream=None, events=None):
-    """buffers: an ss_layer_buffers; events: None or 5 raw hipEvent_t
+    """buffers: an ss_layer_buffers; events: None or 6 raw hipEvent_t
     handles.  Returns the number of blocks gathered."""
     n = ctypes.c_int64(0)
     ev = None
     if events is not None:
-        ev = (ctypes.c_void_p * 5)(*events)
+        ev = (ctypes.c_void_p * 6)(*events)
     _check(lib().ss_decode_layer(ctypes.byref(buffers), step, _ptr(q), _ptr(out), _stream(stream), ev,
                                  ctypes.byref(n)))
     return n.value

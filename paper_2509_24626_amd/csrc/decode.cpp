@@ -34,10 +34,12 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
     ss_status st;
 
     if ((st = record(events, 0, s))) return st;
-    st = ss_score_topk(q, L->meta, L->nblk_dev, L->B, L->Hq, L->Hkv, L->nblk_max, L->d, L->k, L->scores, L->sel_dev,
-                       stream);
+    st = ss_score_blocks(q, L->meta, L->nblk_dev, L->B, L->Hq, L->Hkv, L->nblk_max, L->d, L->scores, stream);
     if (st) return st;
     if ((st = record(events, 1, s))) return st;
+    st = ss_select_topk(L->scores, L->nblk_dev, L->B, L->Hkv, L->nblk_max, L->k, L->sel_dev, stream);
+    if (st) return st;
+    if ((st = record(events, 2, s))) return st;
     if ((st = hip_check(hipMemcpyAsync(L->sel_host, L->sel_dev, sel_bytes, hipMemcpyDeviceToHost, s), "copy sel")))
         return st;
     if ((st = hip_check(hipStreamSynchronize(s), "wait for the selection"))) return st;
@@ -53,15 +55,15 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
                                                  hipMemcpyHostToDevice, s),
                                   "copy miss list")))
         return st;
-    if ((st = record(events, 2, s))) return st;
+    if ((st = record(events, 3, s))) return st;
     st = ss_gather_blocks(L->miss_dev, nm, L->pool, L->pool_off_dev, L->cache_base, L->cache_off_dev, L->nblk_dev,
                           L->capacity_dev, L->B, L->Hkv, (size_t)2 * L->blk * L->d * 2, stream);
     if (st) return st;
-    if ((st = record(events, 3, s))) return st;
+    if ((st = record(events, 4, s))) return st;
     st = ss_sparse_attention(q, L->cache_base, L->cache_off_dev, L->slots_dev, L->slot_limit, L->B, L->Hq, L->Hkv,
                              L->d, L->blk, L->k, L->scale, out, L->attn_ws, L->attn_ws_bytes, stream);
     if (st) return st;
-    if ((st = record(events, 4, s))) return st;
+    if ((st = record(events, 5, s))) return st;
     *n_miss = nm;
     return SS_OK;
 }
