@@ -43,7 +43,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1, help="untimed steps first (the first fills the cache)")
     ap.add_argument("--config", default="2", help="workload index or name (see synth/configs.py)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--cpu-seqs", type=int, default=16, help="sequences in the CPU-oracle sample")
+    ap.add_argument("--parts", type=int, default=8, help="sequence groups pipelined within a layer step")
+    ap.add_argument("--cpu-seqs", type=int, default=64, help="sequences in the CPU-oracle sample")
     ap.add_argument("--cpu-steps", type=int, default=8, help="timed steps in the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pool-flags", type=int, default=0, help="0 coherent, 1 non-coherent pinned pool")
@@ -87,7 +88,7 @@ def main():
     meta_ms = []
     for l in range(cfg.layers):
         t0 = time.perf_counter()
-        L = H.build_hier_layer(cfg, args.seed, l, pool, l * per_layer, nblk, progress=log)
+        L = H.build_hier_layer(cfg, args.seed, l, pool, l * per_layer, nblk, progress=log, parts=args.parts)
         layers.append(L)
         qstreams.append(H.query_stream(cfg, args.seed, l, warmup + steps - 1))
     # metadata build (setup path), timed on its own for one layer
@@ -115,7 +116,8 @@ def main():
     log(f"warm-up done ({warmup} step(s)); timing {steps} step(s)")
 
     # ------------------------------------------------------------ timed
-    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in layers] for _ in range(steps)]
+    P = layers[0].parts
+    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(7 * P)] for _ in layers] for _ in range(steps)]
     for row in ev:  # create the underlying events before timing
         for es in row:
             for e in es:
@@ -135,29 +137,34 @@ def main():
         valid_sel.append(int((L.sel >= 0).sum().item()))
 
     # ------------------------------------------------------- accounting
-    stage = {k: [] for k in ("score", "topk", "host", "gather", "attention")}
+    # per launch (one per sequence group): score, top-k, gather, attention
+    stage = {k: [] for k in ("score", "topk", "gather", "attention")}
     for i in range(steps):
         for l in range(len(layers)):
             e = ev[i][l]
-            stage["score"].append(e[0].elapsed_time(e[1]))
-            stage["topk"].append(e[1].elapsed_time(e[2]))
-            stage["host"].append(e[2].elapsed_time(e[3]))
-            stage["gather"].append(e[3].elapsed_time(e[4]))
-            stage["attention"].append(e[4].elapsed_time(e[5]))
+            for p in range(P):
+                b = 7 * p
+                stage["score"].append(e[b + 0].elapsed_time(e[b + 1]))
+                stage["topk"].append(e[b + 1].elapsed_time(e[b + 2]))
+                stage["gather"].append(e[b + 3].elapsed_time(e[b + 4]))
+                stage["attention"].append(e[b + 5].elapsed_time(e[b + 6]))
     avg = {k: float(np.mean(v)) for k, v in stage.items()}
+    per_step_sum = {k: float(np.sum(v)) / steps for k, v in stage.items()}
     units = cfg.B * cfg.Hkv
     blocks = int(nblk.sum()) * cfg.Hkv
     q_bytes = cfg.B * cfg.Hq * D * 2
-    algo = {
+    step_bytes = {
         # metadata rows (lo, hi: 512 B per block) + fp32 scores written + q
-        "score": blocks * (2 * D * 2 + 4) + q_bytes,
+        "score": len(layers) * (blocks * (2 * D * 2 + 4) + q_bytes),
         # scores read + selection written
-        "topk": blocks * 4 + units * cfg.k * 4,
+        "topk": len(layers) * (blocks * 4 + units * cfg.k * 4),
         # missed block records over the host link (mean over the timed steps)
-        "gather": float(n_miss.mean()) * cfg.record_bytes,
+        "gather": float(n_miss.sum()) / steps * cfg.record_bytes,
         # selected K and V records + q + fp32 output
-        "attention": float(np.mean(valid_sel)) * cfg.record_bytes + q_bytes + cfg.B * cfg.Hq * D * 4,
+        "attention": float(np.sum(valid_sel)) * cfg.record_bytes + len(layers) * (q_bytes + cfg.B * cfg.Hq * D * 4),
     }
+    launches = len(layers) * P  # launches of each kernel per step
+    algo = {k: v / launches for k, v in step_bytes.items()}
     roof = {}
     for k, bound, peak in (("score", "hbm", HBM_PEAK_GBS), ("topk", "hbm", HBM_PEAK_GBS),
                            ("gather", "host-link", LINK_PEAK_GBS), ("attention", "hbm", HBM_PEAK_GBS)):
@@ -169,6 +176,7 @@ def main():
     tokens = cfg.B * steps
     value = tokens / wall
     miss_rate = float(n_miss.mean()) / (units * cfg.k)
+    log(f"{value:.0f} tokens/s, {wall / steps * 1e3:.3f} ms/step; kernel ms per step {per_step_sum}")
 
     # ------------------------------------------------------ CPU baseline
     cpu = None
@@ -193,7 +201,8 @@ def main():
                    "layers": cfg.layers, "drift": cfg.drift, "seed": args.seed},
         "roofline": dict(kernel=dominant, **roof[dominant]),
         "rooflines": roof,
-        "stages_ms": {k: round(v, 4) for k, v in avg.items()},
+        "kernel_ms_per_step": {k: round(v, 4) for k, v in per_step_sum.items()},
+        "parts": P,
         "miss_rate": round(miss_rate, 4),
         "gather_GBps": roof["gather"]["achieved"],
         "hbm_frac": {"score": roof["score"]["frac"], "attention": roof["attention"]["frac"]},

@@ -162,6 +162,12 @@ ss_status ss_cache_set_threads(ss_cache *cache, int n_threads);
  * SS_ERR_OOM if miss_cap rows are not enough. */
 ss_status ss_cache_resolve(ss_cache *cache, int64_t step, const int32_t *sel, int k, int32_t *slots,
                            int32_t *miss, int64_t miss_cap, int64_t *n_miss);
+/* ss_cache_resolve restricted to sequences [b_begin, b_end): sel and slots
+ * point at the rows of sequence b_begin ([b_end-b_begin][Hkv][k]); miss rows
+ * carry absolute (b, g).  Other sequences are untouched, so a step can be
+ * resolved in several calls over disjoint ranges with the same step number. */
+ss_status ss_cache_resolve_range(ss_cache *cache, int64_t step, int b_begin, int b_end, const int32_t *sel, int k,
+                                 int32_t *slots, int32_t *miss, int64_t miss_cap, int64_t *n_miss);
 /* State dump for tests: per slot (units in order) the block it holds (-1
  * empty) and its last use.  Arrays hold ss_cache_total_slots entries. */
 ss_status ss_cache_export(const ss_cache *cache, int32_t *slot_block, int64_t *slot_last);
@@ -206,23 +212,36 @@ ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t 
  * The decode step of one layer over the HBM/DRAM hierarchy (Section 3.1's
  * executor / cache-manager exchange): score and select on the GPU, copy the
  * selection to the host, resolve it in the block cache, copy slots and the
- * miss list back, gather the misses, attend.  The only host wait is for the
- * selection; everything after it is enqueued on `stream` and the call
- * returns without waiting for it.
+ * miss list back, gather the misses, attend.
+ * The batch is processed in `parts` consecutive sequence groups (1 <= parts
+ * <= B; 0 means 1) so that the host-link gather of one group overlaps the
+ * scoring and the host resolve of the next: scoring, selection and
+ * attention run on `stream`; the gathers run on a transfer stream the
+ * library creates for this cache handle on first use (default priority)
+ * and orders against `stream` with events.  Selections reach the host, and
+ * slots and miss rows reach the GPU, through the mapped host buffers (no
+ * copy-engine transfers).  The host waits only for each group's selection;
+ * everything after the last resolve is enqueued and the call returns
+ * without waiting.  Work enqueued later on `stream` is ordered after the
+ * whole step.
  * All pointers below are caller-owned.  Device buffers: scores fp32
  * [B][Hkv][nblk_max]; sel_dev and slots_dev int32 [B][Hkv][k]; miss_dev
- * int32 [miss_cap][4] (16-byte aligned); attn_ws of attn_ws_bytes >=
- * ss_sparse_attention_workspace(...).  Host buffers (pinned, for
- * asynchronous copies): sel_host, slots_host int32 [B][Hkv][k]; miss_host
- * int32 [miss_cap][4].  miss_cap >= B*Hkv*k always suffices.
+ * int32 [miss_cap][4] (16-byte aligned); attn_ws of attn_ws_bytes >= the
+ * largest ss_sparse_attention_workspace(...) of a group.  Host buffers
+ * (pinned, mapped, coherent: ss_host_alloc_mapped with flags 0): sel_host,
+ * slots_host int32 [B][Hkv][k]; miss_host int32 [miss_cap][4];
+ * miss_cap >= B*Hkv*k; SS_ERR_INVALID_ARG if they are not mapped.
  * slot_limit: the largest per-unit capacity (slots at or above it are never
- * read).  The cache regions of `cache` index cache_base through
- * cache_off_dev (= ss_cache_region_offsets, copied to the device).
- * events: NULL, or 6 hipEvent_t recorded on `stream` before scoring, after
- * scoring, after selection, before the gather, after the gather and after
- * attention (for per-stage timing).
+ * read).  cache_off_dev = ss_cache_region_offsets, copied to the device.
+ * After the call, miss_host rows [0, *n_miss) hold the step's misses in
+ * unit order (as one ss_cache_resolve would list them).
+ * events: NULL, or 7*parts hipEvent_t; for group p, events[7p+0..6] are
+ * recorded before scoring, after scoring, after selection (on `stream`),
+ * before and after the gather (transfer stream), before and after attention
+ * (on `stream`) -- per-kernel timing.
+ * Streams and events belong to the device current at the first call.
  * On error nothing further is enqueued; a resolve error leaves the cache
- * unchanged. */
+ * unchanged for the groups not yet resolved. */
 typedef struct ss_layer_buffers {
     int B, Hq, Hkv, d, blk, nblk_max, k;
     float scale;
@@ -241,6 +260,7 @@ typedef struct ss_layer_buffers {
     int64_t miss_cap;
     void *attn_ws;
     size_t attn_ws_bytes;
+    int parts;
 } ss_layer_buffers;
 
 ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, const void *q, float *out, void *stream,

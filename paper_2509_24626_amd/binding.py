@@ -40,7 +40,7 @@ class ss_layer_buffers(ctypes.Structure):
                 ("pool_off_dev", _vp), ("cache", _vp), ("cache_base", _vp), ("cache_off_dev", _vp),
                 ("capacity_dev", _vp), ("slot_limit", _i32), ("scores", _vp), ("sel_dev", _vp),
                 ("slots_dev", _vp), ("miss_dev", _vp), ("sel_host", _vp), ("slots_host", _vp),
-                ("miss_host", _vp), ("miss_cap", _i64), ("attn_ws", _vp), ("attn_ws_bytes", _sz)]
+                ("miss_host", _vp), ("miss_cap", _i64), ("attn_ws", _vp), ("attn_ws_bytes", _sz), ("parts", _i32)]
 
 _SIGNATURES = {
     "ss_abi_version": (_i32, []),
@@ -58,6 +58,7 @@ _SIGNATURES = {
     "ss_cache_region_offsets": (_i32, [_vp, _vp]),
     "ss_cache_set_threads": (_i32, [_vp, _i32]),
     "ss_cache_resolve": (_i32, [_vp, _i64, _vp, _i32, _vp, _vp, _i64, _vp]),
+    "ss_cache_resolve_range": (_i32, [_vp, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _i64, _vp]),
     "ss_cache_export": (_i32, [_vp, _vp, _vp]),
     "ss_gather_blocks": (_i32, [_vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _sz, _vp]),
     "ss_sparse_attention_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32]),
@@ -184,6 +185,14 @@ def ss_cache_resolve(handle, step, sel, k, slots, miss, miss_cap):
     return n.value
 
 
+def ss_cache_resolve_range(handle, step, b_begin, b_end, sel, k, slots, miss, miss_cap):
+    """Host arrays holding the rows of sequences [b_begin, b_end); returns the miss rows written."""
+    n = ctypes.c_int64(0)
+    _check(lib().ss_cache_resolve_range(handle, step, b_begin, b_end, _ptr(sel), k, _ptr(slots), _ptr(miss),
+                                        miss_cap, ctypes.byref(n)))
+    return n.value
+
+
 def ss_cache_export(handle, slot_block, slot_last):
     _check(lib().ss_cache_export(handle, _ptr(slot_block), _ptr(slot_last)))
 
@@ -205,12 +214,12 @@ def ss_sparse_attention(q, kv_base, region_off, slots, slot_limit, B, Hq, Hkv, d
 
 
 def ss_decode_layer(buffers, step, q, out, stream=None, events=None):
-    """buffers: an ss_layer_buffers; events: None or 6 raw hipEvent_t
+    """buffers: an ss_layer_buffers; events: None or 7*parts raw hipEvent_t
     handles.  Returns the number of blocks gathered."""
     n = ctypes.c_int64(0)
     ev = None
     if events is not None:
-        ev = (ctypes.c_void_p * 6)(*events)
+        ev = (ctypes.c_void_p * len(events))(*events)
     _check(lib().ss_decode_layer(ctypes.byref(buffers), step, _ptr(q), _ptr(out), _stream(stream), ev,
                                  ctypes.byref(n)))
     return n.value

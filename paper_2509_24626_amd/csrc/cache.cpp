@@ -146,7 +146,24 @@ struct ss_cache {
     int threads = 1;                          // workers used by resolve
     std::vector<std::vector<uint64_t>> mark;  // per worker: slot bitmap for ordering
     std::vector<std::vector<int32_t>> touched;  // per worker
+    void *exec = nullptr;                       // GPU-side step state (decode.cpp)
+    void (*exec_free)(void *) = nullptr;
+    ~ss_cache()
+    {
+        if (exec && exec_free) exec_free(exec);
+    }
 };
+
+namespace ss {
+void *cache_exec(ss_cache *c) { return c->exec; }
+void cache_set_exec(ss_cache *c, void *exec, void (*exec_free)(void *))
+{
+    c->exec = exec;
+    c->exec_free = exec_free;
+}
+int cache_batch(const ss_cache *c) { return c->B; }
+int cache_kv_heads(const ss_cache *c) { return c->Hkv; }
+}  // namespace ss
 
 namespace {
 
@@ -328,9 +345,19 @@ ss_status ss_cache_set_threads(ss_cache *c, int n)
 ss_status ss_cache_resolve(ss_cache *c, int64_t step, const int32_t *sel, int k, int32_t *slots, int32_t *miss,
                            int64_t miss_cap, int64_t *n_miss)
 {
+    SS_CHECK_ARG(c, "ss_cache_resolve: null cache");
+    return ss_cache_resolve_range(c, step, 0, c->B, sel, k, slots, miss, miss_cap, n_miss);
+}
+
+ss_status ss_cache_resolve_range(ss_cache *c, int64_t step, int b_begin, int b_end, const int32_t *sel, int k,
+                                 int32_t *slots, int32_t *miss, int64_t miss_cap, int64_t *n_miss)
+{
     SS_CHECK_ARG(c && n_miss && k > 0 && miss_cap >= 0, "ss_cache_resolve: bad argument");
+    SS_CHECK_ARG(0 <= b_begin && b_begin <= b_end && b_end <= c->B, "ss_cache_resolve: sequence range [%d, %d) "
+                 "outside [0, %d)", b_begin, b_end, c->B);
     *n_miss = 0;
-    const int units = (int)c->units.size();
+    const int u0 = b_begin * c->Hkv;
+    const int units = (b_end - b_begin) * c->Hkv;
     if (units == 0) return SS_OK;
     SS_CHECK_ARG(sel && slots && (miss || miss_cap == 0), "ss_cache_resolve: null pointer");
     SS_CHECK_ARG(step >= c->last_step, "ss_cache_resolve: step %lld precedes the previous step %lld",
@@ -351,9 +378,10 @@ ss_status ss_cache_resolve(ss_cache *c, int64_t step, const int32_t *sel, int k,
     workers.run([&](int w) {
         if (w >= nt) return;
         const int lo = (int)((int64_t)units * w / nt), hi = (int)((int64_t)units * (w + 1) / nt);
-        for (int u = lo; u < hi; ++u) {
+        for (int i = lo; i < hi; ++i) {
+            const int u = u0 + i;
             const unit_state &st = c->units[u];
-            const int32_t *su = sel + (int64_t)u * k;
+            const int32_t *su = sel + (int64_t)i * k;
             const int cnt = check_unit(st, su, k);
             if (cnt < 0) {
                 int expect = -1;
@@ -363,8 +391,8 @@ ss_status ss_cache_resolve(ss_cache *c, int64_t step, const int32_t *sel, int k,
             }
             const int32_t *bs = c->block_slot.data() + st.block_base;
             int64_t m = 0;
-            for (int i = 0; i < k; ++i)
-                if (su[i] >= 0 && bs[su[i]] < 0) ++m;
+            for (int e = 0; e < k; ++e)
+                if (su[e] >= 0 && bs[su[e]] < 0) ++m;
             c->miss_count[u] = m;
         }
     });
@@ -377,7 +405,7 @@ ss_status ss_cache_resolve(ss_cache *c, int64_t step, const int32_t *sel, int k,
                         "ss_cache_resolve: unit %d selection is not strictly ascending in [0, nblk) then -1", u);
     }
     int64_t total = 0;
-    for (int u = 0; u < units; ++u) {
+    for (int u = u0; u < u0 + units; ++u) {
         const int64_t m = c->miss_count[u];
         c->miss_count[u] = total;  // becomes the unit's first output row
         total += m;
@@ -390,9 +418,11 @@ ss_status ss_cache_resolve(ss_cache *c, int64_t step, const int32_t *sel, int k,
     workers.run([&](int w) {
         if (w >= nt) return;
         const int lo = (int)((int64_t)units * w / nt), hi = (int)((int64_t)units * (w + 1) / nt);
-        for (int u = lo; u < hi; ++u)
-            resolve_unit(c, w, u, step, sel + (int64_t)u * k, k, slots + (int64_t)u * k, miss + 4 * c->miss_count[u],
+        for (int i = lo; i < hi; ++i) {
+            const int u = u0 + i;
+            resolve_unit(c, w, u, step, sel + (int64_t)i * k, k, slots + (int64_t)i * k, miss + 4 * c->miss_count[u],
                          u / c->Hkv, u % c->Hkv);
+        }
     });
     c->last_step = step;
     *n_miss = total;

@@ -3,9 +3,72 @@
 // which resolves them against the HBM block cache and loads the misses
 // from DRAM in one fused gather (Section 3.1, Section 3.2.1); attention
 // then reads only HBM.
+//
+// The batch runs as a pipeline over sequence groups.  Scoring and
+// selection of every group are enqueued up front on the caller's stream;
+// the top-k kernel writes each selection both to HBM and straight into
+// pinned, mapped host memory.  The host then takes the groups in order:
+// wait for the group's selection, resolve it, and enqueue its gather on the
+// transfer stream (the kernel reads the miss rows from mapped host memory
+// and also copies the group's slot table to HBM) and its attention on the
+// caller's stream behind that gather.  So the host-link transfer of group p
+// overlaps the resolve of group p+1 and the scoring still in flight, and
+// attention of group p overlaps the gather of group p+1.  Every hand-off is
+// a kernel on a compute queue: no copy-engine transfer, whose cross-engine
+// synchronisation costs tens of microseconds per hand-off, is on the path.
+#include <thread>
+#include <vector>
+
 #include "internal.hpp"
 
+namespace ss {
+ss_status launch_topk(const float *scores, const int32_t *nblk, int B, int Hkv, int nblk_max, int k, int32_t *sel,
+                      int32_t *mirror, hipStream_t s);
+ss_status launch_gather(const int32_t *miss, int64_t n_miss, const void *pool_base, const int64_t *pool_off,
+                        void *cache_base, const int64_t *cache_off, const int32_t *nblk, const int32_t *capacity,
+                        int B, int Hkv, size_t record_bytes, const int32_t *copy_src, int32_t *copy_dst,
+                        int64_t copy_n, hipStream_t s);
+void *cache_exec(ss_cache *c);
+void cache_set_exec(ss_cache *c, void *exec, void (*exec_free)(void *));
+int cache_batch(const ss_cache *c);
+int cache_kv_heads(const ss_cache *c);
+}  // namespace ss
+
 namespace {
+
+struct exec_state {
+    hipStream_t xfer = nullptr;
+    hipEvent_t start = nullptr;
+    std::vector<hipEvent_t> sel_ready, gathered;
+    // device addresses of the caller's pinned host buffers (looked up once)
+    const void *host_key[3] = {nullptr, nullptr, nullptr};
+    void *host_dev[3] = {nullptr, nullptr, nullptr};
+};
+
+ss_status device_address(exec_state *e, int i, void *host, void **dev)
+{
+    if (e->host_key[i] != host) {
+        void *d = nullptr;
+        if (hipHostGetDevicePointer(&d, host, 0) != hipSuccess || !d) {
+            (void)hipGetLastError();
+            return ss::fail(SS_ERR_INVALID_ARG, "ss_decode_layer: host buffer %d is not pinned, mapped memory", i);
+        }
+        e->host_key[i] = host;
+        e->host_dev[i] = d;
+    }
+    *dev = e->host_dev[i];
+    return SS_OK;
+}
+
+void exec_free(void *p)
+{
+    exec_state *e = static_cast<exec_state *>(p);
+    for (hipEvent_t ev : e->sel_ready) (void)hipEventDestroy(ev);
+    for (hipEvent_t ev : e->gathered) (void)hipEventDestroy(ev);
+    if (e->start) (void)hipEventDestroy(e->start);
+    if (e->xfer) (void)hipStreamDestroy(e->xfer);
+    delete e;
+}
 
 ss_status hip_check(hipError_t e, const char *what)
 {
@@ -13,10 +76,47 @@ ss_status hip_check(hipError_t e, const char *what)
     return SS_OK;
 }
 
+ss_status get_exec(ss_cache *c, int parts, exec_state **out)
+{
+    exec_state *e = static_cast<exec_state *>(ss::cache_exec(c));
+    ss_status st;
+    if (!e) {
+        e = new exec_state;
+        if ((st = hip_check(hipStreamCreateWithFlags(&e->xfer, hipStreamNonBlocking), "create transfer stream")) ||
+            (st = hip_check(hipEventCreateWithFlags(&e->start, hipEventDisableTiming), "create event"))) {
+            exec_free(e);
+            return st;
+        }
+        ss::cache_set_exec(c, e, exec_free);
+    }
+    while ((int)e->sel_ready.size() < parts) {
+        hipEvent_t a = nullptr, b = nullptr;
+        if ((st = hip_check(hipEventCreateWithFlags(&a, hipEventDisableTiming), "create event"))) return st;
+        if ((st = hip_check(hipEventCreateWithFlags(&b, hipEventDisableTiming), "create event"))) {
+            (void)hipEventDestroy(a);
+            return st;
+        }
+        e->sel_ready.push_back(a);
+        e->gathered.push_back(b);
+    }
+    *out = e;
+    return SS_OK;
+}
+
+ss_status wait_host(hipEvent_t ev)
+{
+    for (;;) {
+        hipError_t r = hipEventQuery(ev);
+        if (r == hipSuccess) return SS_OK;
+        if (r != hipErrorNotReady) return hip_check(r, "wait for a selection");
+        std::this_thread::yield();
+    }
+}
+
 ss_status record(void *const *events, int i, hipStream_t s)
 {
     if (!events || !events[i]) return SS_OK;
-    return hip_check(hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), s), "hipEventRecord");
+    return hip_check(hipEventRecord(reinterpret_cast<hipEvent_t>(events[i]), s), "record timing event");
 }
 
 }  // namespace
@@ -26,44 +126,82 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
 {
     SS_CHECK_ARG(L && q && out && n_miss, "ss_decode_layer: null argument");
     SS_CHECK_ARG(L->cache && L->sel_host && L->slots_host && L->miss_host && L->sel_dev && L->slots_dev &&
-                     L->miss_dev,
+                     L->miss_dev && L->scores && L->meta && L->nblk_dev,
                  "ss_decode_layer: null buffer");
+    SS_CHECK_ARG(L->B == ss::cache_batch(L->cache) && L->Hkv == ss::cache_kv_heads(L->cache),
+                 "ss_decode_layer: shape differs from the cache handle's");
     *n_miss = 0;
-    hipStream_t s = ss::as_stream(stream);
-    const size_t sel_bytes = (size_t)L->B * L->Hkv * L->k * sizeof(int32_t);
-    ss_status st;
+    const int B = L->B, Hkv = L->Hkv, Hq = L->Hq, k = L->k, d = L->d;
+    if (B == 0) return SS_OK;
+    SS_CHECK_ARG(k > 0, "ss_decode_layer: k=%d", k);
+    const int64_t rows_per_seq = (int64_t)Hkv * k;
+    SS_CHECK_ARG(L->miss_cap >= (int64_t)B * rows_per_seq, "ss_decode_layer: miss_cap %lld < B*Hkv*k",
+                 (long long)L->miss_cap);
+    int P = L->parts < 1 ? 1 : (L->parts > B ? B : L->parts);
+    exec_state *ex = nullptr;
+    ss_status st = get_exec(L->cache, P, &ex);
+    if (st) return st;
+    hipStream_t s = ss::as_stream(stream), x = ex->xfer;
+    const size_t rec = (size_t)2 * L->blk * d * 2;
+    const char *q8 = static_cast<const char *>(q);
+    const char *meta8 = static_cast<const char *>(L->meta);
+    auto b_of = [&](int p) { return (int)((int64_t)B * p / P); };
 
-    if ((st = record(events, 0, s))) return st;
-    st = ss_score_blocks(q, L->meta, L->nblk_dev, L->B, L->Hq, L->Hkv, L->nblk_max, L->d, L->scores, stream);
-    if (st) return st;
-    if ((st = record(events, 1, s))) return st;
-    st = ss_select_topk(L->scores, L->nblk_dev, L->B, L->Hkv, L->nblk_max, L->k, L->sel_dev, stream);
-    if (st) return st;
-    if ((st = record(events, 2, s))) return st;
-    if ((st = hip_check(hipMemcpyAsync(L->sel_host, L->sel_dev, sel_bytes, hipMemcpyDeviceToHost, s), "copy sel")))
+    int32_t *sel_hd = nullptr, *slots_hd = nullptr, *miss_hd = nullptr;  // device views of the host buffers
+    if ((st = device_address(ex, 0, L->sel_host, (void **)&sel_hd)) ||
+        (st = device_address(ex, 1, L->slots_host, (void **)&slots_hd)) ||
+        (st = device_address(ex, 2, L->miss_host, (void **)&miss_hd)))
         return st;
-    if ((st = hip_check(hipStreamSynchronize(s), "wait for the selection"))) return st;
 
-    int64_t nm = 0;
-    st = ss_cache_resolve(L->cache, step, L->sel_host, L->k, L->slots_host, L->miss_host, L->miss_cap, &nm);
-    if (st) return st;
+    // the transfer stream starts after everything already on `stream`
+    if ((st = hip_check(hipEventRecord(ex->start, s), "record")) ||
+        (st = hip_check(hipStreamWaitEvent(x, ex->start, 0), "order transfer stream")))
+        return st;
 
-    if ((st = hip_check(hipMemcpyAsync(L->slots_dev, L->slots_host, sel_bytes, hipMemcpyHostToDevice, s),
-                        "copy slots")))
-        return st;
-    if (nm > 0 && (st = hip_check(hipMemcpyAsync(L->miss_dev, L->miss_host, (size_t)nm * 4 * sizeof(int32_t),
-                                                 hipMemcpyHostToDevice, s),
-                                  "copy miss list")))
-        return st;
-    if ((st = record(events, 3, s))) return st;
-    st = ss_gather_blocks(L->miss_dev, nm, L->pool, L->pool_off_dev, L->cache_base, L->cache_off_dev, L->nblk_dev,
-                          L->capacity_dev, L->B, L->Hkv, (size_t)2 * L->blk * L->d * 2, stream);
-    if (st) return st;
-    if ((st = record(events, 4, s))) return st;
-    st = ss_sparse_attention(q, L->cache_base, L->cache_off_dev, L->slots_dev, L->slot_limit, L->B, L->Hq, L->Hkv,
-                             L->d, L->blk, L->k, L->scale, out, L->attn_ws, L->attn_ws_bytes, stream);
-    if (st) return st;
-    if ((st = record(events, 5, s))) return st;
-    *n_miss = nm;
+    // scoring and selection of every group; selections land in HBM and host memory
+    for (int p = 0; p < P; ++p) {
+        const int b0 = b_of(p), Bp = b_of(p + 1) - b0;
+        if ((st = record(events, 7 * p + 0, s))) return st;
+        st = ss_score_blocks(q8 + (size_t)b0 * Hq * d * 2, meta8 + (size_t)b0 * Hkv * L->nblk_max * 2 * d * 2,
+                             L->nblk_dev + b0, Bp, Hq, Hkv, L->nblk_max, d, L->scores + (size_t)b0 * Hkv * L->nblk_max,
+                             stream);
+        if (st) return st;
+        if ((st = record(events, 7 * p + 1, s))) return st;
+        st = ss::launch_topk(L->scores + (size_t)b0 * Hkv * L->nblk_max, L->nblk_dev + b0, Bp, Hkv, L->nblk_max, k,
+                             L->sel_dev + b0 * rows_per_seq, sel_hd + b0 * rows_per_seq, s);
+        if (st) return st;
+        if ((st = record(events, 7 * p + 2, s))) return st;
+        if ((st = hip_check(hipEventRecord(ex->sel_ready[p], s), "record"))) return st;
+    }
+
+    // resolve group by group; gather on the transfer stream, attend behind it
+    int64_t total = 0;
+    for (int p = 0; p < P; ++p) {
+        const int b0 = b_of(p), b1 = b_of(p + 1), Bp = b1 - b0;
+        const int64_t row0 = b0 * rows_per_seq;
+        if ((st = wait_host(ex->sel_ready[p]))) return st;
+        // miss rows of the step are kept compact: this group appends at `total`
+        int64_t np = 0;
+        st = ss_cache_resolve_range(L->cache, step, b0, b1, L->sel_host + row0, k, L->slots_host + row0,
+                                    L->miss_host + 4 * total, L->miss_cap - total, &np);
+        if (st) return st;
+        if ((st = record(events, 7 * p + 3, x))) return st;
+        st = ss::launch_gather(miss_hd + 4 * total, np, L->pool, L->pool_off_dev, L->cache_base, L->cache_off_dev,
+                               L->nblk_dev, L->capacity_dev, B, Hkv, rec, slots_hd + row0, L->slots_dev + row0,
+                               (int64_t)Bp * rows_per_seq, x);
+        if (st) return st;
+        if ((st = record(events, 7 * p + 4, x))) return st;
+        if ((st = hip_check(hipEventRecord(ex->gathered[p], x), "record")) ||
+            (st = hip_check(hipStreamWaitEvent(s, ex->gathered[p], 0), "order attention after gather")))
+            return st;
+        if ((st = record(events, 7 * p + 5, s))) return st;
+        st = ss_sparse_attention(q8 + (size_t)b0 * Hq * d * 2, L->cache_base, L->cache_off_dev + b0 * Hkv,
+                                 L->slots_dev + row0, L->slot_limit, Bp, Hq, Hkv, d, L->blk, k, L->scale,
+                                 out + (size_t)b0 * Hq * d, L->attn_ws, L->attn_ws_bytes, stream);
+        if (st) return st;
+        if ((st = record(events, 7 * p + 6, s))) return st;
+        total += np;
+    }
+    *n_miss = total;
     return SS_OK;
 }

@@ -53,7 +53,8 @@ struct block_scan {
 
 template <int NT, int R>
 __global__ __launch_bounds__(NT) void topk_kernel(const float *__restrict__ scores, const int32_t *__restrict__ nblk,
-                                                  int Hkv, int nblk_max, int k, int32_t *__restrict__ sel)
+                                                  int Hkv, int nblk_max, int k, int32_t *__restrict__ sel,
+                                                  int32_t *__restrict__ mirror)
 {
     __shared__ int hist[256];
     __shared__ int wave_tot[NT / 64];
@@ -66,11 +67,15 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float *__restrict__ scor
     n = n < 0 ? 0 : (n > nblk_max ? nblk_max : n);
     const int m = k < n ? k : n;
     int32_t *out = sel + (int64_t)u * k;
+    int32_t *out2 = mirror ? mirror + (int64_t)u * k : nullptr;  // copy in mapped host memory
     const float *s = scores + (int64_t)u * nblk_max;
     const int t = threadIdx.x;
     const int lane = t & 63, wave = t >> 6;
 
-    for (int i = m + t; i < k; i += NT) out[i] = -1;
+    for (int i = m + t; i < k; i += NT) {
+        out[i] = -1;
+        if (out2) out2[i] = -1;
+    }
     if (m == 0) return;
 
     uint32_t key[R];
@@ -177,32 +182,37 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float *__restrict__ scor
         const bool eq = key[r] == T && base + r < n;
         const bool take = key[r] > T || (eq && eq_quota > 0);
         if (eq && eq_quota > 0) --eq_quota;
-        if (take && pos < m) out[pos++] = base + r;  // pos < m always holds; the guard keeps writes in range
+        if (take && pos < m) {  // pos < m always holds; the guard keeps writes in range
+            out[pos] = base + r;
+            if (out2) out2[pos] = base + r;
+            ++pos;
+        }
     }
 }
 
 template <int NT, int R>
 void launch(const float *scores, const int32_t *nblk, int units, int Hkv, int nblk_max, int k, int32_t *sel,
-            hipStream_t s)
+            int32_t *mirror, hipStream_t s)
 {
-    topk_kernel<NT, R><<<dim3(units), dim3(NT), 0, s>>>(scores, nblk, Hkv, nblk_max, k, sel);
+    topk_kernel<NT, R><<<dim3(units), dim3(NT), 0, s>>>(scores, nblk, Hkv, nblk_max, k, sel, mirror);
 }
 
 }  // namespace
 
 namespace ss {
 
+// `mirror` (nullable): a second copy of the selection, e.g. in mapped host memory
 ss_status launch_topk(const float *scores, const int32_t *nblk, int B, int Hkv, int nblk_max, int k, int32_t *sel,
-                      hipStream_t s)
+                      int32_t *mirror, hipStream_t s)
 {
     const int units = B * Hkv;
     if (units == 0) return SS_OK;
-    if (nblk_max <= 256 * 4) launch<256, 4>(scores, nblk, units, Hkv, nblk_max, k, sel, s);
-    else if (nblk_max <= 256 * 8) launch<256, 8>(scores, nblk, units, Hkv, nblk_max, k, sel, s);
-    else if (nblk_max <= 256 * 16) launch<256, 16>(scores, nblk, units, Hkv, nblk_max, k, sel, s);
-    else if (nblk_max <= 256 * 32) launch<256, 32>(scores, nblk, units, Hkv, nblk_max, k, sel, s);
-    else if (nblk_max <= 512 * 32) launch<512, 32>(scores, nblk, units, Hkv, nblk_max, k, sel, s);
-    else launch<1024, 64>(scores, nblk, units, Hkv, nblk_max, k, sel, s);
+    if (nblk_max <= 256 * 4) launch<256, 4>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 256 * 8) launch<256, 8>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 256 * 16) launch<256, 16>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 256 * 32) launch<256, 32>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 512 * 32) launch<512, 32>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else launch<1024, 64>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
     return check_launch("ss_select_topk");
 }
 
@@ -221,7 +231,7 @@ extern "C" ss_status ss_select_topk(const float *scores, const int32_t *nblk, in
     SS_CHECK_SUPPORTED(nblk_max <= ss::kMaxBlocks, "ss_select_topk: nblk_max=%d > %d", nblk_max, ss::kMaxBlocks);
     if (B == 0) return SS_OK;
     SS_CHECK_ARG(nblk && sel && (scores || nblk_max == 0), "ss_select_topk: null pointer");
-    return ss::launch_topk(scores, nblk, B, Hkv, nblk_max, k, sel, ss::as_stream(stream));
+    return ss::launch_topk(scores, nblk, B, Hkv, nblk_max, k, sel, nullptr, ss::as_stream(stream));
 }
 
 extern "C" ss_status ss_score_topk(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv,
@@ -235,5 +245,5 @@ extern "C" ss_status ss_score_topk(const void *q, const void *meta, const int32_
     hipStream_t s = ss::as_stream(stream);
     st = ss::launch_score(q, meta, nblk, B, Hq, Hkv, nblk_max, scores, s);
     if (st != SS_OK) return st;
-    return ss::launch_topk(scores, nblk, B, Hkv, nblk_max, k, sel, s);
+    return ss::launch_topk(scores, nblk, B, Hkv, nblk_max, k, sel, nullptr, s);
 }

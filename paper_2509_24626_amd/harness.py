@@ -103,8 +103,9 @@ class HierLayer:
     """One layer of the hierarchical workload: its DRAM pool slice, HBM
     metadata, HBM block cache and step buffers."""
 
-    def __init__(self, cfg, nblk_host, capacity, pool, pool_off_host, meta):
+    def __init__(self, cfg, nblk_host, capacity, pool, pool_off_host, meta, parts=1):
         self.cfg = cfg
+        self.parts = max(1, min(parts, cfg.B))
         B, Hkv, k = cfg.B, cfg.Hkv, cfg.k
         self.units = B * Hkv
         self.nblk_host = np.asarray(nblk_host, np.int32)
@@ -127,11 +128,16 @@ class HierLayer:
         self.slots = torch.empty(B, Hkv, k, dtype=torch.int32, device="cuda")
         self.miss_cap = self.units * k
         self.miss = torch.empty(self.miss_cap, 4, dtype=torch.int32, device="cuda")
-        self.sel_h = torch.empty(B, Hkv, k, dtype=torch.int32, pin_memory=True)
-        self.slots_h = torch.empty(B, Hkv, k, dtype=torch.int32, pin_memory=True)
-        self.miss_h = torch.empty(self.miss_cap, 4, dtype=torch.int32, pin_memory=True)
+        # pinned, mapped, coherent host buffers the kernels read and write directly
+        self._staging = HostPool(max(1, (2 * self.units * k + 4 * self.miss_cap) * 4))
+        st = self._staging.t.view(torch.int32)
+        self.sel_h = st[:self.units * k].view(B, Hkv, k)
+        self.slots_h = st[self.units * k:2 * self.units * k].view(B, Hkv, k)
+        self.miss_h = st[2 * self.units * k:2 * self.units * k + 4 * self.miss_cap].view(self.miss_cap, 4)
         self.out = torch.empty(B, cfg.Hq, D, dtype=torch.float32, device="cuda")
-        self.ws_bytes = ss.ss_sparse_attention_workspace(B, cfg.Hq, Hkv, D, cfg.blk, k)
+        # attention runs per sequence group; one workspace serves the groups in turn
+        sizes = {B * (i + 1) // self.parts - B * i // self.parts for i in range(self.parts)}
+        self.ws_bytes = max(ss.ss_sparse_attention_workspace(b, cfg.Hq, Hkv, D, cfg.blk, k) for b in sizes)
         self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device="cuda")
         p = ss._ptr
         self.buffers = ss.ss_layer_buffers(
@@ -140,7 +146,8 @@ class HierLayer:
             cache_base=p(self.cache), cache_off_dev=p(self.cache_off), capacity_dev=p(self.cap_dev),
             slot_limit=int(self.capacity.max()) if self.units else 0, scores=p(self.scores), sel_dev=p(self.sel),
             slots_dev=p(self.slots), miss_dev=p(self.miss), sel_host=p(self.sel_h), slots_host=p(self.slots_h),
-            miss_host=p(self.miss_h), miss_cap=self.miss_cap, attn_ws=p(self.ws), attn_ws_bytes=self.ws_bytes)
+            miss_host=p(self.miss_h), miss_cap=self.miss_cap, attn_ws=p(self.ws), attn_ws_bytes=self.ws_bytes,
+            parts=self.parts)
         self.last_n_miss = 0
 
     def step(self, t, q, events=None):
@@ -151,6 +158,10 @@ class HierLayer:
         if self.handle:
             ss.ss_cache_destroy(self.handle)
             self.handle = None
+        if self._staging is not None:
+            self.sel_h = self.slots_h = self.miss_h = None
+            self._staging.close()
+            self._staging = None
 
 
 def cache_capacity(cfg, nblk):
@@ -166,7 +177,7 @@ def pool_layout(cfg, nblk):
     return off, int(per_unit.sum())
 
 
-def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None):
+def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None, parts=1):
     """Draws one layer's KV per sequence on the GPU, builds its metadata in
     HBM and copies the records into `pool` at pool_base_off.  Returns the
     HierLayer (its pool offsets are relative to the pool base)."""
@@ -190,7 +201,7 @@ def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None)
         if progress and b % 16 == 15:
             progress(f"layer {layer}: {b + 1}/{cfg.B} sequences in the DRAM pool")
     torch.cuda.synchronize()
-    L = HierLayer(cfg, nblk, cache_capacity(cfg, nblk), pool, off, meta)
+    L = HierLayer(cfg, nblk, cache_capacity(cfg, nblk), pool, off, meta, parts)
     return L
 
 

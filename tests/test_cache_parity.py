@@ -140,3 +140,37 @@ def test_region_offsets():
     ss.ss_cache_region_offsets(c.h, off)
     assert off.tolist() == [0, 3 * 4096, 3 * 4096, 8 * 4096]
     assert ss.ss_cache_total_slots(c.h) == 9
+
+
+@pytest.mark.parametrize("cuts", [[0, 3], [0, 1, 3], [0, 1, 2, 3], [0, 0, 2, 3]])
+def test_resolve_in_ranges_equals_whole(oracle_impl, cuts):
+    """A step resolved as several disjoint sequence ranges (same step
+    number) gives exactly the whole-batch result, step after step."""
+    nblk = [64, 40, 97]
+    Hkv, k = 2, 10
+    cap = np.array([[16, 12], [13, 20], [25, 14]], np.int32)
+    stream = synth.gen.selection_stream(nblk, Hkv, k, 12, 0.4, 23)
+    lib = LibCache(3, Hkv, nblk, cap)
+    ora = oracle_impl.lru(3, Hkv, nblk, cap)
+    for t in range(12):
+        sel = stream[t]
+        slots = np.empty_like(sel)
+        miss_all = []
+        for b0, b1 in zip(cuts[:-1], cuts[1:]):
+            rows = (b1 - b0) * Hkv * k
+            miss = np.empty((max(rows, 1), 4), np.int32)
+            n = ss.ss_cache_resolve_range(lib.h, t, b0, b1, np.ascontiguousarray(sel[b0:b1]), k,
+                                          slots[b0:b1], miss, rows)
+            miss_all.append(miss[:n])
+        os_, om = ora.step(t, sel)
+        np.testing.assert_array_equal(slots, os_)
+        np.testing.assert_array_equal(np.concatenate(miss_all), om)
+
+
+def test_resolve_range_rejects_bad_range():
+    c = LibCache(2, 1, [10, 10], [[4], [4]])
+    sel = np.zeros((1, 1, 2), np.int32)
+    for b0, b1 in [(-1, 1), (1, 0), (0, 3)]:
+        with pytest.raises(ss.SparseServeError) as e:
+            ss.ss_cache_resolve_range(c.h, 0, b0, b1, sel, 2, np.empty_like(sel), np.empty((4, 4), np.int32), 4)
+        assert e.value.status == ss.SS_ERR_INVALID_ARG

@@ -32,15 +32,17 @@ def ss():
     return binding
 
 
-def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_diverged_frac=0.25):
+def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_diverged_frac=0.25, parts=1):
     from paper_2509_24626_amd import harness as H
     lens = synth.gen.lengths(cfg, seed)
     nblk = (lens // cfg.blk).astype(np.int32)
     off, total = H.pool_layout(cfg, nblk)
-    print(f"[gpu] {cfg.name}: pool {total / 2**30:.2f} GiB, sampled sequences {sample_b}", flush=True)
+    print(f"[gpu] {cfg.name}: pool {total / 2**30:.2f} GiB, sampled sequences {sample_b}, {parts} group(s)",
+          flush=True)
     pool = H.HostPool(total, flags)
     try:
-        L = H.build_hier_layer(cfg, seed, layer, pool, 0, nblk, progress=lambda m: print("[gpu]", m, flush=True))
+        L = H.build_hier_layer(cfg, seed, layer, pool, 0, nblk, progress=lambda m: print("[gpu]", m, flush=True),
+                               parts=parts)
         qs = H.query_stream(cfg, seed, layer, steps)
         Hkv, k, G, rb = cfg.Hkv, cfg.k, cfg.G, cfg.record_bytes
         sb = list(sample_b)
@@ -111,6 +113,11 @@ def test_hier_small_lockstep(ss, oracle_impl):
     assert 0 < np.mean(rate[1:]) < 1
 
 
+@pytest.mark.parametrize("parts", [2, 3])
+def test_hier_small_pipelined_groups(ss, oracle_impl, parts):
+    lockstep(oracle_impl, SMALL, seed=3, sample_b=range(SMALL.B), steps=6, parts=parts)
+
+
 def test_hier_small_noncoherent_pool(ss, oracle_impl):
     lockstep(oracle_impl, SMALL, seed=4, sample_b=range(SMALL.B), steps=3, flags=1)
 
@@ -130,7 +137,7 @@ def test_hier_128k_full_size_sampled(ss, oracle_impl):
     heads, 8192 blocks of 16 tokens, k=128, 25% cache, 16 drifting steps
     after the warm-up); the oracle follows 3 of the 64 sequences."""
     cfg = synth.get(2)
-    rate = lockstep(oracle_impl, cfg, seed=0, sample_b=[0, 31, 63], steps=cfg.steps)
+    rate = lockstep(oracle_impl, cfg, seed=0, sample_b=[0, 31, 63], steps=cfg.steps, parts=8)
     assert 0.05 < np.mean(rate[1:]) < 0.5
 
 
@@ -138,7 +145,7 @@ def test_hier_gqa7_full_size_sampled(ss, oracle_impl):
     """The Qwen-like GQA-7 fragmentation workload at full size (B=48, 28/4
     heads, 16384 blocks of 8 tokens, k=512, 15% cache, 8 steps)."""
     cfg = synth.get(4)
-    lockstep(oracle_impl, cfg, seed=0, sample_b=[0, 47], steps=cfg.steps)
+    lockstep(oracle_impl, cfg, seed=0, sample_b=[0, 47], steps=cfg.steps, parts=6)
 
 
 def test_gather_bytes_and_range_checks(ss):
