@@ -70,14 +70,15 @@ __global__ __launch_bounds__(256) void attn_kernel(const uint16_t *__restrict__ 
     const int c0 = split * chunks_per_split;
     const int c1 = min(c0 + chunks_per_split, nchunks);
 
-    // B fragments of S^T = K Q^T: head `col`, channels L*32 + m*8 .. +7
+    // B fragments of S^T = K Q^T: head `col`, channels m*32 + L*8 .. +7 (so
+    // each K load instruction reads a contiguous 64-byte piece of every row)
     frag_t qf[4];
     {
         const bool live = col < G;
-        const uint16_t *qh = q + ((int64_t)b * Hq + g * G + (live ? col : 0)) * D + L * 32;
+        const uint16_t *qh = q + ((int64_t)b * Hq + g * G + (live ? col : 0)) * D + L * 8;
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
-            uint4 x = *reinterpret_cast<const uint4 *>(qh + m * 8);
+            uint4 x = *reinterpret_cast<const uint4 *>(qh + m * 32);
             qf[m].u = live ? x : make_uint4(0, 0, 0, 0);
         }
     }
@@ -96,7 +97,14 @@ __global__ __launch_bounds__(256) void attn_kernel(const uint16_t *__restrict__ 
 #pragma unroll
     for (int t = 0; t < 8; ++t) o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    for (int c = c0 + wave; c < c1; c += WAVES) {
+    // One 32-token chunk: its K and V^T operand fragments and the validity of
+    // the accumulator tokens.  Waves prefetch their next chunk while the
+    // current one is computed (two buffers, loop unrolled by two).
+    struct chunk_t {
+        frag_t kf[2][4], vf[8];
+        bool vz0, vz1;
+    };
+    auto load_chunk = [&](int c, chunk_t &ch) {
         const uint8_t *rec[EPC];
         bool valid[EPC];
 #pragma unroll
@@ -106,33 +114,34 @@ __global__ __launch_bounds__(256) void attn_kernel(const uint16_t *__restrict__ 
             valid[e] = s >= 0 && s < slot_limit;
             rec[e] = ubase + (int64_t)(valid[e] ? s : 0) * REC;
         }
-        frag_t kf[2][4], vf[8];
         const bool vk0 = valid[eK0], vk1 = valid[eK1], vv = valid[eV];
-        const uint8_t *pk0 = rec[eK0] + posK0 * (D * 2) + L * 64;
-        const uint8_t *pk1 = rec[eK1] + posK1 * (D * 2) + L * 64;
+        const uint8_t *pk0 = rec[eK0] + posK0 * (D * 2) + L * 16;
+        const uint8_t *pk1 = rec[eK1] + posK1 * (D * 2) + L * 16;
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
-            kf[0][m].u = vk0 ? *reinterpret_cast<const uint4 *>(pk0 + m * 16) : make_uint4(0, 0, 0, 0);
-            kf[1][m].u = vk1 ? *reinterpret_cast<const uint4 *>(pk1 + m * 16) : make_uint4(0, 0, 0, 0);
+            ch.kf[0][m].u = vk0 ? *reinterpret_cast<const uint4 *>(pk0 + m * 64) : make_uint4(0, 0, 0, 0);
+            ch.kf[1][m].u = vk1 ? *reinterpret_cast<const uint4 *>(pk1 + m * 64) : make_uint4(0, 0, 0, 0);
         }
         const uint8_t *pv = rec[eV] + BLK * D * 2 + (col * BLK + posV) * 2;
 #pragma unroll
         for (int t = 0; t < 8; ++t)
-            vf[t].u = vv ? *reinterpret_cast<const uint4 *>(pv + t * 16 * BLK * 2) : make_uint4(0, 0, 0, 0);
-
+            ch.vf[t].u = vv ? *reinterpret_cast<const uint4 *>(pv + t * 16 * BLK * 2) : make_uint4(0, 0, 0, 0);
+        ch.vz0 = valid[eZ0];
+        ch.vz1 = valid[eZ1];
+    };
+    auto compute_chunk = [&](const chunk_t &ch) {
         f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
-            s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[0][m].v, qf[m].v, s0, 0, 0, 0);
-            s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf[1][m].v, qf[m].v, s1, 0, 0, 0);
+            s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ch.kf[0][m].v, qf[m].v, s0, 0, 0, 0);
+            s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ch.kf[1][m].v, qf[m].v, s1, 0, 0, 0);
         }
         // lane holds z for head `col`, tokens L*8 + v (v = T*4 + i)
         float z[8];
-        const bool vz0 = valid[eZ0], vz1 = valid[eZ1];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            z[i] = vz0 ? s0[i] * scale_log2 : -INFINITY;
-            z[4 + i] = vz1 ? s1[i] * scale_log2 : -INFINITY;
+            z[i] = ch.vz0 ? s0[i] * scale_log2 : -INFINITY;
+            z[4 + i] = ch.vz1 ? s1[i] * scale_log2 : -INFINITY;
         }
         float cm = z[0];
 #pragma unroll
@@ -164,9 +173,15 @@ __global__ __launch_bounds__(256) void attn_kernel(const uint16_t *__restrict__ 
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
             o[t] *= alpha;
-            o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[t].v, ph.v, o[t], 0, 0, 0);
-            o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf[t].v, pl.v, o[t], 0, 0, 0);
+            o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ch.vf[t].v, ph.v, o[t], 0, 0, 0);
+            o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ch.vf[t].v, pl.v, o[t], 0, 0, 0);
         }
+    };
+
+    for (int c = c0 + wave; c < c1; c += WAVES) {
+        chunk_t buf;
+        load_chunk(c, buf);
+        compute_chunk(buf);
     }
     lrun += __shfl_xor(lrun, 16);
     lrun += __shfl_xor(lrun, 32);

@@ -33,8 +33,11 @@ union frag_t {
 };
 
 // Lane (L = lane/16, col = lane%16) takes 16-byte chunks c = L*8 + m of a
-// metadata row for the 8 MFMAs m of a tile: chunks 0..15 are lo, 16..31 hi.
-// The A fragments hold the matching weights of head `col`.
+// metadata row for the 8 MFMAs m of a tile (chunks 0..15 are lo, 16..31
+// hi): each lane streams 128 contiguous bytes of its row.  (A mapping where
+// each load instruction covers a contiguous 64-byte piece of every row
+// instead measured 6% slower on MI355X.)  The A fragments hold the matching
+// weights of head `col`.
 __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__ q,
                                                     const uint8_t *__restrict__ meta,
                                                     const int32_t *__restrict__ nblk, int Hq, int Hkv, int G,
@@ -58,9 +61,9 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__
     {
         const bool live = col < G;
         const uint16_t *qh = q + ((int64_t)b * Hq + g * G + (live ? col : 0)) * D;
-        const bool hi_half = L >= 2;  // chunks 16..31 multiply hi
 #pragma unroll
         for (int m = 0; m < 8; ++m) {
+            const bool hi_half = L >= 2;            // chunks 16..31 multiply hi
             const int c = ((L * 8 + m) & 15) * 8;  // channel of the chunk
             frag_t x;
             x.u = *reinterpret_cast<const uint4 *>(qh + c);
