@@ -3,38 +3,54 @@
 // chosen in Section 2.2).
 //
 // The G query heads that share a KV head make both products small dense
-// contractions, run on v_mfma_f32_16x16x32_bf16 with heads as the 16-wide
-// N dimension (padded with zero queries):
-//   S^T[32 tok x 16 heads] = K[32 tok x 128] * Q^T         (2 row tiles x 4 k-steps)
-//   O^T[128 ch x 16 heads] += V^T[128 x 32 tok] * P^T      (8 row tiles, K = 32 tokens)
-// A wave consumes 32 tokens (16 KiB of K and V) per step.  The K rows of
-// the two S^T tiles are permuted (tile T, row r -> token (r/4)*8 + T*4 + r%4)
-// so that the accumulator lane holding head `col` ends up with exactly the
-// 8 consecutive tokens (lane/16)*8 .. +7, which is the B-operand fragment
-// the PV product needs: P never moves between lanes.  The V tile of a
-// block record is stored channel-major, so each V^T fragment is one
-// 16-byte load.
+// contractions, run on MFMA with heads as the 16-wide N dimension (padded
+// with zero queries).  A wave consumes 16 tokens (8 KiB of K and V) per
+// step:
+//   S^T[16 tok x 16 heads]  = K[16 tok x 128] * Q^T     4 x v_mfma_f32_16x16x32_bf16
+//   O^T[128 ch x 16 heads] += V^T[128 x 16 tok] * P^T   8 x v_mfma_f32_16x16x16_bf16 (x2, hi/lo)
+// The S^T accumulator leaves lane (L = lane/16, col = lane%16) holding head
+// `col` for tokens 4L .. 4L+3, which is exactly the lane's B fragment of the
+// 16x16x16 PV product, so P never moves between lanes.  K fragments are one
+// 16-byte load per lane (channels m*32 + 8L .. +7, so each load instruction
+// reads a contiguous 64-byte piece of 16 token rows); the V tile of a block
+// record is stored channel-major, so each V^T fragment is one 8-byte load.
+// Each wave keeps two steps in flight (the next step's loads are issued
+// before the current step is computed).  K and V are read with raw buffer
+// loads over the unit's cache region: a skipped entry gets an offset past
+// the region's end, which the hardware answers with zeros, so the loads
+// are unconditional and the compiler can wait for exactly one step's loads
+// (a conditional load forces a wait for all outstanding loads).
 //
-// Softmax runs online in the exp2 domain with fp32 state per head.  P is
-// split into bf16 hi + lo parts (two PV MFMAs), which keeps about 16
+// Softmax runs online in the exp2 domain with fp32 state per head; the
+// accumulator rescale is skipped while no head's running maximum changes.
+// P enters the PV product as a bf16 hi + lo pair, which keeps about 16
 // significant bits of every probability.
 //
 // Work split: grid (unit, split); a workgroup of 4 waves owns a contiguous
-// range of 32-token chunks, waves take chunks round-robin, the 4 wave
-// partials are merged in LDS in wave order, and with several splits a
-// second kernel merges the split partials in split order.  All merges run
-// in a fixed order, so results do not depend on scheduling.
+// range of 16-token steps, waves take steps round-robin, the 4 wave partials
+// are merged in LDS in wave order, and with several splits a second kernel
+// merges the split partials in split order.  All merges run in a fixed
+// order, so results do not depend on scheduling.
 #include "internal.hpp"
 
 namespace {
 
 constexpr int D = ss::kHeadDim;
 constexpr int WAVES = 4;
+constexpr int TOK = 16;  // tokens per wave step
 
-union frag_t {
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+constexpr int kBufferFlags = 0x00020000;  // raw buffer descriptor word 3 for gfx9 (32-bit data)
+
+union frag8_t {  // 8 x bf16: A/B fragment of the 16x16x32 MFMA
     bf16x8_t v;
     uint4 u;
-    uint16_t h[8];
+};
+
+union frag4_t {  // 4 x bf16: A/B fragment of the 16x16x16 MFMA
+    s16x4_t v;
+    uint2 u;
+    uint16_t h[4];
 };
 
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f)
@@ -47,32 +63,34 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f)
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
 struct split_plan {
-    int splits, chunks_per_split;
+    int splits, steps_per_split;
 };
 
 template <int BLK>
-__global__ __launch_bounds__(256) void attn_kernel(const uint16_t *__restrict__ q, const uint8_t *__restrict__ kv,
-                                                   const int64_t *__restrict__ region_off,
-                                                   const int32_t *__restrict__ slots, int slot_limit, int Hq,
-                                                   int Hkv, int G, int k, float scale_log2, int chunks_per_split,
-                                                   float *__restrict__ out, float *__restrict__ ws)
+__global__ __launch_bounds__(256, 3) void attn_kernel(const uint16_t *__restrict__ q, const uint8_t *__restrict__ kv,
+                                                      const int64_t *__restrict__ region_off,
+                                                      const int32_t *__restrict__ slots, int slot_limit, int Hq,
+                                                      int Hkv, int G, int k, float scale_log2, int steps_per_split,
+                                                      float *__restrict__ out, float *__restrict__ ws)
 {
     constexpr int64_t REC = 2LL * BLK * D * 2;
-    constexpr int EPC = 32 / BLK;  // block records per 32-token chunk
     __shared__ float sm_m[WAVES][16], sm_l[WAVES][16];
     __shared__ float sm_o[WAVES][16][D + 4];
 
     const int u = blockIdx.x, split = blockIdx.y, splits = gridDim.y;
     const int b = u / Hkv, g = u - b * Hkv;
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    // wave-uniform, so per-step slot indices are scalar loads: a vector load
+    // would make every step wait for the previous step's K/V loads (the
+    // vector-memory counter completes in order)
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int L = lane >> 4, col = lane & 15;
-    const int nchunks = (k + EPC - 1) / EPC;
-    const int c0 = split * chunks_per_split;
-    const int c1 = min(c0 + chunks_per_split, nchunks);
+    const int nsteps = (int)(((int64_t)k * BLK + TOK - 1) / TOK);
+    const int s_begin = split * steps_per_split;
+    const int s_end = min(s_begin + steps_per_split, nsteps);
 
-    // B fragments of S^T = K Q^T: head `col`, channels m*32 + L*8 .. +7 (so
-    // each K load instruction reads a contiguous 64-byte piece of every row)
-    frag_t qf[4];
+    // B fragments of S^T = K Q^T: head `col`, channels m*32 + 8L .. +7
+    frag8_t qf[4];
     {
         const bool live = col < G;
         const uint16_t *qh = q + ((int64_t)b * Hq + g * G + (live ? col : 0)) * D + L * 8;
@@ -85,108 +103,103 @@ __global__ __launch_bounds__(256) void attn_kernel(const uint16_t *__restrict__ 
 
     const uint8_t *ubase = kv + region_off[u];
     const int32_t *us = slots + (int64_t)u * k;
-    // token handled by this lane's A rows in the two S^T tiles, and its record
-    const int tokA0 = (col >> 2) * 8 + (col & 3);  // tile 0; tile 1 adds 4
-    const int eK0 = tokA0 / BLK, eK1 = (tokA0 + 4) / BLK;
-    const int posK0 = tokA0 % BLK, posK1 = (tokA0 + 4) % BLK;
-    const int eV = (L * 8) / BLK, posV = (L * 8) % BLK;  // V^T fragment: tokens L*8 .. +7
-    const int eZ0 = (L * 8) / BLK, eZ1 = (L * 8 + 4) / BLK;  // records of accumulator tokens
+    const uint32_t lim = (uint32_t)slot_limit * (uint32_t)REC;  // bytes of the region (< 2^31, host-checked)
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc((void *)ubase, (short)0, (int)lim,
+                                                                          kBufferFlags);
 
     float mrun = -INFINITY, lrun = 0.f;
     f32x4_t o[8];
 #pragma unroll
     for (int t = 0; t < 8; ++t) o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    // One 32-token chunk: its K and V^T operand fragments and the validity of
-    // the accumulator tokens.  Waves prefetch their next chunk while the
-    // current one is computed (two buffers, loop unrolled by two).
-    struct chunk_t {
-        frag_t kf[2][4], vf[8];
-        bool vz0, vz1;
+    struct step_t {
+        frag8_t kf[4];
+        frag4_t vf[8];
+        bool vz;  // the lane's accumulator tokens 4L .. 4L+3 are selected
     };
-    auto load_chunk = [&](int c, chunk_t &ch) {
-        const uint8_t *rec[EPC];
-        bool valid[EPC];
+    // token t of the unit's selected-token sequence -> (entry t / BLK, position t % BLK)
+    auto load_step = [&](int st, step_t &x) {
+        const int tk = st * TOK + col;     // this lane's K row
+        const int tv = st * TOK + L * 4;   // this lane's V^T / accumulator tokens
+        // entries of the step (uniform): one, or two when BLK = 8
+        const int e0 = (st * TOK) / BLK;
+        const int s0 = e0 < k ? us[e0] : -1;
+        const int s1 = (BLK == 8 && e0 + 1 < k) ? us[e0 + 1] : -1;
+        const int sk = (BLK == 8 && col >= 8) ? s1 : s0;
+        const int sv = (BLK == 8 && L >= 2) ? s1 : s0;
+        const bool live = st < s_end;  // steps past the range load zeros
+        const bool vk = live && sk >= 0 && sk < slot_limit;
+        const bool vv = live && sv >= 0 && sv < slot_limit;
+        // skipped entries read at `lim`, past the region: the loads return zeros
+        const uint32_t ko = vk ? (uint32_t)sk * (uint32_t)REC + (tk % BLK) * (D * 2) + L * 16 : lim;
 #pragma unroll
-        for (int e = 0; e < EPC; ++e) {
-            const int idx = c * EPC + e;
-            const int s = idx < k ? us[idx] : -1;
-            valid[e] = s >= 0 && s < slot_limit;
-            rec[e] = ubase + (int64_t)(valid[e] ? s : 0) * REC;
-        }
-        const bool vk0 = valid[eK0], vk1 = valid[eK1], vv = valid[eV];
-        const uint8_t *pk0 = rec[eK0] + posK0 * (D * 2) + L * 16;
-        const uint8_t *pk1 = rec[eK1] + posK1 * (D * 2) + L * 16;
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            ch.kf[0][m].u = vk0 ? *reinterpret_cast<const uint4 *>(pk0 + m * 64) : make_uint4(0, 0, 0, 0);
-            ch.kf[1][m].u = vk1 ? *reinterpret_cast<const uint4 *>(pk1 + m * 64) : make_uint4(0, 0, 0, 0);
-        }
-        const uint8_t *pv = rec[eV] + BLK * D * 2 + (col * BLK + posV) * 2;
+        for (int m = 0; m < 4; ++m)
+            x.kf[m].v = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rsrc, ko + m * 64, 0, 0));
+        const uint32_t vo = vv ? (uint32_t)sv * (uint32_t)REC + BLK * D * 2 + (col * BLK + tv % BLK) * 2 : lim;
 #pragma unroll
         for (int t = 0; t < 8; ++t)
-            ch.vf[t].u = vv ? *reinterpret_cast<const uint4 *>(pv + t * 16 * BLK * 2) : make_uint4(0, 0, 0, 0);
-        ch.vz0 = valid[eZ0];
-        ch.vz1 = valid[eZ1];
+            x.vf[t].v = __builtin_bit_cast(s16x4_t, __builtin_amdgcn_raw_buffer_load_b64(rsrc, vo + t * 16 * BLK * 2, 0, 0));
+        x.vz = vv;
     };
-    auto compute_chunk = [&](const chunk_t &ch) {
-        f32x4_t s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    auto compute_step = [&](const step_t &x) {
+        f32x4_t sacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ch.kf[0][m].v, qf[m].v, s0, 0, 0, 0);
-            s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ch.kf[1][m].v, qf[m].v, s1, 0, 0, 0);
-        }
-        // lane holds z for head `col`, tokens L*8 + v (v = T*4 + i)
-        float z[8];
+        for (int m = 0; m < 4; ++m) sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x.kf[m].v, qf[m].v, sacc, 0, 0, 0);
+        float z[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            z[i] = ch.vz0 ? s0[i] * scale_log2 : -INFINITY;
-            z[4 + i] = ch.vz1 ? s1[i] * scale_log2 : -INFINITY;
-        }
-        float cm = z[0];
-#pragma unroll
-        for (int v = 1; v < 8; ++v) cm = fmaxf(cm, z[v]);
+        for (int i = 0; i < 4; ++i) z[i] = x.vz ? sacc[i] * scale_log2 : -INFINITY;
+        float cm = fmaxf(fmaxf(z[0], z[1]), fmaxf(z[2], z[3]));
         cm = fmaxf(cm, __shfl_xor(cm, 16));
         cm = fmaxf(cm, __shfl_xor(cm, 32));
         const float mnew = fmaxf(mrun, cm);
-        float p[8], alpha;
+        float p[4], alpha = 1.f;
         if (mnew == -INFINITY) {
-            alpha = 1.f;
 #pragma unroll
-            for (int v = 0; v < 8; ++v) p[v] = 0.f;
+            for (int i = 0; i < 4; ++i) p[i] = 0.f;
         } else {
             alpha = __builtin_amdgcn_exp2f(mrun - mnew);
 #pragma unroll
-            for (int v = 0; v < 8; ++v) p[v] = __builtin_amdgcn_exp2f(z[v] - mnew);
+            for (int i = 0; i < 4; ++i) p[i] = __builtin_amdgcn_exp2f(z[i] - mnew);
+        }
+        if (__any(mnew != mrun)) {
+#pragma unroll
+            for (int t = 0; t < 8; ++t) o[t] *= alpha;
         }
         mrun = mnew;
+        frag4_t ph, pl;
         float psum = 0.f;
-        frag_t ph, pl;
 #pragma unroll
-        for (int v = 0; v < 8; ++v) {
-            psum += p[v];
-            const uint16_t hi = f32_to_bf16_rne(p[v]);
-            ph.h[v] = hi;
-            pl.h[v] = f32_to_bf16_rne(p[v] - bf16_to_f32(hi));
+        for (int i = 0; i < 4; ++i) {
+            psum += p[i];
+            const uint16_t hi = f32_to_bf16_rne(p[i]);
+            ph.h[i] = hi;
+            pl.h[i] = f32_to_bf16_rne(p[i] - bf16_to_f32(hi));
         }
         lrun = lrun * alpha + psum;
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-            o[t] *= alpha;
-            o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ch.vf[t].v, ph.v, o[t], 0, 0, 0);
-            o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ch.vf[t].v, pl.v, o[t], 0, 0, 0);
+            o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(x.vf[t].v, ph.v, o[t], 0, 0, 0);
+            o[t] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(x.vf[t].v, pl.v, o[t], 0, 0, 0);
         }
     };
 
-    for (int c = c0 + wave; c < c1; c += WAVES) {
-        chunk_t buf;
-        load_chunk(c, buf);
-        compute_chunk(buf);
+    // the prefetches are unconditional (a step past the end loads zeros) so
+    // that every path has the same loads in flight and each compute waits
+    // only for its own step
+    step_t bufA, bufB;
+    int st = s_begin + wave;
+    load_step(st, bufA);
+    for (; st < s_end; st += 2 * WAVES) {
+        load_step(st + WAVES, bufB);
+        compute_step(bufA);
+        if (st + WAVES >= s_end) break;
+        load_step(st + 2 * WAVES, bufA);
+        compute_step(bufB);
     }
     lrun += __shfl_xor(lrun, 16);
     lrun += __shfl_xor(lrun, 32);
 
-    // wave partials -> LDS; lane holds O^T[16t + L*4 + i][col]
+    // wave partials -> LDS; lane holds O^T[16t + 4L + i][col]
     if (L == 0) {
         sm_m[wave][col] = mrun;
         sm_l[wave][col] = lrun;
@@ -214,12 +227,12 @@ __global__ __launch_bounds__(256) void attn_kernel(const uint16_t *__restrict__ 
         if (splits == 1) {
             out[((int64_t)b * Hq + g * G + h) * D + ch] = lsum > 0.f ? osum / lsum : 0.f;
         } else {
-            float *p = ws + (((int64_t)u * splits + split) * G + h) * (D + 2);
+            float *pp = ws + (((int64_t)u * splits + split) * G + h) * (D + 2);
             if (ch == 0) {
-                p[0] = M;
-                p[1] = lsum;
+                pp[0] = M;
+                pp[1] = lsum;
             }
-            p[2 + ch] = osum;
+            pp[2 + ch] = osum;
         }
     }
 }
@@ -246,17 +259,16 @@ __global__ __launch_bounds__(D) void combine_kernel(const float *__restrict__ ws
 
 split_plan plan(int units, int k, int blk)
 {
-    const int epc = 32 / blk;
-    const int chunks = (k + epc - 1) / epc;
-    const int target_wg = 1024;
+    const int steps = (int)(((int64_t)k * blk + TOK - 1) / TOK);
+    const int target_wg = 512;  // two 4-wave workgroups per CU
     int splits = units > 0 ? (target_wg + units - 1) / units : 1;
-    int max_splits = chunks / (WAVES * 2);  // keep >= 2 chunks per wave
+    int max_splits = steps / (WAVES * 4);  // keep >= 4 steps per wave
     if (max_splits < 1) max_splits = 1;
     if (splits > max_splits) splits = max_splits;
     if (splits < 1) splits = 1;
-    int cps = (chunks + splits - 1) / splits;
-    splits = (chunks + cps - 1) / cps;
-    return {splits, cps};
+    int sps = (steps + splits - 1) / splits;
+    splits = (steps + sps - 1) / sps;
+    return {splits, sps};
 }
 
 }  // namespace
@@ -284,6 +296,8 @@ extern "C" ss_status ss_sparse_attention(const void *q, const void *kv_base, con
     SS_CHECK_ARG(std::isfinite(scale), "ss_sparse_attention: scale not finite");
     if (B == 0) return SS_OK;
     SS_CHECK_ARG(q && kv_base && region_off && slots && out, "ss_sparse_attention: null pointer");
+    SS_CHECK_SUPPORTED(slot_limit >= 0 && (int64_t)slot_limit * 2 * blk * D * 2 <= 0x7FFFFFFF,
+                       "ss_sparse_attention: slot_limit=%d records exceed a 2 GiB region", slot_limit);
     const int units = B * Hkv;
     split_plan sp = plan(units, k, blk);
     const size_t need = ss_sparse_attention_workspace(B, Hq, Hkv, d, blk, k);
@@ -297,9 +311,9 @@ extern "C" ss_status ss_sparse_attention(const void *q, const void *kv_base, con
     const uint8_t *kv = static_cast<const uint8_t *>(kv_base);
     float *ws = static_cast<float *>(workspace);
     switch (blk) {
-    case 8: attn_kernel<8><<<grid, dim3(256), 0, s>>>(qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.chunks_per_split, out, ws); break;
-    case 16: attn_kernel<16><<<grid, dim3(256), 0, s>>>(qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.chunks_per_split, out, ws); break;
-    default: attn_kernel<32><<<grid, dim3(256), 0, s>>>(qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.chunks_per_split, out, ws); break;
+    case 8: attn_kernel<8><<<grid, dim3(256), 0, s>>>(qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
+    case 16: attn_kernel<16><<<grid, dim3(256), 0, s>>>(qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
+    default: attn_kernel<32><<<grid, dim3(256), 0, s>>>(qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
     }
     ss_status st = ss::check_launch("ss_sparse_attention");
     if (st != SS_OK || sp.splits == 1) return st;
