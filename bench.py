@@ -12,9 +12,12 @@ timing starts; the warm-up step fills the cold cache.
 
 Prints one JSON line on stdout (progress goes to stderr):
   value      = B * steps / wall time of the timed steps (tokens/s)
-  roofline   = the step's dominant kernel against its bound (HBM 8 TB/s, or
-               the PCIe 5.0 x16 host link at 63.0 GB/s per direction)
-  rooflines  = every kernel of the step, each with its algorithmic bytes
+  roofline   = the step's dominant kernel, the gather over the PCIe 5.0 x16
+               host link (63.0 GB/s per direction): missed-record bytes per
+               step / the link's busy time (the union of the HIP-event
+               intervals of the step's gather launches in the timed region)
+  rooflines_isolated = scoring, top-k and attention each launched alone on
+               the same data, against the HBM peak (8 TB/s)
   cpu_baseline = the CPU oracle on a bounded sample of the same workload.
 """
 import argparse
@@ -43,7 +46,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1, help="untimed steps first (the first fills the cache)")
     ap.add_argument("--config", default="2", help="workload index or name (see synth/configs.py)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--parts", type=int, default=8, help="sequence groups pipelined within a layer step")
+    ap.add_argument("--parts", default="tent6",
+                    help="sequence groups pipelined within a layer step: N (equal), tentN (small first/last), "
+                         "or comma-separated sizes")
     ap.add_argument("--cpu-seqs", type=int, default=64, help="sequences in the CPU-oracle sample")
     ap.add_argument("--cpu-steps", type=int, default=8, help="timed steps in the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -86,9 +91,14 @@ def main():
     pool = H.HostPool(total, args.pool_flags)
     layers, qstreams = [], []
     meta_ms = []
+    if args.parts.startswith("tent"):
+        parts = H.tent_parts(cfg.B, int(args.parts[4:]))
+    elif "," in args.parts:
+        parts = [int(x) for x in args.parts.split(",")]
+    else:
+        parts = int(args.parts)
     for l in range(cfg.layers):
-        t0 = time.perf_counter()
-        L = H.build_hier_layer(cfg, args.seed, l, pool, l * per_layer, nblk, progress=log, parts=args.parts)
+        L = H.build_hier_layer(cfg, args.seed, l, pool, l * per_layer, nblk, progress=log, parts=parts)
         layers.append(L)
         qstreams.append(H.query_stream(cfg, args.seed, l, warmup + steps - 1))
     # metadata build (setup path), timed on its own for one layer
@@ -118,65 +128,74 @@ def main():
     # ------------------------------------------------------------ timed
     P = layers[0].parts
     ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(7 * P)] for _ in layers] for _ in range(steps)]
+    # every timing event is a barrier packet on its queue; record only the step's
+    # start and end and each gather's start and end (the dominant kernel)
+    used = [False] * (7 * P)
+    used[0] = used[7 * (P - 1) + 6] = True
+    for p in range(P):
+        used[7 * p + 3] = used[7 * p + 4] = True
     for row in ev:  # create the underlying events before timing
         for es in row:
             for e in es:
                 e.record()
     torch.cuda.synchronize()
     n_miss = np.zeros((steps, len(layers)), np.int64)
-    valid_sel = []
     t0 = time.perf_counter()
     for i in range(steps):
         s = warmup + i
         for l, L in enumerate(layers):
-            L.step(s, qstreams[l][s][1], events=[e.cuda_event for e in ev[i][l]])
+            L.step(s, qstreams[l][s][1], events=[e.cuda_event if used[j] else None for j, e in enumerate(ev[i][l])])
             n_miss[i, l] = L.last_n_miss
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    for L in layers:
-        valid_sel.append(int((L.sel >= 0).sum().item()))
 
     # ------------------------------------------------------- accounting
-    # per launch (one per sequence group): score, top-k, gather, attention
-    stage = {k: [] for k in ("score", "topk", "gather", "attention")}
+    # Gathers of consecutive groups overlap (two transfer streams), so the
+    # link's busy time is the union of the gather intervals of a step.  Also
+    # per step: the ramp before the first gather starts, idle gaps inside
+    # the gather span, and the tail after the last gather ends.
+    pipe = {"ramp": [], "link_busy": [], "link_gaps": [], "tail": []}
+    gather_launch_ms = []
     for i in range(steps):
         for l in range(len(layers)):
             e = ev[i][l]
-            for p in range(P):
-                b = 7 * p
-                stage["score"].append(e[b + 0].elapsed_time(e[b + 1]))
-                stage["topk"].append(e[b + 1].elapsed_time(e[b + 2]))
-                stage["gather"].append(e[b + 3].elapsed_time(e[b + 4]))
-                stage["attention"].append(e[b + 5].elapsed_time(e[b + 6]))
-    avg = {k: float(np.mean(v)) for k, v in stage.items()}
-    per_step_sum = {k: float(np.sum(v)) / steps for k, v in stage.items()}
+            iv = sorted((e[0].elapsed_time(e[7 * p + 3]), e[0].elapsed_time(e[7 * p + 4])) for p in range(P))
+            gather_launch_ms += [b - a for a, b in iv]
+            busy, cur_a, cur_b = 0.0, iv[0][0], iv[0][1]
+            for a, b in iv[1:]:
+                if a > cur_b:
+                    busy += cur_b - cur_a
+                    cur_a, cur_b = a, b
+                else:
+                    cur_b = max(cur_b, b)
+            busy += cur_b - cur_a
+            first, last = iv[0][0], max(b for _, b in iv)
+            pipe["ramp"].append(first)
+            pipe["link_busy"].append(busy)
+            pipe["link_gaps"].append(last - first - busy)
+            pipe["tail"].append(e[0].elapsed_time(e[7 * (P - 1) + 6]) - last)
+    pipe = {k: round(float(np.mean(v)), 4) for k, v in pipe.items()}
     units = cfg.B * cfg.Hkv
-    blocks = int(nblk.sum()) * cfg.Hkv
-    q_bytes = cfg.B * cfg.Hq * D * 2
-    step_bytes = {
-        # metadata rows (lo, hi: 512 B per block) + fp32 scores written + q
-        "score": len(layers) * (blocks * (2 * D * 2 + 4) + q_bytes),
-        # scores read + selection written
-        "topk": len(layers) * (blocks * 4 + units * cfg.k * 4),
-        # missed block records over the host link (mean over the timed steps)
-        "gather": float(n_miss.sum()) / steps * cfg.record_bytes,
-        # selected K and V records + q + fp32 output
-        "attention": float(np.sum(valid_sel)) * cfg.record_bytes + len(layers) * (q_bytes + cfg.B * cfg.Hq * D * 4),
-    }
-    launches = len(layers) * P  # launches of each kernel per step
-    algo = {k: v / launches for k, v in step_bytes.items()}
-    roof = {}
-    for k, bound, peak in (("score", "hbm", HBM_PEAK_GBS), ("topk", "hbm", HBM_PEAK_GBS),
-                           ("gather", "host-link", LINK_PEAK_GBS), ("attention", "hbm", HBM_PEAK_GBS)):
-        ach = algo[k] / (avg[k] * 1e-3) / 1e9 if avg[k] > 0 else 0.0
-        roof[k] = {"bound": bound, "achieved": round(ach, 2), "peak": round(peak, 2), "unit": "GB/s",
-                   "frac": round(ach / peak, 4), "bytes_per_launch": int(algo[k]), "ms_per_launch": round(avg[k], 4),
-                   "traffic": None}
-    dominant = max(("score", "topk", "gather", "attention"), key=lambda k: avg[k])
+    # the gather's algorithmic bytes per step: the missed block records (mean
+    # over the timed steps) over the host link, against the link's busy time
+    gather_bytes = float(n_miss.sum()) / steps * cfg.record_bytes
+    busy_ms = pipe["link_busy"] * len(layers)
+    ach = gather_bytes / (busy_ms * 1e-3) / 1e9 if busy_ms > 0 else 0.0
+    roof = {"gather": {"bound": "host-link", "achieved": round(ach, 2), "peak": round(LINK_PEAK_GBS, 2),
+                       "unit": "GB/s", "frac": round(ach / LINK_PEAK_GBS, 4), "bytes_per_step": int(gather_bytes),
+                       "link_busy_ms_per_step": round(busy_ms, 4), "launches_per_step": len(layers) * P,
+                       "ms_per_launch": round(float(np.mean(gather_launch_ms)), 4), "traffic": None}}
+    dominant = "gather"  # pipeline_ms shows the link busy for most of the step
     tokens = cfg.B * steps
     value = tokens / wall
     miss_rate = float(n_miss.mean()) / (units * cfg.k)
-    log(f"{value:.0f} tokens/s, {wall / steps * 1e3:.3f} ms/step; kernel ms per step {per_step_sum}")
+    log(f"{value:.0f} tokens/s, {wall / steps * 1e3:.3f} ms/step; gather {ach:.1f} GB/s; pipeline {pipe}")
+
+    # ------------------------------------------- isolated kernel rates
+    # Each kernel alone over the whole batch (one launch, nothing else on the
+    # GPU), on the last timed step's data: the HBM kernels' own rates, which
+    # the overlapped step hides behind the host-link gather.
+    iso = isolated_rates(cfg, layers[0], qstreams[0][warmup + steps - 1][1], ss, torch)
 
     # ------------------------------------------------------ CPU baseline
     cpu = None
@@ -200,12 +219,12 @@ def main():
                    "context": int(lens.max()), "block": cfg.blk, "topk_blocks": cfg.k, "cache_frac": cfg.cache_frac,
                    "layers": cfg.layers, "drift": cfg.drift, "seed": args.seed},
         "roofline": dict(kernel=dominant, **roof[dominant]),
-        "rooflines": roof,
-        "kernel_ms_per_step": {k: round(v, 4) for k, v in per_step_sum.items()},
-        "parts": P,
+        "pipeline_ms": pipe,
+        "rooflines_isolated": iso,
+        "parts": layers[0].part_sizes,
         "miss_rate": round(miss_rate, 4),
         "gather_GBps": roof["gather"]["achieved"],
-        "hbm_frac": {"score": roof["score"]["frac"], "attention": roof["attention"]["frac"]},
+        "hbm_frac": {"score": iso["score"]["frac"], "attention": iso["attention"]["frac"]},
         "metadata_build": {"ms": round(float(np.median(meta_ms)), 4), "bytes": meta_bytes,
                            "GBps": round(meta_bytes / (np.median(meta_ms) * 1e-3) / 1e9, 1),
                            "note": "setup path (when blocks fill), one sequence, not in the step"},
@@ -215,6 +234,49 @@ def main():
     for L in layers:
         L.close()
     pool.close()
+
+
+def isolated_rates(cfg, L, q, ss, torch, reps=10):
+    """Median duration of score, top-k and attention over the full batch,
+    each launched alone after a cache flush, as a fraction of the HBM peak.
+    HIP events bracket each launch, so the figure includes the launch's
+    dispatch latency (a few microseconds)."""
+    B, Hq, Hkv, k = cfg.B, cfg.Hq, cfg.Hkv, cfg.k
+    nb = L.nblk_host
+    blocks = int(nb.sum()) * Hkv
+    valid = int((L.slots >= 0).sum().item())
+    ws_bytes = ss.ss_sparse_attention_workspace(B, Hq, Hkv, D, cfg.blk, k)
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+    out = torch.empty(B, Hq, D, dtype=torch.float32, device="cuda")
+    runs = {
+        "score": (lambda: ss.ss_score_blocks(q, L.meta, L.nblk, B, Hq, Hkv, cfg.nblk_max, D, L.scores),
+                  blocks * (2 * D * 2 + 4) + B * Hq * D * 2),
+        "topk": (lambda: ss.ss_select_topk(L.scores, L.nblk, B, Hkv, cfg.nblk_max, k, L.sel),
+                 blocks * 4 + B * Hkv * k * 4),
+        "attention": (lambda: ss.ss_sparse_attention(q, L.cache, L.cache_off, L.slots, int(L.capacity.max()), B, Hq,
+                                                     Hkv, D, cfg.blk, k, 1.0 / math.sqrt(D), out, ws, ws_bytes),
+                      valid * cfg.record_bytes + B * Hq * D * (2 + 4)),
+    }
+    res = {}
+    # a 1 GiB read before every timed launch evicts the 256 MB last-level
+    # cache, so each launch streams its bytes from HBM
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    flush.fill_(1.0)
+    for name, (fn, nbytes) in runs.items():
+        ts = []
+        for _ in range(reps):
+            flush.sum()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        ms = float(np.median(ts))
+        ach = nbytes / (ms * 1e-3) / 1e9
+        res[name] = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(ach / HBM_PEAK_GBS, 4), "bytes_per_launch": int(nbytes), "ms_per_launch": round(ms, 4)}
+    return res
 
 
 def cpu_baseline(cfg, pool, L, qs, nblk, args, warmup):

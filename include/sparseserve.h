@@ -214,11 +214,14 @@ ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t 
  * selection to the host, resolve it in the block cache, copy slots and the
  * miss list back, gather the misses, attend.
  * The batch is processed in `parts` consecutive sequence groups (1 <= parts
- * <= B; 0 means 1) so that the host-link gather of one group overlaps the
+ * <= B; 0 means 1) -- equal groups, or group p = sequences
+ * [part_end[p-1], part_end[p]) when part_end (host int32 [parts], strictly
+ * increasing, last = B) is given -- so that the host-link gather of one
+ * group overlaps the
  * scoring and the host resolve of the next: scoring, selection and
- * attention run on `stream`; the gathers run on a transfer stream the
- * library creates for this cache handle on first use (default priority)
- * and orders against `stream` with events.  Selections reach the host, and
+ * attention run on `stream`; the gathers run on two transfer streams the
+ * library creates for this cache handle on first use (default priority;
+ * groups alternate between them) and orders against `stream` with events.  Selections reach the host, and
  * slots and miss rows reach the GPU, through the mapped host buffers (no
  * copy-engine transfers).  The host waits only for each group's selection;
  * everything after the last resolve is enqueued and the call returns
@@ -237,7 +240,7 @@ ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t 
  * unit order (as one ss_cache_resolve would list them).
  * events: NULL, or 7*parts hipEvent_t; for group p, events[7p+0..6] are
  * recorded before scoring, after scoring, after selection (on `stream`),
- * before and after the gather (transfer stream), before and after attention
+ * before and after the gather (its transfer stream), before and after attention
  * (on `stream`) -- per-kernel timing.
  * Streams and events belong to the device current at the first call.
  * On error nothing further is enqueued; a resolve error leaves the cache
@@ -261,6 +264,7 @@ typedef struct ss_layer_buffers {
     void *attn_ws;
     size_t attn_ws_bytes;
     int parts;
+    const int32_t *part_end;    /* host int32 [parts] or NULL */
 } ss_layer_buffers;
 
 ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, const void *q, float *out, void *stream,

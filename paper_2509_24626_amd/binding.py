@@ -40,7 +40,8 @@ class ss_layer_buffers(ctypes.Structure):
                 ("pool_off_dev", _vp), ("cache", _vp), ("cache_base", _vp), ("cache_off_dev", _vp),
                 ("capacity_dev", _vp), ("slot_limit", _i32), ("scores", _vp), ("sel_dev", _vp),
                 ("slots_dev", _vp), ("miss_dev", _vp), ("sel_host", _vp), ("slots_host", _vp),
-                ("miss_host", _vp), ("miss_cap", _i64), ("attn_ws", _vp), ("attn_ws_bytes", _sz), ("parts", _i32)]
+                ("miss_host", _vp), ("miss_cap", _i64), ("attn_ws", _vp), ("attn_ws_bytes", _sz), ("parts", _i32),
+                ("part_end", _vp)]
 
 _SIGNATURES = {
     "ss_abi_version": (_i32, []),

@@ -13,7 +13,9 @@
 // and also copies the group's slot table to HBM) and its attention on the
 // caller's stream behind that gather.  So the host-link transfer of group p
 // overlaps the resolve of group p+1 and the scoring still in flight, and
-// attention of group p overlaps the gather of group p+1.  Every hand-off is
+// attention of group p overlaps the gather of group p+1.  Groups alternate
+// between two transfer streams, so a group's gather starts while the
+// previous one drains (no launch gap, no idle tail on the link).  Every hand-off is
 // a kernel on a compute queue: no copy-engine transfer, whose cross-engine
 // synchronisation costs tens of microseconds per hand-off, is on the path.
 #include <thread>
@@ -37,7 +39,7 @@ int cache_kv_heads(const ss_cache *c);
 namespace {
 
 struct exec_state {
-    hipStream_t xfer = nullptr;
+    hipStream_t xfer[2] = {nullptr, nullptr};  // groups alternate between them
     hipEvent_t start = nullptr;
     std::vector<hipEvent_t> sel_ready, gathered;
     // device addresses of the caller's pinned host buffers (looked up once)
@@ -66,7 +68,8 @@ void exec_free(void *p)
     for (hipEvent_t ev : e->sel_ready) (void)hipEventDestroy(ev);
     for (hipEvent_t ev : e->gathered) (void)hipEventDestroy(ev);
     if (e->start) (void)hipEventDestroy(e->start);
-    if (e->xfer) (void)hipStreamDestroy(e->xfer);
+    for (hipStream_t x : e->xfer)
+        if (x) (void)hipStreamDestroy(x);
     delete e;
 }
 
@@ -82,7 +85,8 @@ ss_status get_exec(ss_cache *c, int parts, exec_state **out)
     ss_status st;
     if (!e) {
         e = new exec_state;
-        if ((st = hip_check(hipStreamCreateWithFlags(&e->xfer, hipStreamNonBlocking), "create transfer stream")) ||
+        if ((st = hip_check(hipStreamCreateWithFlags(&e->xfer[0], hipStreamNonBlocking), "create transfer stream")) ||
+            (st = hip_check(hipStreamCreateWithFlags(&e->xfer[1], hipStreamNonBlocking), "create transfer stream")) ||
             (st = hip_check(hipEventCreateWithFlags(&e->start, hipEventDisableTiming), "create event"))) {
             exec_free(e);
             return st;
@@ -138,14 +142,22 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
     SS_CHECK_ARG(L->miss_cap >= (int64_t)B * rows_per_seq, "ss_decode_layer: miss_cap %lld < B*Hkv*k",
                  (long long)L->miss_cap);
     int P = L->parts < 1 ? 1 : (L->parts > B ? B : L->parts);
+    if (L->part_end) {
+        P = L->parts;
+        SS_CHECK_ARG(P >= 1 && L->part_end[P - 1] == B, "ss_decode_layer: part_end must end at B=%d", B);
+        for (int p = 0; p < P; ++p)
+            SS_CHECK_ARG(L->part_end[p] > (p ? L->part_end[p - 1] : 0),
+                         "ss_decode_layer: part_end must be strictly increasing");
+    }
     exec_state *ex = nullptr;
     ss_status st = get_exec(L->cache, P, &ex);
     if (st) return st;
-    hipStream_t s = ss::as_stream(stream), x = ex->xfer;
+    hipStream_t s = ss::as_stream(stream);
     const size_t rec = (size_t)2 * L->blk * d * 2;
     const char *q8 = static_cast<const char *>(q);
     const char *meta8 = static_cast<const char *>(L->meta);
-    auto b_of = [&](int p) { return (int)((int64_t)B * p / P); };
+    const int32_t *pe = L->part_end;
+    auto b_of = [&](int p) { return p == 0 ? 0 : (pe ? pe[p - 1] : (int)((int64_t)B * p / P)); };
 
     int32_t *sel_hd = nullptr, *slots_hd = nullptr, *miss_hd = nullptr;  // device views of the host buffers
     if ((st = device_address(ex, 0, L->sel_host, (void **)&sel_hd)) ||
@@ -153,9 +165,10 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
         (st = device_address(ex, 2, L->miss_host, (void **)&miss_hd)))
         return st;
 
-    // the transfer stream starts after everything already on `stream`
+    // the transfer streams start after everything already on `stream`
     if ((st = hip_check(hipEventRecord(ex->start, s), "record")) ||
-        (st = hip_check(hipStreamWaitEvent(x, ex->start, 0), "order transfer stream")))
+        (st = hip_check(hipStreamWaitEvent(ex->xfer[0], ex->start, 0), "order transfer stream")) ||
+        (st = hip_check(hipStreamWaitEvent(ex->xfer[1], ex->start, 0), "order transfer stream")))
         return st;
 
     // scoring and selection of every group; selections land in HBM and host memory
@@ -179,6 +192,9 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
     for (int p = 0; p < P; ++p) {
         const int b0 = b_of(p), b1 = b_of(p + 1), Bp = b1 - b0;
         const int64_t row0 = b0 * rows_per_seq;
+        // consecutive groups' gathers run on alternate transfer streams, so the
+        // next gather is already streaming while the previous one drains
+        hipStream_t x = ex->xfer[p & 1];
         if ((st = wait_host(ex->sel_ready[p]))) return st;
         // miss rows of the step are kept compact: this group appends at `total`
         int64_t np = 0;

@@ -105,7 +105,15 @@ class HierLayer:
 
     def __init__(self, cfg, nblk_host, capacity, pool, pool_off_host, meta, parts=1):
         self.cfg = cfg
-        self.parts = max(1, min(parts, cfg.B))
+        # parts: a group count (equal groups) or a list of group sizes
+        if isinstance(parts, (list, tuple)):
+            assert sum(parts) == cfg.B and all(p > 0 for p in parts)
+            self.part_sizes = list(parts)
+        else:
+            n = max(1, min(parts, cfg.B))
+            self.part_sizes = [cfg.B * (i + 1) // n - cfg.B * i // n for i in range(n)]
+        self.parts = len(self.part_sizes)
+        self.part_end = np.cumsum(self.part_sizes).astype(np.int32)
         B, Hkv, k = cfg.B, cfg.Hkv, cfg.k
         self.units = B * Hkv
         self.nblk_host = np.asarray(nblk_host, np.int32)
@@ -136,8 +144,7 @@ class HierLayer:
         self.miss_h = st[2 * self.units * k:2 * self.units * k + 4 * self.miss_cap].view(self.miss_cap, 4)
         self.out = torch.empty(B, cfg.Hq, D, dtype=torch.float32, device="cuda")
         # attention runs per sequence group; one workspace serves the groups in turn
-        sizes = {B * (i + 1) // self.parts - B * i // self.parts for i in range(self.parts)}
-        self.ws_bytes = max(ss.ss_sparse_attention_workspace(b, cfg.Hq, Hkv, D, cfg.blk, k) for b in sizes)
+        self.ws_bytes = max(ss.ss_sparse_attention_workspace(b, cfg.Hq, Hkv, D, cfg.blk, k) for b in set(self.part_sizes))
         self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device="cuda")
         p = ss._ptr
         self.buffers = ss.ss_layer_buffers(
@@ -147,7 +154,7 @@ class HierLayer:
             slot_limit=int(self.capacity.max()) if self.units else 0, scores=p(self.scores), sel_dev=p(self.sel),
             slots_dev=p(self.slots), miss_dev=p(self.miss), sel_host=p(self.sel_h), slots_host=p(self.slots_h),
             miss_host=p(self.miss_h), miss_cap=self.miss_cap, attn_ws=p(self.ws), attn_ws_bytes=self.ws_bytes,
-            parts=self.parts)
+            parts=self.parts, part_end=self.part_end.ctypes.data)
         self.last_n_miss = 0
 
     def step(self, t, q, events=None):
@@ -175,6 +182,17 @@ def pool_layout(cfg, nblk):
     per_unit = np.repeat(np.asarray(nblk, np.int64), cfg.Hkv) * cfg.record_bytes
     off = np.concatenate([[0], np.cumsum(per_unit)[:-1]]).astype(np.int64)
     return off, int(per_unit.sum())
+
+
+def tent_parts(B, n):
+    """Group sizes that grow then shrink (small first and last groups), so the
+    link starts early and little work is left after the last gather."""
+    n = max(1, min(n, B))
+    w = np.array([min(i + 1, n - i) for i in range(n)], np.float64) ** 2
+    sizes = np.maximum(1, np.floor(w / w.sum() * B)).astype(int)
+    i = int(np.argmax(w))
+    sizes[i] += B - int(sizes.sum())
+    return [int(x) for x in sizes]
 
 
 def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None, parts=1):
