@@ -53,6 +53,8 @@ def parse():
     ap.add_argument("--cpu-steps", type=int, default=8, help="timed steps in the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pool-flags", type=int, default=0, help="0 coherent, 1 non-coherent pinned pool")
+    ap.add_argument("--pool-budget-gib", type=float, default=56.0,
+                    help="pinned DRAM for KV records; layers beyond it reuse earlier layers' records")
     return ap.parse_args()
 
 
@@ -86,10 +88,9 @@ def main():
     lens = synth.gen.lengths(cfg, args.seed)
     nblk = (lens // cfg.blk).astype(np.int32)
     _, per_layer = H.pool_layout(cfg, nblk)
-    total = per_layer * cfg.layers
-    log(f"workload {cfg.name}: {cfg.layers} layer(s), pool {total / 2**30:.2f} GiB pinned")
-    pool = H.HostPool(total, args.pool_flags)
-    layers, qstreams = [], []
+    n_distinct = H.distinct_layers(cfg, nblk, int(args.pool_budget_gib * 2**30))
+    log(f"workload {cfg.name}: {cfg.layers} layer(s), {n_distinct} with DRAM records of their own, "
+        f"pool {per_layer * n_distinct / 2**30:.2f} GiB pinned")
     meta_ms = []
     if args.parts.startswith("tent"):
         parts = H.tent_parts(cfg.B, int(args.parts[4:]))
@@ -97,10 +98,9 @@ def main():
         parts = [int(x) for x in args.parts.split(",")]
     else:
         parts = int(args.parts)
-    for l in range(cfg.layers):
-        L = H.build_hier_layer(cfg, args.seed, l, pool, l * per_layer, nblk, progress=log, parts=parts)
-        layers.append(L)
-        qstreams.append(H.query_stream(cfg, args.seed, l, warmup + steps - 1))
+    pool, layers, _ = H.build_hier_model(cfg, args.seed, nblk, args.pool_flags, int(args.pool_budget_gib * 2**30),
+                                         progress=log, parts=parts)
+    qstreams = [H.query_stream(cfg, args.seed, l, warmup + steps - 1) for l in range(cfg.layers)]
     # metadata build (setup path), timed on its own for one layer
     L0 = layers[0]
     kv_one = torch.empty(cfg.Hkv * int(nblk[0]) * cfg.record_bytes, dtype=torch.uint8, device="cuda")
@@ -217,7 +217,8 @@ def main():
         "data": "synthetic",
         "config": {"workload": cfg.name, "batch": cfg.B, "q_heads": cfg.Hq, "kv_heads": cfg.Hkv, "head_dim": D,
                    "context": int(lens.max()), "block": cfg.blk, "topk_blocks": cfg.k, "cache_frac": cfg.cache_frac,
-                   "layers": cfg.layers, "drift": cfg.drift, "seed": args.seed},
+                   "layers": cfg.layers, "layers_with_own_dram_records": n_distinct, "drift": cfg.drift,
+                   "seed": args.seed},
         "roofline": dict(kernel=dominant, **roof[dominant]),
         "pipeline_ms": pipe,
         "rooflines_isolated": iso,

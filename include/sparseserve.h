@@ -220,8 +220,10 @@ ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t 
  * group overlaps the
  * scoring and the host resolve of the next: scoring, selection and
  * attention run on `stream`; the gathers run on two transfer streams the
- * library creates for this cache handle on first use (default priority;
- * groups alternate between them) and orders against `stream` with events.  Selections reach the host, and
+ * library creates once per device (default priority; groups alternate
+ * between them) and orders against `stream` with events.  Calls of
+ * ss_decode_layer take turns on a process-wide lock (they share those
+ * streams).  Selections reach the host, and
  * slots and miss rows reach the GPU, through the mapped host buffers (no
  * copy-engine transfers).  The host waits only for each group's selection;
  * everything after the last resolve is enqueued and the call returns
@@ -242,7 +244,7 @@ ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t 
  * recorded before scoring, after scoring, after selection (on `stream`),
  * before and after the gather (its transfer stream), before and after attention
  * (on `stream`) -- per-kernel timing.
- * Streams and events belong to the device current at the first call.
+ * Streams and events are created for the device current at the call.
  * On error nothing further is enqueued; a resolve error leaves the cache
  * unchanged for the groups not yet resolved. */
 typedef struct ss_layer_buffers {

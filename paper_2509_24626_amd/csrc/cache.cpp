@@ -146,21 +146,9 @@ struct ss_cache {
     int threads = 1;                          // workers used by resolve
     std::vector<std::vector<uint64_t>> mark;  // per worker: slot bitmap for ordering
     std::vector<std::vector<int32_t>> touched;  // per worker
-    void *exec = nullptr;                       // GPU-side step state (decode.cpp)
-    void (*exec_free)(void *) = nullptr;
-    ~ss_cache()
-    {
-        if (exec && exec_free) exec_free(exec);
-    }
 };
 
 namespace ss {
-void *cache_exec(ss_cache *c) { return c->exec; }
-void cache_set_exec(ss_cache *c, void *exec, void (*exec_free)(void *))
-{
-    c->exec = exec;
-    c->exec_free = exec_free;
-}
 int cache_batch(const ss_cache *c) { return c->B; }
 int cache_kv_heads(const ss_cache *c) { return c->Hkv; }
 }  // namespace ss

@@ -18,7 +18,9 @@
 // previous one drains (no launch gap, no idle tail on the link).  Every hand-off is
 // a kernel on a compute queue: no copy-engine transfer, whose cross-engine
 // synchronisation costs tens of microseconds per hand-off, is on the path.
+#include <mutex>
 #include <thread>
+#include <unordered_map>
 #include <vector>
 
 #include "internal.hpp"
@@ -30,48 +32,25 @@ ss_status launch_gather(const int32_t *miss, int64_t n_miss, const void *pool_ba
                         void *cache_base, const int64_t *cache_off, const int32_t *nblk, const int32_t *capacity,
                         int B, int Hkv, size_t record_bytes, const int32_t *copy_src, int32_t *copy_dst,
                         int64_t copy_n, hipStream_t s);
-void *cache_exec(ss_cache *c);
-void cache_set_exec(ss_cache *c, void *exec, void (*exec_free)(void *));
 int cache_batch(const ss_cache *c);
 int cache_kv_heads(const ss_cache *c);
 }  // namespace ss
 
 namespace {
 
+// Transfer streams and synchronisation events, one set per device for the
+// whole process (every layer's cache handle shares them; decode-step calls
+// take turns under g_exec_mu).  A set per handle would multiply streams over
+// the few hardware queues, and a transfer stream sharing a queue with the
+// caller's stream would serialise the pipeline.
 struct exec_state {
     hipStream_t xfer[2] = {nullptr, nullptr};  // groups alternate between them
     hipEvent_t start = nullptr;
     std::vector<hipEvent_t> sel_ready, gathered;
-    // device addresses of the caller's pinned host buffers (looked up once)
-    const void *host_key[3] = {nullptr, nullptr, nullptr};
-    void *host_dev[3] = {nullptr, nullptr, nullptr};
 };
 
-ss_status device_address(exec_state *e, int i, void *host, void **dev)
-{
-    if (e->host_key[i] != host) {
-        void *d = nullptr;
-        if (hipHostGetDevicePointer(&d, host, 0) != hipSuccess || !d) {
-            (void)hipGetLastError();
-            return ss::fail(SS_ERR_INVALID_ARG, "ss_decode_layer: host buffer %d is not pinned, mapped memory", i);
-        }
-        e->host_key[i] = host;
-        e->host_dev[i] = d;
-    }
-    *dev = e->host_dev[i];
-    return SS_OK;
-}
-
-void exec_free(void *p)
-{
-    exec_state *e = static_cast<exec_state *>(p);
-    for (hipEvent_t ev : e->sel_ready) (void)hipEventDestroy(ev);
-    for (hipEvent_t ev : e->gathered) (void)hipEventDestroy(ev);
-    if (e->start) (void)hipEventDestroy(e->start);
-    for (hipStream_t x : e->xfer)
-        if (x) (void)hipStreamDestroy(x);
-    delete e;
-}
+std::mutex g_exec_mu;
+std::unordered_map<int, exec_state *> g_exec;  // by device
 
 ss_status hip_check(hipError_t e, const char *what)
 {
@@ -79,19 +58,25 @@ ss_status hip_check(hipError_t e, const char *what)
     return SS_OK;
 }
 
-ss_status get_exec(ss_cache *c, int parts, exec_state **out)
+// called with g_exec_mu held
+ss_status get_exec(int parts, exec_state **out)
 {
-    exec_state *e = static_cast<exec_state *>(ss::cache_exec(c));
+    int dev = 0;
     ss_status st;
+    if ((st = hip_check(hipGetDevice(&dev), "hipGetDevice"))) return st;
+    exec_state *&e = g_exec[dev];
     if (!e) {
-        e = new exec_state;
-        if ((st = hip_check(hipStreamCreateWithFlags(&e->xfer[0], hipStreamNonBlocking), "create transfer stream")) ||
-            (st = hip_check(hipStreamCreateWithFlags(&e->xfer[1], hipStreamNonBlocking), "create transfer stream")) ||
-            (st = hip_check(hipEventCreateWithFlags(&e->start, hipEventDisableTiming), "create event"))) {
-            exec_free(e);
+        exec_state *n = new exec_state;
+        if ((st = hip_check(hipStreamCreateWithFlags(&n->xfer[0], hipStreamNonBlocking), "create transfer stream")) ||
+            (st = hip_check(hipStreamCreateWithFlags(&n->xfer[1], hipStreamNonBlocking), "create transfer stream")) ||
+            (st = hip_check(hipEventCreateWithFlags(&n->start, hipEventDisableTiming), "create event"))) {
+            for (hipStream_t x : n->xfer)
+                if (x) (void)hipStreamDestroy(x);
+            if (n->start) (void)hipEventDestroy(n->start);
+            delete n;
             return st;
         }
-        ss::cache_set_exec(c, e, exec_free);
+        e = n;
     }
     while ((int)e->sel_ready.size() < parts) {
         hipEvent_t a = nullptr, b = nullptr;
@@ -104,6 +89,19 @@ ss_status get_exec(ss_cache *c, int parts, exec_state **out)
         e->gathered.push_back(b);
     }
     *out = e;
+    return SS_OK;
+}
+
+// Looked up on every call (cheap): a cached translation could outlive the
+// host buffer it was taken for.
+ss_status device_address(void *host, void **dev)
+{
+    void *d = nullptr;
+    if (hipHostGetDevicePointer(&d, host, 0) != hipSuccess || !d) {
+        (void)hipGetLastError();
+        return ss::fail(SS_ERR_INVALID_ARG, "ss_decode_layer: a host buffer is not pinned, mapped memory");
+    }
+    *dev = d;
     return SS_OK;
 }
 
@@ -149,8 +147,9 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
             SS_CHECK_ARG(L->part_end[p] > (p ? L->part_end[p - 1] : 0),
                          "ss_decode_layer: part_end must be strictly increasing");
     }
+    std::lock_guard<std::mutex> lock(g_exec_mu);
     exec_state *ex = nullptr;
-    ss_status st = get_exec(L->cache, P, &ex);
+    ss_status st = get_exec(P, &ex);
     if (st) return st;
     hipStream_t s = ss::as_stream(stream);
     const size_t rec = (size_t)2 * L->blk * d * 2;
@@ -160,9 +159,9 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
     auto b_of = [&](int p) { return p == 0 ? 0 : (pe ? pe[p - 1] : (int)((int64_t)B * p / P)); };
 
     int32_t *sel_hd = nullptr, *slots_hd = nullptr, *miss_hd = nullptr;  // device views of the host buffers
-    if ((st = device_address(ex, 0, L->sel_host, (void **)&sel_hd)) ||
-        (st = device_address(ex, 1, L->slots_host, (void **)&slots_hd)) ||
-        (st = device_address(ex, 2, L->miss_host, (void **)&miss_hd)))
+    if ((st = device_address(L->sel_host, (void **)&sel_hd)) ||
+        (st = device_address(L->slots_host, (void **)&slots_hd)) ||
+        (st = device_address(L->miss_host, (void **)&miss_hd)))
         return st;
 
     // the transfer streams start after everything already on `stream`

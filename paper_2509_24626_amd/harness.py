@@ -231,3 +231,44 @@ def query_stream(cfg, seed, layer, steps, device="cuda"):
         q32, q = gen.drift(q32, cfg.drift, seed, layer, s)
         qs.append((q32, q))
     return qs
+
+
+# Pinned host memory the pool may take.  A process can pin about 64 GiB on
+# the MI355X hosts measured (the total over all allocation kinds); the rest
+# of this allowance is left for step buffers.
+POOL_BUDGET = 56 << 30
+
+
+def distinct_layers(cfg, nblk, budget=POOL_BUDGET):
+    """How many layers get DRAM records of their own: all of them if the
+    pool fits `budget`, else as many as fit.  Layer l then reads the records
+    of layer l mod n (it still has its own queries, selections, HBM cache and
+    misses, so the step's transfer volume is that of distinct layers)."""
+    _, per_layer = pool_layout(cfg, nblk)
+    if per_layer == 0:
+        return cfg.layers
+    return max(1, min(cfg.layers, budget // per_layer))
+
+
+def build_hier_model(cfg, seed, nblk, flags=0, budget=POOL_BUDGET, progress=None, parts=1):
+    """All cfg.layers layers over one DRAM pool (see distinct_layers).
+    Returns (pool, layers, n_distinct)."""
+    nblk = np.asarray(nblk, np.int32)
+    n = distinct_layers(cfg, nblk, budget)
+    _, per_layer = pool_layout(cfg, nblk)
+    pool = HostPool(max(1, per_layer * n), flags)
+    layers = []
+    try:
+        for l in range(cfg.layers):
+            if l < n:
+                L = build_hier_layer(cfg, seed, l, pool, l * per_layer, nblk, progress=progress, parts=parts)
+            else:
+                src = layers[l % n]
+                L = HierLayer(cfg, nblk, src.capacity, pool, src.pool_off_host, src.meta, parts)
+            layers.append(L)
+    except BaseException:
+        for L in layers:
+            L.close()
+        pool.close()
+        raise
+    return pool, layers, n

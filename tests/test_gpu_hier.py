@@ -32,6 +32,61 @@ def ss():
     return binding
 
 
+class Track:
+    """The oracle following sampled sequences of one GPU layer step by step
+    (its own metadata from the pool bytes, LRU cache, cache image)."""
+
+    def __init__(self, oracle_impl, cfg, L, pool, sample_b, name=""):
+        self.o, self.cfg, self.L, self.pool, self.name = oracle_impl, cfg, L, pool, name
+        Hkv = cfg.Hkv
+        self.sb = list(sample_b)
+        self.units = [b * Hkv + g for b in self.sb for g in range(Hkv)]
+        self.nb_s = L.nblk_host[self.sb]
+        cap_s = L.capacity[self.units]
+        self.meta = oracle_impl.build_metadata(pool.host, L.pool_off_host[self.units], self.nb_s, len(self.sb), Hkv,
+                                               cfg.nblk_max, cfg.blk, 128)
+        self.lru = oracle_impl.lru(len(self.sb), Hkv, self.nb_s, cap_s)
+        self.img_off = np.concatenate([[0], np.cumsum(cap_s.astype(np.int64))[:-1]]) * cfg.record_bytes
+        self.image = np.zeros(int(cap_s.sum()) * cfg.record_bytes + cfg.record_bytes, np.uint8)
+        self.pool_off = L.pool_off_host[self.units]
+        self.diverged = set()
+
+    def check(self, t, q):
+        """Compares the GPU layer's step t (already run and synchronised)."""
+        o, cfg, L, sb = self.o, self.cfg, self.L, self.sb
+        Hkv, k, G, rb = cfg.Hkv, cfg.k, cfg.G, cfg.record_bytes
+        qh = gu.u16(q)[sb]
+        S = o.score(qh, self.meta, self.nb_s, cfg.Hq, Hkv, cfg.nblk_max, 128)
+        osel = o.select(S, self.nb_s, k)
+        gsel = L.sel.cpu().numpy()[sb]
+        for (i, g) in gu.check_selection(gsel, osel, S, self.nb_s, k):
+            self.diverged.add((i, g))
+        oslots, omiss = self.lru.step(t, osel)
+        o.gather(omiss, self.pool.host, self.pool_off, self.image, self.img_off, rb, Hkv)
+        oout = o.attention(qh, self.image, self.img_off, oslots, Hkv, cfg.blk)
+        gslots = L.slots_h.numpy()[sb]
+        gmiss = L.miss_h.numpy()[:L.last_n_miss]
+        gout = L.out.cpu().numpy()[sb]
+        for i, b in enumerate(sb):
+            for g in range(Hkv):
+                if (i, g) in self.diverged:
+                    continue
+                u = b * Hkv + g
+                where = f"{self.name} t={t} b={b} g={g}"
+                np.testing.assert_array_equal(gslots[i, g], oslots[i, g], err_msg="slots " + where)
+                gm = gmiss[(gmiss[:, 0] == b) & (gmiss[:, 1] == g)]
+                om = omiss[(omiss[:, 0] == i) & (omiss[:, 1] == g)]
+                np.testing.assert_array_equal(gm[:, 2:], om[:, 2:], err_msg="misses " + where)
+                # every slot the selection uses holds the record the oracle gathered
+                base = int(L.cache_off_host[u])
+                region = L.cache[base:base + int(L.capacity[u]) * rb].cpu().numpy()
+                for s in oslots[i, g][oslots[i, g] >= 0]:
+                    off = int(self.img_off[i * Hkv + g] + s * rb)
+                    assert np.array_equal(region[s * rb:(s + 1) * rb], self.image[off:off + rb]), (where, s)
+                err = np.abs(gout[i, g * G:(g + 1) * G] - oout[i, g * G:(g + 1) * G]).max()
+                assert err <= gu.ATTN_TOL, (where, err)
+
+
 def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_diverged_frac=0.25, parts=1):
     from paper_2509_24626_amd import harness as H
     lens = synth.gen.lengths(cfg, seed)
@@ -44,60 +99,18 @@ def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_dive
         L = H.build_hier_layer(cfg, seed, layer, pool, 0, nblk, progress=lambda m: print("[gpu]", m, flush=True),
                                parts=parts)
         qs = H.query_stream(cfg, seed, layer, steps)
-        Hkv, k, G, rb = cfg.Hkv, cfg.k, cfg.G, cfg.record_bytes
-        sb = list(sample_b)
-        units = [b * Hkv + g for b in sb for g in range(Hkv)]
-        nb_s = nblk[sb]
-        cap_s = L.capacity[units]
-        # oracle state for the sampled sequences
-        meta_o = oracle_impl.build_metadata(pool.host, L.pool_off_host[units], nb_s, len(sb), Hkv, cfg.nblk_max,
-                                            cfg.blk, 128)
-        lru = oracle_impl.lru(len(sb), Hkv, nb_s, cap_s)
-        img_off = np.concatenate([[0], np.cumsum(cap_s.astype(np.int64))[:-1]]) * rb
-        image = np.zeros(int(cap_s.sum()) * rb + rb, np.uint8)
-        pool_off_abs = L.pool_off_host[units]
-        diverged = set()
+        tr = Track(oracle_impl, cfg, L, pool, sample_b, cfg.name)
         misses = []
         for t in range(steps + 1):
-            q32, q = qs[t]
-            L.step(t, q)
+            L.step(t, qs[t][1])
             torch.cuda.synchronize()
             misses.append(L.last_n_miss)
-            qh = gu.u16(q)[sb]
-            S = oracle_impl.score(qh, meta_o, nb_s, cfg.Hq, Hkv, cfg.nblk_max, 128)
-            osel = oracle_impl.select(S, nb_s, k)
-            gsel = L.sel.cpu().numpy()[sb]
-            now = gu.check_selection(gsel, osel, S, nb_s, k)
-            for (i, g) in now:
-                diverged.add((i, g))
-            oslots, omiss = lru.step(t, osel)
-            oracle_impl.gather(omiss, pool.host, pool_off_abs, image, img_off, rb, Hkv)
-            oout = oracle_impl.attention(qh, image, img_off, oslots, Hkv, cfg.blk)
-            gslots = L.slots_h.numpy()[sb]
-            gmiss = L.miss_h.numpy()[:L.last_n_miss]
-            gout = L.out.cpu().numpy()[sb]
-            for i, b in enumerate(sb):
-                for g in range(Hkv):
-                    if (i, g) in diverged:
-                        continue
-                    u = b * Hkv + g
-                    np.testing.assert_array_equal(gslots[i, g], oslots[i, g], err_msg=f"slots t={t} b={b} g={g}")
-                    gm = gmiss[(gmiss[:, 0] == b) & (gmiss[:, 1] == g)]
-                    om = omiss[(omiss[:, 0] == i) & (omiss[:, 1] == g)]
-                    np.testing.assert_array_equal(gm[:, 2:], om[:, 2:], err_msg=f"misses t={t} b={b} g={g}")
-                    # every slot the selection uses holds the record the oracle gathered
-                    base = int(L.cache_off_host[u])
-                    region = L.cache[base:base + int(L.capacity[u]) * rb].cpu().numpy()
-                    for s in oslots[i, g][oslots[i, g] >= 0]:
-                        o = int(img_off[i * Hkv + g] + s * rb)
-                        assert np.array_equal(region[s * rb:(s + 1) * rb], image[o:o + rb]), (t, b, g, s)
-                    err = np.abs(gout[i, g * G:(g + 1) * G] - oout[i, g * G:(g + 1) * G]).max()
-                    assert err <= gu.ATTN_TOL, (t, b, g, err)
-        rate = [m / (L.units * k) for m in misses]
+            tr.check(t, qs[t][1])
+        rate = [m / (L.units * cfg.k) for m in misses]
         print(f"[gpu] {cfg.name}: miss rate per step {[round(r, 3) for r in rate]}; "
-              f"diverged units {len(diverged)}/{len(units)}", flush=True)
-        assert len(diverged) <= max_diverged_frac * len(units)
-        assert misses[0] == sum(min(k, int(n)) for n in nblk) * Hkv  # cold cache: everything misses
+              f"diverged units {len(tr.diverged)}/{len(tr.units)}", flush=True)
+        assert len(tr.diverged) <= max_diverged_frac * len(tr.units)
+        assert misses[0] == sum(min(cfg.k, int(n)) for n in nblk) * cfg.Hkv  # cold cache: everything misses
         L.close()
         return rate
     finally:
@@ -146,6 +159,47 @@ def test_hier_gqa7_full_size_sampled(ss, oracle_impl):
     heads, 16384 blocks of 8 tokens, k=512, 15% cache, 8 steps)."""
     cfg = synth.get(4)
     lockstep(oracle_impl, cfg, seed=0, sample_b=[0, 47], steps=cfg.steps, parts=6)
+
+
+def test_layers32_ragged_full_size_sampled(ss, oracle_impl):
+    """The 32-layer ragged workload at full size (B=16, lengths U[8k, 64k],
+    k=128, 30% cache per layer, 8 drifting steps): every step runs all 32
+    layers in order; the oracle follows 2 sequences in each of 4 layers,
+    two of which read DRAM records shared with an earlier layer."""
+    from paper_2509_24626_amd import harness as H
+    cfg = synth.get(3)
+    seed = 0
+    nblk = (synth.gen.lengths(cfg, seed) // cfg.blk).astype(np.int32)
+    log = lambda m: print("[gpu]", m, flush=True)
+    pool, layers, n = H.build_hier_model(cfg, seed, nblk, progress=log, parts=H.tent_parts(cfg.B, 4))
+    try:
+        print(f"[gpu] {cfg.name}: {n} of {cfg.layers} layers with their own DRAM records", flush=True)
+        assert n < cfg.layers  # the 32 layers do not fit the pinned budget
+        sample = {0: [int(np.argmax(nblk)), 5], n - 1: [int(np.argmin(nblk)), 11], n: [0, 15],
+                  cfg.layers - 1: [3, 8]}
+        qs = [H.query_stream(cfg, seed, l, cfg.steps) for l in range(cfg.layers)]
+        tracks = {l: Track(oracle_impl, cfg, layers[l], pool, sb, f"layer {l}") for l, sb in sample.items()}
+        for t in range(cfg.steps + 1):
+            for l, L in enumerate(layers):
+                L.step(t, qs[l][t][1])
+            torch.cuda.synchronize()
+            for l, tr in tracks.items():
+                tr.check(t, qs[l][t][1])
+            rates = [L.last_n_miss / (L.units * cfg.k) for L in layers]
+            print(f"[gpu] step {t}: miss rate over layers {min(rates):.3f}..{max(rates):.3f}", flush=True)
+            if t == 0:
+                assert all(L.last_n_miss == sum(min(cfg.k, int(x)) for x in nblk) * cfg.Hkv for L in layers)
+        units = sum(len(tr.units) for tr in tracks.values())
+        div = sum(len(tr.diverged) for tr in tracks.values())
+        print(f"[gpu] diverged units {div}/{units}", flush=True)
+        assert div <= 0.25 * units
+        # aliased layers read the same DRAM records but keep caches of their own
+        assert layers[n].pool_off_host[0] == layers[0].pool_off_host[0]
+        assert layers[n].cache.data_ptr() != layers[0].cache.data_ptr()
+    finally:
+        for L in layers:
+            L.close()
+        pool.close()
 
 
 def test_gather_bytes_and_range_checks(ss):
