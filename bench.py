@@ -53,6 +53,12 @@ def parse():
     ap.add_argument("--cpu-steps", type=int, default=8, help="timed steps in the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--pool-flags", type=int, default=0, help="0 coherent, 1 non-coherent pinned pool")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB copy kernel (the scale for HBM traffic counters) and exit")
+    ap.add_argument("--summarize-pmc", nargs=4, metavar=("FETCH", "WRITE", "COPY_FETCH", "COPY_WRITE"),
+                    help="rocprofv3 --pmc output folders of this script (FETCH_SIZE, WRITE_SIZE) and of "
+                         "--calibrate-copy; prints the traffic summary and exits (no GPU)")
+    ap.add_argument("--bench-json", help="with --summarize-pmc: the JSON line the profiled run printed")
     ap.add_argument("--pool-budget-gib", type=float, default=56.0,
                     help="pinned DRAM for KV records; layers beyond it reuse earlier layers' records")
     return ap.parse_args()
@@ -60,6 +66,12 @@ def parse():
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(args)
+        return
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU: the decode path has no cross-GPU step (every (sequence, KV head) "
@@ -181,10 +193,12 @@ def main():
     gather_bytes = float(n_miss.sum()) / steps * cfg.record_bytes
     busy_ms = pipe["link_busy"] * len(layers)
     ach = gather_bytes / (busy_ms * 1e-3) / 1e9 if busy_ms > 0 else 0.0
+    key = (cfg.name, args.seed, steps, warmup, tuple(layers[0].part_sizes))
     roof = {"gather": {"bound": "host-link", "achieved": round(ach, 2), "peak": round(LINK_PEAK_GBS, 2),
                        "unit": "GB/s", "frac": round(ach / LINK_PEAK_GBS, 4), "bytes_per_step": int(gather_bytes),
                        "link_busy_ms_per_step": round(busy_ms, 4), "launches_per_step": len(layers) * P,
-                       "ms_per_launch": round(float(np.mean(gather_launch_ms)), 4), "traffic": None}}
+                       "ms_per_launch": round(float(np.mean(gather_launch_ms)), 4),
+                       "traffic": traffic("gather", key)}}
     dominant = "gather"  # pipeline_ms shows the link busy for most of the step
     tokens = cfg.B * steps
     value = tokens / wall
@@ -196,6 +210,8 @@ def main():
     # GPU), on the last timed step's data: the HBM kernels' own rates, which
     # the overlapped step hides behind the host-link gather.
     iso = isolated_rates(cfg, layers[0], qstreams[0][warmup + steps - 1][1], ss, torch)
+    for name in iso:
+        iso[name]["traffic"] = traffic(name, key)
 
     # ------------------------------------------------------ CPU baseline
     cpu = None
@@ -235,6 +251,134 @@ def main():
     for L in layers:
         L.close()
     pool.close()
+
+
+# ------------------------------------------------------- HBM traffic
+# Measured HBM bytes of the step's kernels: two rocprofv3 --pmc runs of this
+# script with default arguments (FETCH_SIZE, then WRITE_SIZE, KiB per
+# dispatch), each counter scaled by what it reads for a plain copy of known
+# size (--calibrate-copy), written by --summarize-pmc.  A figure is reported
+# only for the workload and arguments it was taken with, and only while the
+# sources of its kernel hash as they did then; otherwise traffic is null.
+KERNEL_SOURCES = {
+    "gather": ["gather.hip", "decode.cpp"],
+    "score": ["score.hip"],
+    "topk": ["topk.hip"],
+    "attention": ["attention.hip"],
+}
+# hierarchical 128k-context layer, seed 0, 16 timed steps after 1 warm-up, groups 2,9,22,20,9,2
+_KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 16, 1, [2, 9, 22, 20, 9, 2]]
+TRAFFIC = {
+    "gather": {"key": _KEY, "digest": "6bd3251b3905aab8", "bytes": 260451784, "fetch": 131055560,
+               "write": 129396224},
+    "score": {"key": _KEY, "digest": "8d78773623e12ba9", "bytes": 2170171879, "fetch": 2152767879,
+              "write": 17404000},
+    "topk": {"key": _KEY, "digest": "8f6b9786eb7729ab", "bytes": 17254011, "fetch": 16991867, "write": 262144},
+    "attention": {"key": _KEY, "digest": "e242170c7670baf1", "bytes": 539115813, "fetch": 538067237,
+                  "write": 1048576},
+}
+
+
+def source_digest(kernel):
+    import hashlib
+    h = hashlib.sha256()
+    base = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2509_24626_amd", "csrc")
+    for f in KERNEL_SOURCES[kernel]:
+        with open(os.path.join(base, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic(kernel, key):
+    rec = TRAFFIC.get(kernel)
+    norm = lambda k: (k[0], int(k[1]), int(k[2]), int(k[3]), tuple(int(x) for x in k[4]))
+    if not rec or norm(rec["key"]) != norm(key):
+        return None
+    if rec["digest"] != source_digest(kernel):
+        return None
+    return rec["bytes"]
+
+
+def calibrate_copy(reps=5):
+    """A plain copy of known size for scaling the traffic counters: 1 GiB
+    read and 1 GiB written per launch (an elementwise multiply by 1)."""
+    import torch
+    n = 1 << 28
+    src = torch.empty(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    src.fill_(1.0)
+    for _ in range(reps):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": n * 4, "launches": reps}), flush=True)
+
+
+def _pmc_rows(folder, counter):
+    """Per-dispatch (kernel name, grid size, value) of one counter, in
+    dispatch order, from a rocprofv3 csv output folder."""
+    import csv
+    import glob
+    files = sorted(glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True))
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {folder}")
+    rows = {}
+    for f in files:
+        with open(f, newline="") as fh:
+            for r in csv.DictReader(fh):
+                if r.get("Counter_Name") != counter:
+                    continue
+                did = int(r["Dispatch_Id"])
+                name, grid, val = r["Kernel_Name"], int(r.get("Grid_Size", 0) or 0), float(r["Counter_Value"])
+                if did in rows:
+                    val += rows[did][2]
+                rows[did] = (name, grid, val)
+    return [rows[k] for k in sorted(rows)]
+
+
+def summarize_pmc(args):
+    fetch_dir, write_dir, cf_dir, cw_dir = args.summarize_pmc
+    with open(args.bench_json) as fh:
+        bench = json.loads([ln for ln in fh if ln.startswith("{")][-1])
+    scale = {}
+    for c, folder in (("FETCH_SIZE", cf_dir), ("WRITE_SIZE", cw_dir)):
+        vals = [v for n, _, v in _pmc_rows(folder, c) if "Mul" in n]
+        if not vals:
+            raise SystemExit(f"no copy kernel dispatches in {folder}")
+        scale[c] = (1 << 30) / (float(np.median(vals)) * 1024)
+    P = len(bench["parts"]) * bench["config"]["layers"]
+    steps, warmup = bench["steps"], bench["warmup"]
+    out = {}
+    lines = []
+    for c, folder in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
+        rows = _pmc_rows(folder, c)
+        g = [v for n, _, v in rows if "gather_kernel" in n]
+        assert len(g) == (warmup + steps) * P, (len(g), warmup, steps, P)
+        timed = g[warmup * P:]
+        per_step = sum(timed) / steps * 1024 * scale[c]
+        out.setdefault("gather", {})[c] = per_step
+        for name, tag in (("score", "score_kernel"), ("topk", "topk_kernel"), ("attention", "attn_kernel")):
+            # the isolated full-batch launches are each kernel's last 10 dispatches
+            vals = [v for n, _, v in rows if tag in n][-10:]
+            out.setdefault(name, {})[c] = float(np.median(vals)) * 1024 * scale[c]
+    key = [bench["config"]["workload"], bench["config"]["seed"], steps, warmup, bench["parts"]]
+    algo = {"gather": bench["roofline"]["bytes_per_step"]}
+    for name in ("score", "topk", "attention"):
+        algo[name] = bench["rooflines_isolated"][name]["bytes_per_launch"]
+    lines.append(f"copy-kernel scale: FETCH_SIZE x{scale['FETCH_SIZE']:.4f}, WRITE_SIZE x{scale['WRITE_SIZE']:.4f}")
+    lines.append("")
+    lines.append("| kernel | unit | fetched bytes | written bytes | traffic | algorithmic bytes | traffic / algorithmic |")
+    lines.append("|---|---|---|---|---|---|---|")
+    table = {}
+    for name, v in out.items():
+        t = v["FETCH_SIZE"] + v["WRITE_SIZE"]
+        unit = "per step (all gather launches)" if name == "gather" else "per launch (isolated, full batch)"
+        lines.append(f"| {name} | {unit} | {v['FETCH_SIZE']:.4g} | {v['WRITE_SIZE']:.4g} | {t:.4g} | {algo[name]:.4g} "
+                     f"| {t / algo[name]:.3f} |")
+        table[name] = {"key": key, "digest": source_digest(name), "bytes": int(round(t)),
+                       "fetch": int(round(v["FETCH_SIZE"])), "write": int(round(v["WRITE_SIZE"]))}
+    print("\n".join(lines))
+    print()
+    print("TRAFFIC = " + json.dumps(table, indent=1))
 
 
 def isolated_rates(cfg, L, q, ss, torch, reps=10):
