@@ -384,8 +384,9 @@ def summarize_pmc(args):
 def isolated_rates(cfg, L, q, ss, torch, reps=10):
     """Median duration of score, top-k and attention over the full batch,
     each launched alone after a cache flush, as a fraction of the HBM peak.
-    HIP events bracket each launch, so the figure includes the launch's
-    dispatch latency (a few microseconds)."""
+    The timing events are attached to the kernel dispatch itself
+    (ss_time_next_kernel), so they bracket the kernel's execution without
+    the queue's dispatch latency."""
     B, Hq, Hkv, k = cfg.B, cfg.Hq, cfg.Hkv, cfg.k
     nb = L.nblk_host
     blocks = int(nb.sum()) * Hkv
@@ -412,9 +413,10 @@ def isolated_rates(cfg, L, q, ss, torch, reps=10):
         for _ in range(reps):
             flush.sum()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            fn()
+            e0.record()  # creates the events
             e1.record()
+            ss.ss_time_next_kernel(e0, e1)
+            fn()
             torch.cuda.synchronize()
             ts.append(e0.elapsed_time(e1))
         ms = float(np.median(ts))
@@ -464,6 +466,14 @@ def cpu_baseline(cfg, pool, L, qs, nblk, args, warmup):
         t0 = time.perf_counter()
         list(ex.map(lambda b: [step(b, states[b], s) for s in range(1, nsteps + 1)], range(nseq)))
         wall = time.perf_counter() - t0
+    # the same steps on one thread, for a few fresh sequences
+    n1 = min(4, nseq)
+    states1 = [prepare(b) for b in range(n1)]
+    t0 = time.perf_counter()
+    for b in range(n1):
+        for s in range(1, nsteps + 1):
+            step(b, states1[b], s)
+    wall1 = time.perf_counter() - t0
     cpu_model = ""
     try:
         for line in open("/proc/cpuinfo"):
@@ -476,7 +486,9 @@ def cpu_baseline(cfg, pool, L, qs, nblk, args, warmup):
             "sample": f"{nseq} of {cfg.B} sequences (all {Hkv} KV heads each) x {nsteps} decode steps of layer 0 "
                       f"after an untimed cache-fill step; score, select, LRU resolve, gather, attention; "
                       f"{wall:.2f} s wall, {threads} threads, one sequence per thread",
-            "cpu": cpu_model}
+            "cpu": cpu_model,
+            "single_thread": {"value": round(n1 * nsteps / wall1, 3), "unit": "tokens/s", "cores": 1,
+                              "sample": f"{n1} sequences x {nsteps} steps on one thread, {wall1:.2f} s"}}
 
 
 if __name__ == "__main__":

@@ -83,6 +83,19 @@ const char *ss_last_error(void);
 ss_status ss_host_alloc_mapped(size_t bytes, unsigned flags, void **host_ptr, void **dev_ptr);
 ss_status ss_host_free(void *host_ptr);
 
+/* Measurement hook (not part of the method).  The next kernel that the
+ * calling thread launches through this library -- the scoring, top-k,
+ * gather, attention or metadata kernel of the next call that launches one;
+ * for a split attention, its first kernel only -- records `start_event`
+ * (may be NULL) when it starts executing and `stop_event` (may be NULL)
+ * when it finishes, as hipExtLaunchKernel does: kernel execution time
+ * without the queue's dispatch latency.  Events are hipEvent_t created by
+ * the caller.  The setting is per thread and is consumed by that one
+ * launch; ss_time_next_kernel(NULL, NULL) cancels it.  ss_decode_layer
+ * attaches its gather timing events (see below) the same way.  Always
+ * returns SS_OK. */
+ss_status ss_time_next_kernel(void *start_event, void *stop_event);
+
 /* --------------------------------------------------------------- metadata
  * Block metadata is the bounding cuboid of the block's keys: the
  * channel-wise minimum (lo) and maximum (hi) of K over the blk tokens
@@ -240,10 +253,11 @@ ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t 
  * read).  cache_off_dev = ss_cache_region_offsets, copied to the device.
  * After the call, miss_host rows [0, *n_miss) hold the step's misses in
  * unit order (as one ss_cache_resolve would list them).
- * events: NULL, or 7*parts hipEvent_t; for group p, events[7p+0..6] are
- * recorded before scoring, after scoring, after selection (on `stream`),
- * before and after the gather (its transfer stream), before and after attention
- * (on `stream`) -- per-kernel timing.
+ * events: NULL, or 7*parts hipEvent_t (any entry may be NULL); for group p,
+ * events[7p+0..2] are recorded on `stream` before scoring, after scoring
+ * and after selection, events[7p+3..4] are attached to the gather kernel
+ * itself (its start and end of execution, as ss_time_next_kernel does), and
+ * events[7p+5..6] are recorded on `stream` before and after attention.
  * Streams and events are created for the device current at the call.
  * On error nothing further is enqueued; a resolve error leaves the cache
  * unchanged for the groups not yet resolved. */

@@ -49,6 +49,7 @@ _SIGNATURES = {
     "ss_last_error": (ctypes.c_char_p, []),
     "ss_host_alloc_mapped": (_i32, [_sz, ctypes.c_uint, _vp, _vp]),
     "ss_host_free": (_i32, [_vp]),
+    "ss_time_next_kernel": (_i32, [_vp, _vp]),
     "ss_build_metadata": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),
     "ss_score_blocks": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),
     "ss_select_topk": (_i32, [_vp, _vp, _i32, _i32, _i32, _i32, _vp, _vp]),
@@ -135,6 +136,13 @@ def ss_host_alloc_mapped(nbytes, flags=0):
 
 def ss_host_free(host_address):
     _check(lib().ss_host_free(host_address))
+
+
+def ss_time_next_kernel(start_event=None, stop_event=None):
+    """Attach timing events to the next kernel this thread launches through
+    the library (torch.cuda.Event objects or raw hipEvent_t values)."""
+    ev = lambda e: None if e is None else (e if isinstance(e, int) else e.cuda_event)
+    _check(lib().ss_time_next_kernel(ev(start_event), ev(stop_event)))
 
 
 def ss_build_metadata(kv_base, unit_off, nblk, B, Hkv, nblk_max, blk, d, meta, stream=None):

@@ -311,9 +311,9 @@ extern "C" ss_status ss_sparse_attention(const void *q, const void *kv_base, con
     const uint8_t *kv = static_cast<const uint8_t *>(kv_base);
     float *ws = static_cast<float *>(workspace);
     switch (blk) {
-    case 8: attn_kernel<8><<<grid, dim3(256), 0, s>>>(qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
-    case 16: attn_kernel<16><<<grid, dim3(256), 0, s>>>(qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
-    default: attn_kernel<32><<<grid, dim3(256), 0, s>>>(qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
+    case 8: ss::launch(attn_kernel<8>, grid, dim3(256), s, qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
+    case 16: ss::launch(attn_kernel<16>, grid, dim3(256), s, qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
+    default: ss::launch(attn_kernel<32>, grid, dim3(256), s, qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
     }
     ss_status st = ss::check_launch("ss_sparse_attention");
     if (st != SS_OK || sp.splits == 1) return st;

@@ -200,12 +200,18 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
         st = ss_cache_resolve_range(L->cache, step, b0, b1, L->sel_host + row0, k, L->slots_host + row0,
                                     L->miss_host + 4 * total, L->miss_cap - total, &np);
         if (st) return st;
-        if ((st = record(events, 7 * p + 3, x))) return st;
+        // the gather's timing events ride on its dispatch (kernel execution only)
+        hipEvent_t g0 = events ? reinterpret_cast<hipEvent_t>(events[7 * p + 3]) : nullptr;
+        hipEvent_t g1 = events ? reinterpret_cast<hipEvent_t>(events[7 * p + 4]) : nullptr;
+        ss::set_kernel_timing(g0, g1);
         st = ss::launch_gather(miss_hd + 4 * total, np, L->pool, L->pool_off_dev, L->cache_base, L->cache_off_dev,
                                L->nblk_dev, L->capacity_dev, B, Hkv, rec, slots_hd + row0, L->slots_dev + row0,
                                (int64_t)Bp * rows_per_seq, x);
+        const ss::kernel_timing unused = ss::take_kernel_timing();  // set if nothing was launched
         if (st) return st;
-        if ((st = record(events, 7 * p + 4, x))) return st;
+        if ((unused.start && (st = hip_check(hipEventRecord(unused.start, x), "record timing event"))) ||
+            (unused.stop && (st = hip_check(hipEventRecord(unused.stop, x), "record timing event"))))
+            return st;
         if ((st = hip_check(hipEventRecord(ex->gathered[p], x), "record")) ||
             (st = hip_check(hipStreamWaitEvent(s, ex->gathered[p], 0), "order attention after gather")))
             return st;

@@ -72,7 +72,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const int4 *__restrict__ mi
 }
 
 template <int CH>
-void launch(const int4 *miss, int64_t n_miss, const uint8_t *pool, const int64_t *pool_off, uint8_t *cache,
+void launch_variant(const int4 *miss, int64_t n_miss, const uint8_t *pool, const int64_t *pool_off, uint8_t *cache,
             const int64_t *cache_off, const int32_t *nblk, const int32_t *cap, int B, int Hkv,
             const int32_t *copy_src, int32_t *copy_dst, int64_t copy_n, hipStream_t s)
 {
@@ -81,9 +81,8 @@ void launch(const int4 *miss, int64_t n_miss, const uint8_t *pool, const int64_t
     const int64_t max_blocks = 64;
     if (blocks > max_blocks) blocks = max_blocks;
     if (blocks < 1) blocks = 1;
-    gather_kernel<CH, RPI><<<dim3((unsigned)blocks), dim3(256), 0, s>>>(miss, n_miss, pool, pool_off, cache,
-                                                                         cache_off, nblk, cap, B, Hkv, copy_src,
-                                                                         copy_dst, copy_n);
+    ss::launch(gather_kernel<CH, RPI>, dim3((unsigned)blocks), dim3(256), s, miss, n_miss, pool, pool_off, cache,
+               cache_off, nblk, cap, B, Hkv, copy_src, copy_dst, copy_n);
 }
 
 }  // namespace
@@ -102,9 +101,9 @@ ss_status launch_gather(const int32_t *miss, int64_t n_miss, const void *pool_ba
     const uint8_t *p = static_cast<const uint8_t *>(pool_base);
     uint8_t *c = static_cast<uint8_t *>(cache_base);
     switch (record_bytes) {
-    case 4096: launch<1>(m, n_miss, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, copy_src, copy_dst, copy_n, s); break;
-    case 8192: launch<2>(m, n_miss, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, copy_src, copy_dst, copy_n, s); break;
-    default: launch<4>(m, n_miss, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, copy_src, copy_dst, copy_n, s); break;
+    case 4096: launch_variant<1>(m, n_miss, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, copy_src, copy_dst, copy_n, s); break;
+    case 8192: launch_variant<2>(m, n_miss, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, copy_src, copy_dst, copy_n, s); break;
+    default: launch_variant<4>(m, n_miss, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, copy_src, copy_dst, copy_n, s); break;
     }
     return check_launch("ss_gather_blocks");
 }

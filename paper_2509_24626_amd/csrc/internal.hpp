@@ -3,6 +3,7 @@
 // builtins.  Not part of the public interface.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdarg>
@@ -26,6 +27,28 @@ constexpr int kMaxGroup = 16;
 constexpr int kMaxBlocks = 65536;
 
 inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+// Start/stop events that a measurement attaches to the next kernel the
+// calling thread launches (ss_time_next_kernel); the launch takes and
+// clears them.
+struct kernel_timing {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+kernel_timing take_kernel_timing();
+void set_kernel_timing(hipEvent_t start, hipEvent_t stop);
+
+// Launches `k`, attaching this thread's pending timing events, if any, to
+// the dispatch itself, so they bracket the kernel's execution and not the
+// queue's dispatch latency.
+template <typename... P, typename... A>
+inline void launch(void (*k)(P...), dim3 grid, dim3 block, hipStream_t s, A... args)
+{
+    const kernel_timing t = take_kernel_timing();
+    if (t.start || t.stop)
+        hipExtLaunchKernelGGL(k, grid, block, 0, s, t.start, t.stop, 0, static_cast<P>(args)...);
+    else
+        k<<<grid, block, 0, s>>>(static_cast<P>(args)...);
+}
 
 }  // namespace ss
 

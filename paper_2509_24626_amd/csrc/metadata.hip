@@ -112,9 +112,9 @@ extern "C" ss_status ss_build_metadata(const void *kv_base, const int64_t *unit_
     const uint8_t *kv = static_cast<const uint8_t *>(kv_base);
     uint16_t *m = static_cast<uint16_t *>(meta);
     switch (blk) {
-    case 8: meta_kernel<8><<<dim3((unsigned)grid), dim3(256), 0, s>>>(kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
-    case 16: meta_kernel<16><<<dim3((unsigned)grid), dim3(256), 0, s>>>(kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
-    default: meta_kernel<32><<<dim3((unsigned)grid), dim3(256), 0, s>>>(kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
+    case 8: ss::launch(meta_kernel<8>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
+    case 16: ss::launch(meta_kernel<16>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
+    default: ss::launch(meta_kernel<32>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
     }
     return ss::check_launch("ss_build_metadata");
 }

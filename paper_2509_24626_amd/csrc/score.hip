@@ -128,9 +128,8 @@ ss_status launch_score(const void *q, const void *meta, const int32_t *nblk, int
     const int64_t grid = (int64_t)B * Hkv * chunks;
     if (grid == 0) return SS_OK;
     SS_CHECK_SUPPORTED(grid <= 0x7FFFFFFF, "score: grid too large");
-    score_kernel<<<dim3((unsigned)grid), dim3(256), 0, s>>>(static_cast<const uint16_t *>(q),
-                                                             static_cast<const uint8_t *>(meta), nblk, Hq, Hkv,
-                                                             Hq / Hkv, nblk_max, chunks, scores);
+    ss::launch(score_kernel, dim3((unsigned)grid), dim3(256), s, static_cast<const uint16_t *>(q),
+               static_cast<const uint8_t *>(meta), nblk, Hq, Hkv, Hq / Hkv, nblk_max, chunks, scores);
     return check_launch("ss_score_blocks");
 }
 

@@ -5,6 +5,7 @@
 
 namespace {
 thread_local std::string g_last_error;
+thread_local ss::kernel_timing g_timing;
 }
 
 namespace ss {
@@ -21,6 +22,15 @@ ss_status fail(ss_status code, const char *fmt, ...)
 }
 
 void clear_error() { g_last_error.clear(); }
+
+kernel_timing take_kernel_timing()
+{
+    kernel_timing t = g_timing;
+    g_timing = kernel_timing{};
+    return t;
+}
+
+void set_kernel_timing(hipEvent_t start, hipEvent_t stop) { g_timing = kernel_timing{start, stop}; }
 
 ss_status check_launch(const char *what)
 {
@@ -73,6 +83,12 @@ ss_status ss_host_alloc_mapped(size_t bytes, unsigned flags, void **host_ptr, vo
     *host_ptr = h;
     *dev_ptr = d;
     ss::clear_error();
+    return SS_OK;
+}
+
+ss_status ss_time_next_kernel(void *start_event, void *stop_event)
+{
+    ss::set_kernel_timing(reinterpret_cast<hipEvent_t>(start_event), reinterpret_cast<hipEvent_t>(stop_event));
     return SS_OK;
 }
 

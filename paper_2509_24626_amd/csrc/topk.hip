@@ -191,10 +191,10 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float *__restrict__ scor
 }
 
 template <int NT, int R>
-void launch(const float *scores, const int32_t *nblk, int units, int Hkv, int nblk_max, int k, int32_t *sel,
+void launch_variant(const float *scores, const int32_t *nblk, int units, int Hkv, int nblk_max, int k, int32_t *sel,
             int32_t *mirror, hipStream_t s)
 {
-    topk_kernel<NT, R><<<dim3(units), dim3(NT), 0, s>>>(scores, nblk, Hkv, nblk_max, k, sel, mirror);
+    ss::launch(topk_kernel<NT, R>, dim3(units), dim3(NT), s, scores, nblk, Hkv, nblk_max, k, sel, mirror);
 }
 
 }  // namespace
@@ -207,12 +207,12 @@ ss_status launch_topk(const float *scores, const int32_t *nblk, int B, int Hkv, 
 {
     const int units = B * Hkv;
     if (units == 0) return SS_OK;
-    if (nblk_max <= 256 * 4) launch<256, 4>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
-    else if (nblk_max <= 256 * 8) launch<256, 8>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
-    else if (nblk_max <= 256 * 16) launch<256, 16>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
-    else if (nblk_max <= 256 * 32) launch<256, 32>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
-    else if (nblk_max <= 512 * 32) launch<512, 32>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
-    else launch<1024, 64>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    if (nblk_max <= 256 * 4) launch_variant<256, 4>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 256 * 8) launch_variant<256, 8>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 256 * 16) launch_variant<256, 16>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 256 * 32) launch_variant<256, 32>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 512 * 32) launch_variant<512, 32>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else launch_variant<1024, 64>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
     return check_launch("ss_select_topk");
 }
 

@@ -200,6 +200,36 @@ def test_runs_are_bitwise_deterministic(ss):
     np.testing.assert_array_equal(res[0][1].view(np.uint32), res[1][1].view(np.uint32))
 
 
+def test_kernel_timing_hook(ss):
+    """ss_time_next_kernel: the attached events bracket exactly one kernel
+    (within the stream-recorded bracket around the same call), the call's
+    result is unchanged, and the setting is consumed by that launch."""
+    w = workload("gqa7-blk8-ragged")
+    meta = gu.run_metadata(ss, w)
+    scores = torch.empty(w.B, w.Hkv, w.nblk_max, dtype=torch.float32, device="cuda")
+    ref = torch.empty_like(scores)
+    ss.ss_score_blocks(w.q, meta, w.nblk, w.B, w.Hq, w.Hkv, w.nblk_max, w.d, ref)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in ev:
+        e.record()
+    torch.cuda.synchronize()
+    ev[0].record()
+    ss.ss_time_next_kernel(ev[1], ev[2])
+    ss.ss_score_blocks(w.q, meta, w.nblk, w.B, w.Hq, w.Hkv, w.nblk_max, w.d, scores)
+    ev[3].record()
+    torch.cuda.synchronize()
+    inner, outer = ev[1].elapsed_time(ev[2]), ev[0].elapsed_time(ev[3])
+    print(f"[gpu] kernel {inner * 1e3:.1f} us inside a {outer * 1e3:.1f} us bracket", flush=True)
+    assert 0 < inner <= outer
+    assert ev[0].elapsed_time(ev[1]) >= 0 and ev[2].elapsed_time(ev[3]) >= 0
+    valid_rows_equal(scores.cpu().numpy(), ref.cpu().numpy(), w.nblk_host)
+    # consumed: the next launch does not touch the events again
+    ss.ss_score_blocks(w.q, meta, w.nblk, w.B, w.Hq, w.Hkv, w.nblk_max, w.d, scores)
+    torch.cuda.synchronize()
+    assert ev[1].elapsed_time(ev[2]) == inner
+    ss.ss_time_next_kernel(None, None)
+
+
 def test_llama3_8b_shape_full_size(ss, oracle_impl):
     """The Llama-3-8B-shaped single layer at full size (B=32, 32/8 heads,
     32k context, blk 16, k=128, 64 planted blocks per head), every unit
