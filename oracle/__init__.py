@@ -47,8 +47,10 @@ def load(path):
     L.oracle_lru_export.argtypes = [vp, vp, vp]
     L.oracle_gather.argtypes = [vp, i64, vp, vp, vp, vp, sz, i32]
     L.oracle_attention.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, ctypes.c_double, vp]
+    L.oracle_append.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, vp, vp]
+    L.oracle_save.argtypes = [vp, i32, vp, i32, i32, i32, i32, vp, vp, vp]
     for f in ("oracle_build_metadata", "oracle_score", "oracle_select", "oracle_lru_step",
-              "oracle_gather", "oracle_attention"):
+              "oracle_gather", "oracle_attention", "oracle_append", "oracle_save"):
         getattr(L, f).restype = i32
     return L
 
@@ -133,6 +135,36 @@ class Oracle:
         _check(self.L.oracle_attention(_addr(q), _addr(base), _addr(region_off), _addr(slots), B, Hq, Hkv, d,
                                        blk, k, float(scale), _addr(out)), "attention")
         return out
+
+    # O6
+    def append(self, new_kv, len_, nblk, blk, nblk_max, open_rec, meta):
+        """new_kv uint16 [B][Hkv][2][d]; len_, nblk int32 [B] (updated in
+        place); open_rec uint16 [B][Hkv][2*blk*d] and meta uint16
+        [B][Hkv][nblk_max][2][d] (updated in place)."""
+        new_kv = _c(new_kv, np.uint16)
+        B, Hkv, _, d = new_kv.shape
+        for a, dt in ((len_, np.int32), (nblk, np.int32), (open_rec, np.uint16), (meta, np.uint16)):
+            assert isinstance(a, np.ndarray) and a.dtype == dt and a.flags.c_contiguous
+        rc = self.L.oracle_append(_addr(new_kv), _addr(len_), _addr(nblk), B, Hkv, blk, d, nblk_max,
+                                  _addr(open_rec), _addr(meta))
+        if rc == 2:
+            raise OverflowError("a filled block lies past nblk_max")
+        _check(rc, "append")
+
+    # O7
+    def save(self, new_kv, len_, blk, pool, pool_off, pool_blocks):
+        """new_kv uint16 [B][n_new][Hkv][2][d]; len_ int32 [B] (not changed);
+        pool: host memory (array or address) updated in place."""
+        new_kv = _c(new_kv, np.uint16)
+        B, n_new, Hkv, _, d = new_kv.shape
+        len_ = _c(len_, np.int32)
+        pool_off = _c(pool_off, np.int64)
+        pool_blocks = _c(pool_blocks, np.int32)
+        rc = self.L.oracle_save(_addr(new_kv), n_new, _addr(len_), B, Hkv, blk, d, _addr(pool), _addr(pool_off),
+                                _addr(pool_blocks))
+        if rc == 2:
+            raise OverflowError("a token lies past the unit's pool blocks")
+        _check(rc, "save")
 
     def lru(self, B, Hkv, nblk, cap):
         return LRU(self.L, B, Hkv, nblk, cap)

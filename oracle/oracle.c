@@ -2,7 +2,8 @@
  * CPU oracle for the decode-step hot path of SparseServe (arXiv 2509.24626):
  * block metadata, block criticality scoring, top-k block selection, the LRU
  * HBM block cache, the miss gather and sparse attention over the selected
- * blocks.
+ * blocks; and on the saving side, appending new tokens to the open blocks
+ * (with metadata when a block fills) and saving them to the DRAM pool.
  *
  * TEST INFRASTRUCTURE ONLY.  Nothing in the product library calls, links or
  * loads this file; only the tests, the smoke check and the benchmark's CPU
@@ -431,5 +432,100 @@ int oracle_attention(const uint16_t *q, const void *base, const int64_t *region_
             for (int c = 0; c < d; ++c) o[c] = (float)acc[c];
         }
     free(z); free(kv_of); free(t_of); free(acc);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------
+ * Writing one token into a block record: the K row at position p and the V
+ * column at position p (V tiles are channel-major), in the record layout
+ * stated at the top of this file.  kv holds the token's K (d values) then
+ * its V (d values).
+ * ---------------------------------------------------------------------- */
+static void put_token(uint16_t *rec, int blk, int d, int p, const uint16_t *kv)
+{
+    for (int c = 0; c < d; ++c)
+        rec[p * d + c] = kv[c];
+    for (int c = 0; c < d; ++c)
+        rec[blk * d + c * blk + p] = kv[d + c];
+}
+
+/* ------------------------------------------------------------------------
+ * O6  Appending a decode step's new tokens in HBM (Section 3.2.2: the
+ * layer's new KV tensor, one token per sequence and head, goes into the
+ * free slot of the sequence's open block; Section 3.1: a block's metadata
+ * is created when the block fills).
+ *   new_kv : [B][Hkv][2][d] bf16, K then V of sequence b's new token
+ *   len    : [B] tokens of sequence b before this token (updated: +1)
+ *   nblk   : [B] full blocks of sequence b (set to j + 1 when block j fills)
+ *   open   : [B][Hkv] block records, the open block of each (b, g)
+ *   meta   : [B][Hkv][nblk_max][2][d], written for the block that fills
+ * The token goes to block j = len / blk at position p = len % blk.  When
+ * p == blk - 1 the open record is complete: its metadata (O0 on that one
+ * record) is stored as block j of the unit.  Returns 2 if a block that
+ * fills has j >= nblk_max; nothing is changed then.
+ * ---------------------------------------------------------------------- */
+int oracle_append(const uint16_t *new_kv, int32_t *len, int32_t *nblk, int B, int Hkv,
+                  int blk, int d, int nblk_max, void *open, uint16_t *meta)
+{
+    if (B < 0 || Hkv <= 0 || blk <= 0 || d <= 0 || nblk_max < 0)
+        return 1;
+    size_t record_bytes = (size_t)2 * blk * d * 2;
+    for (int b = 0; b < B; ++b)
+        if (len[b] < 0 || (len[b] % blk == blk - 1 && len[b] / blk >= nblk_max))
+            return 2;
+    for (int b = 0; b < B; ++b) {
+        int j = len[b] / blk, p = len[b] % blk;
+        for (int g = 0; g < Hkv; ++g) {
+            int u = b * Hkv + g;
+            uint16_t *rec = (uint16_t *)((char *)open + (int64_t)u * (int64_t)record_bytes);
+            put_token(rec, blk, d, p, new_kv + (int64_t)u * 2 * d);
+            if (p == blk - 1) {
+                int64_t zero = 0;
+                int32_t one = 1;
+                oracle_build_metadata(rec, &zero, &one, 1, 1, 1, blk, d, record_bytes,
+                                      meta + ((int64_t)u * nblk_max + j) * 2 * d);
+            }
+        }
+        len[b] += 1;
+        if (p == blk - 1)
+            nblk[b] = j + 1;
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------
+ * O7  Saving new tokens to the DRAM pool (Section 3.2.2, FlashD2H: the new
+ * KV tensor is contiguous; it is copied to host memory in one transfer and
+ * host threads then place each token into its KV block in DRAM).  What the
+ * pool holds afterwards is defined here, token by token:
+ *   new_kv      : [B][n_new][Hkv][2][d] bf16, the n_new new tokens of each
+ *                 sequence in order
+ *   len         : [B] tokens of sequence b before the first new token
+ *   pool        : DRAM pool; block j of unit u = b*Hkv + g is the record at
+ *                 pool + pool_off[u] + j * record_bytes
+ *   pool_blocks : [B] blocks the pool holds per unit of sequence b
+ * Token i of sequence b is token T = len[b] + i of the sequence: block
+ * j = T / blk, position p = T % blk.  Returns 2 (nothing written) if some
+ * j >= pool_blocks[b].
+ * ---------------------------------------------------------------------- */
+int oracle_save(const uint16_t *new_kv, int n_new, const int32_t *len, int B, int Hkv,
+                int blk, int d, void *pool, const int64_t *pool_off, const int32_t *pool_blocks)
+{
+    if (B < 0 || n_new < 0 || Hkv <= 0 || blk <= 0 || d <= 0)
+        return 1;
+    size_t record_bytes = (size_t)2 * blk * d * 2;
+    for (int b = 0; b < B; ++b)
+        if (n_new > 0 && (len[b] < 0 || (len[b] + n_new - 1) / blk >= pool_blocks[b]))
+            return 2;
+    for (int b = 0; b < B; ++b)
+        for (int i = 0; i < n_new; ++i) {
+            int T = len[b] + i;
+            int j = T / blk, p = T % blk;
+            for (int g = 0; g < Hkv; ++g) {
+                int u = b * Hkv + g;
+                uint16_t *rec = (uint16_t *)((char *)pool + pool_off[u] + (int64_t)j * (int64_t)record_bytes);
+                put_token(rec, blk, d, p, new_kv + (((int64_t)b * n_new + i) * Hkv + g) * 2 * d);
+            }
+        }
     return 0;
 }

@@ -457,6 +457,165 @@ def pin_attention_empty(O):
     assert np.all(out == 0)
 
 
+# ------------------------------------------------------ O6 append, O7 save
+def record_tokens(rec, blk, d):
+    """Inverse of make_records for one record: uint16 [2*blk*d] -> (K [blk][d], V [blk][d])."""
+    rec = np.asarray(rec, dtype=np.uint16)
+    K = rec[:blk * d].reshape(blk, d)
+    V = rec[blk * d:].reshape(d, blk).T
+    return K, V
+
+
+def _nonzero_bf16(shape, seed):
+    x = rand_bf16(shape, seed)
+    x[(x & 0x7FFF) == 0] = 0x3F80  # no signed zeros: numpy's min/max then agrees with totalOrder
+    return x
+
+
+def pin_append_record_layout(O):
+    """blk appends starting on a block boundary leave the open record equal
+    to the record assembled from the tokens (numpy layout), and the block's
+    metadata equal to numpy's channel-wise min/max of its keys."""
+    B, Hkv, blk, d, nmax = 2, 3, 4, 8, 3
+    tok = _nonzero_bf16((blk, B, Hkv, 2, d), 11)
+    len_ = np.array([0, 4], np.int32)
+    nblk = np.array([0, 1], np.int32)
+    open_rec = np.zeros((B, Hkv, 2 * blk * d), np.uint16)
+    meta = np.zeros((B, Hkv, nmax, 2, d), np.uint16)
+    for t in range(blk):
+        if t < blk - 1:
+            assert list(nblk) == [0, 1]
+        O.append(tok[t], len_, nblk, blk, nmax, open_rec, meta)
+    assert list(len_) == [blk, 2 * blk] and list(nblk) == [1, 2]
+    for b in range(B):
+        j = b  # block filled by these appends
+        for g in range(Hkv):
+            K = tok[:, b, g, 0]
+            V = tok[:, b, g, 1]
+            want = make_records(K[None], V[None])[0]
+            assert np.array_equal(open_rec[b, g], want), (b, g)
+            np.testing.assert_array_equal(meta[b, g, j], _meta_from_keys(bits_to_f64(K)))
+            others = [x for x in range(nmax) if x != j]
+            assert np.all(meta[b, g, others] == 0)
+
+
+def pin_append_ragged_positions(O):
+    """Sequences at different offsets: after each append, positions below the
+    fill level of the open record hold the current block's tokens; blocks
+    fill (nblk, metadata) exactly when their last token arrives."""
+    B, Hkv, blk, d, nmax = 3, 2, 4, 8, 6
+    start = np.array([1, 6, 11], np.int32)
+    steps = 9
+    tok = _nonzero_bf16((steps, B, Hkv, 2, d), 12)
+    len_ = start.copy()
+    nblk = (start // blk).astype(np.int32)
+    open_rec = np.zeros((B, Hkv, 2 * blk * d), np.uint16)
+    meta = np.zeros((B, Hkv, nmax, 2, d), np.uint16)
+    hist = {b: {} for b in range(B)}  # token index -> step
+    for t in range(steps):
+        O.append(tok[t], len_, nblk, blk, nmax, open_rec, meta)
+        for b in range(B):
+            T = start[b] + t
+            hist[b][T] = t
+            assert len_[b] == T + 1 and nblk[b] == (T + 1) // blk
+            j0 = T // blk * blk
+            for g in range(Hkv):
+                K, V = record_tokens(open_rec[b, g], blk, d)
+                for T2 in range(max(j0, start[b]), T + 1):
+                    assert np.array_equal(K[T2 - j0], tok[hist[b][T2], b, g, 0]), (t, b, g, T2)
+                    assert np.array_equal(V[T2 - j0], tok[hist[b][T2], b, g, 1]), (t, b, g, T2)
+                if (T + 1) % blk == 0:  # block T // blk just filled from tokens j0 .. T
+                    if j0 >= start[b]:
+                        Kb = np.stack([tok[hist[b][x], b, g, 0] for x in range(j0, T + 1)])
+                        np.testing.assert_array_equal(meta[b, g, T // blk], _meta_from_keys(bits_to_f64(Kb)))
+    # blocks that were already full before the first append are never written
+    for b in range(B):
+        for j in range(start[b] // blk):
+            assert np.all(meta[b, :, j] == 0)
+
+
+def pin_append_capacity_error(O):
+    """Filling a block at index >= nblk_max is an error and changes nothing."""
+    B, Hkv, blk, d, nmax = 1, 1, 4, 8, 2
+    len_ = np.array([2 * blk - 1], np.int32)
+    nblk = np.array([1], np.int32)
+    open_rec = np.zeros((1, 1, 2 * blk * d), np.uint16)
+    meta = np.zeros((1, 1, nmax, 2, d), np.uint16)
+    O.append(_nonzero_bf16((1, 1, 2, d), 13), len_, nblk, blk, nmax, open_rec, meta)  # fills block 1: fine
+    assert nblk[0] == 2 and len_[0] == 2 * blk
+    len_[0] = 3 * blk - 1
+    before = open_rec.copy()
+    try:
+        O.append(_nonzero_bf16((1, 1, 2, d), 14), len_, nblk, blk, nmax, open_rec, meta)
+    except OverflowError:
+        assert np.array_equal(open_rec, before) and len_[0] == 3 * blk - 1 and nblk[0] == 2
+        return
+    raise AssertionError("filling block nblk_max did not fail")
+
+
+def pin_save_spans_blocks(O):
+    """Saving several tokens per sequence that span block boundaries writes
+    each token at its (block, position) and leaves every other byte of the
+    pool as it was; units sit at arbitrary pool offsets."""
+    B, Hkv, blk, d, n_new = 2, 2, 4, 8, 7
+    rb = 2 * blk * d * 2
+    nb = 4
+    units = B * Hkv
+    off = (np.arange(units, dtype=np.int64)[::-1] * (nb + 1) * rb).copy()  # reversed, with a gap record
+    pool = np.frombuffer(np.random.default_rng(15).bytes((units * (nb + 1)) * rb), np.uint8).copy()
+    before = pool.copy()
+    len_ = np.array([3, 9], np.int32)
+    tok = _nonzero_bf16((B, n_new, Hkv, 2, d), 16)
+    O.save(tok, len_, blk, pool, off, np.full(B, nb, np.int32))
+    touched = np.zeros(pool.size, bool)
+    for b in range(B):
+        for g in range(Hkv):
+            u = b * Hkv + g
+            for j in range(nb):
+                lo = off[u] + j * rb
+                rec = pool[lo:lo + rb].view(np.uint16)
+                K, V = record_tokens(rec, blk, d)
+                K0, V0 = record_tokens(before[lo:lo + rb].view(np.uint16), blk, d)
+                for p in range(blk):
+                    i = j * blk + p - len_[b]
+                    if 0 <= i < n_new:
+                        assert np.array_equal(K[p], tok[b, i, g, 0]) and np.array_equal(V[p], tok[b, i, g, 1]), \
+                            (b, g, j, p)
+                    else:
+                        assert np.array_equal(K[p], K0[p]) and np.array_equal(V[p], V0[p]), (b, g, j, p)
+                touched[lo:lo + rb] = True
+    assert np.array_equal(pool[~touched], before[~touched])
+
+
+def pin_save_full_block_record(O):
+    """Saving exactly one block's tokens from a block boundary writes the
+    record that numpy assembles from those tokens."""
+    B, Hkv, blk, d = 1, 2, 8, 16
+    rb = 2 * blk * d * 2
+    pool = np.zeros(Hkv * 3 * rb, np.uint8)
+    off = np.arange(Hkv, dtype=np.int64) * 3 * rb
+    tok = _nonzero_bf16((B, blk, Hkv, 2, d), 17)
+    O.save(tok, np.array([blk], np.int32), blk, pool, off, np.array([3], np.int32))
+    for g in range(Hkv):
+        rec = pool[off[g] + rb:off[g] + 2 * rb].view(np.uint16)
+        assert np.array_equal(rec, make_records(tok[0, :, g, 0][None], tok[0, :, g, 1][None])[0]), g
+        assert np.all(pool[off[g]:off[g] + rb] == 0) and np.all(pool[off[g] + 2 * rb:off[g] + 3 * rb] == 0)
+
+
+def pin_save_capacity_error(O):
+    """A token past the unit's pool blocks is an error and writes nothing."""
+    blk, d = 4, 8
+    rb = 2 * blk * d * 2
+    pool = np.zeros(2 * rb, np.uint8)
+    try:
+        O.save(_nonzero_bf16((1, 3, 1, 2, d), 18), np.array([6], np.int32), blk, pool, np.zeros(1, np.int64),
+               np.array([2], np.int32))
+    except OverflowError:
+        assert np.all(pool == 0)
+        return
+    raise AssertionError("saving past the pool did not fail")
+
+
 GROUPS = {
     "meta": [pin_meta_bruteforce, pin_meta_ragged_untouched, pin_meta_signed_zero, pin_meta_record_offsets],
     "score": [pin_score_fixture, pin_score_upper_bound, pin_score_point_block, pin_score_corner_tight,
@@ -465,5 +624,7 @@ GROUPS = {
     "lru": [pin_lru_fixture, pin_lru_bruteforce, pin_lru_repeated_step, pin_lru_capacity_error],
     "gather": [pin_gather_bytes],
     "attention": [pin_attention_fixture, pin_attention_dense, pin_attention_subset, pin_attention_empty],
+    "append": [pin_append_record_layout, pin_append_ragged_positions, pin_append_capacity_error],
+    "save": [pin_save_spans_blocks, pin_save_full_block_record, pin_save_capacity_error],
 }
 ALL_PINS = [p for ps in GROUPS.values() for p in ps]

@@ -57,6 +57,20 @@ MUTANTS = [
      "for (int i = 0; i < k - 1; ++i) {\n                int32_t s = slots"),
     ("attn-drops-first-token", "attention", "for (int t = 0; t < blk; ++t) {\n                    kv_of[n] = rec;",
      "for (int t = 1; t < blk; ++t) {\n                    kv_of[n] = rec;"),
+    ("append-v-row-major", "append", "rec[blk * d + c * blk + p] = kv[d + c];", "rec[blk * d + p * d + c] = kv[d + c];"),
+    ("append-position-off-by-one", "append", "int j = len[b] / blk, p = len[b] % blk;",
+     "int j = len[b] / blk, p = (len[b] + 1) % blk;"),
+    ("append-meta-next-block", "append", "meta + ((int64_t)u * nblk_max + j) * 2 * d);",
+     "meta + ((int64_t)u * nblk_max + j + 1) * 2 * d);"),
+    ("append-nblk-not-updated", "append", "            nblk[b] = j + 1;\n", "            nblk[b] += 0;\n"),
+    ("append-k-and-v-swapped", "append", "put_token(rec, blk, d, p, new_kv + (int64_t)u * 2 * d);",
+     "put_token(rec, blk, d, p, new_kv + (int64_t)u * 2 * d + d);"),
+    ("save-v-row-major", "save", "rec[blk * d + c * blk + p] = kv[d + c];", "rec[blk * d + p * d + c] = kv[d + c];"),
+    ("save-ignores-len", "save", "int T = len[b] + i;", "int T = i;"),
+    ("save-token-major-input", "save", "new_kv + (((int64_t)b * n_new + i) * Hkv + g) * 2 * d",
+     "new_kv + (((int64_t)i * B + b) * Hkv + g) * 2 * d"),
+    ("save-ignores-offsets", "save", "(char *)pool + pool_off[u] + (int64_t)j",
+     "(char *)pool + (int64_t)u * pool_blocks[b] * (int64_t)record_bytes + (int64_t)j"),
 ]
 
 
