@@ -157,6 +157,13 @@ int64_t ss_cache_total_slots(const ss_cache *cache);
 ss_status ss_cache_region_offsets(const ss_cache *cache, int64_t *off);
 /* Host threads used by ss_cache_resolve (default: hardware concurrency, at most 16). */
 ss_status ss_cache_set_threads(ss_cache *cache, int n_threads);
+/* New block counts after sequences grew (a block fills when its last token
+ * is appended, Section 3.1): nblk host int32 [B], each >= the current
+ * count (SS_ERR_INVALID_ARG otherwise).  Capacities and cached blocks are
+ * unchanged; the new blocks start uncached.  Cheap unless a sequence
+ * outgrows the room reserved so far (then the host block table is laid out
+ * again, with slack). */
+ss_status ss_cache_set_blocks(ss_cache *cache, const int32_t *nblk);
 
 /* Resolve one step's selection.  Per unit, with sel[u][*] strictly
  * ascending then -1 padded:
@@ -220,6 +227,59 @@ size_t ss_sparse_attention_workspace(int B, int Hq, int Hkv, int d, int blk, int
 ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t *region_off, const int32_t *slots,
                               int32_t slot_limit, int B, int Hq, int Hkv, int d, int blk, int k, float scale,
                               float *out, void *workspace, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------ appending tokens
+ * The decode step's new KV (Section 3.2.2: each layer's new KV tensor, one
+ * token per sequence and KV head, goes into the free slot of the
+ * sequence's open block in HBM) and the metadata of a block that fills
+ * (Section 3.1).  Sequence b's token is token len[b] of the sequence: block
+ * j = len[b] / blk, row p = len[b] % blk of the open record.
+ *   new_kv: device bf16 [B][Hkv][2][d], K then V of each (sequence, head)
+ *   len_dev: device int32 [B] tokens before the append; advanced by 1
+ *   nblk_dev: device int32 [B] full blocks; set to j + 1 when block j fills
+ *   open_blocks: device [B][Hkv] block records (2*blk*d bf16 each: K tile
+ *       row-major, V tile channel-major); row / column p is written
+ *   meta: device bf16 [B][Hkv][nblk_max][2][d]; on a fill, block j's lo/hi
+ *       (channel-wise min/max of the record's K rows, IEEE totalOrder)
+ *   overflow: device int32 or NULL; set to 1 if a block fills at
+ *       j >= nblk_max (its metadata is then not written and nblk_dev not
+ *       advanced; the token is still written and len_dev advanced)
+ * Buffers 4-byte aligned.  d must be 128, blk 8, 16 or 32.  One kernel on
+ * `stream`, one workgroup per sequence. */
+ss_status ss_append_kv(const void *new_kv, int32_t *len_dev, int32_t *nblk_dev, int B, int Hkv, int blk, int d,
+                       int nblk_max, void *open_blocks, void *meta, int32_t *overflow, void *stream);
+
+/* ------------------------------------------------------ FlashD2H saving
+ * CPU-assisted saving of new tokens to the DRAM pool (Section 3.2.2): the
+ * contiguous new-KV tensor is copied to pinned host staging memory in one
+ * transfer on the caller's stream, then this library's host threads place
+ * each token in its block record in the pool (the same record layout).  The
+ * GPU's compute units take no part.
+ *   pool_host: host address of the pool; block j of unit u = b*Hkv + g is
+ *       the record at pool_host + pool_off[u] + j*record_bytes
+ *   pool_off: host int64 [B*Hkv]; pool_blocks: host int32 [B] records the
+ *       pool holds per unit of sequence b (both copied)
+ *   max_new_tokens: largest n_new of ss_kv_save
+ *   staging_slots: pinned staging buffers, used in turn (1..64); a save
+ *       whose buffer is still being scattered waits for it
+ *   threads: host threads that scatter (1..64); they start now
+ * The saver owns its staging memory, events and threads. */
+typedef struct ss_kv_saver ss_kv_saver;
+ss_status ss_kv_saver_create(int B, int Hkv, int blk, int d, void *pool_host, const int64_t *pool_off,
+                             const int32_t *pool_blocks, int max_new_tokens, int staging_slots, int threads,
+                             ss_kv_saver **out);
+/* Waits for the saves in flight, then frees everything. */
+void ss_kv_saver_destroy(ss_kv_saver *saver);
+/* Saves n_new tokens per sequence: new_kv device bf16
+ * [B][n_new][Hkv][2][d]; token i of sequence b is token len[b] + i of the
+ * sequence (len: host int32 [B], copied).  Enqueues the copy on `stream`
+ * and returns; the scatter runs when the copy has finished.  new_kv must
+ * stay unchanged until the copy has run (stream order).  SS_ERR_INVALID_ARG
+ * if a token lies past its unit's pool blocks.  Not thread-safe per saver. */
+ss_status ss_kv_save(ss_kv_saver *saver, const void *new_kv, int n_new, const int32_t *len, void *stream);
+/* Blocks until every save so far is in the pool; returns the first error
+ * met by the asynchronous part (SS_ERR_HIP). */
+ss_status ss_kv_save_wait(ss_kv_saver *saver);
 
 /* ------------------------------------------------------- one layer's step
  * The decode step of one layer over the HBM/DRAM hierarchy (Section 3.1's

@@ -67,6 +67,12 @@ _SIGNATURES = {
     "ss_sparse_attention": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
                                    _sz, _vp]),
     "ss_decode_layer": (_i32, [ctypes.POINTER(ss_layer_buffers), _i64, _vp, _vp, _vp, _vp, _vp]),
+    "ss_cache_set_blocks": (_i32, [_vp, _vp]),
+    "ss_append_kv": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "ss_kv_saver_create": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _i32, _i32, _i32, _vp]),
+    "ss_kv_saver_destroy": (None, [_vp]),
+    "ss_kv_save": (_i32, [_vp, _vp, _i32, _vp, _vp]),
+    "ss_kv_save_wait": (_i32, [_vp]),
 }
 
 
@@ -232,3 +238,40 @@ def ss_decode_layer(buffers, step, q, out, stream=None, events=None):
     _check(lib().ss_decode_layer(ctypes.byref(buffers), step, _ptr(q), _ptr(out), _stream(stream), ev,
                                  ctypes.byref(n)))
     return n.value
+
+
+def ss_cache_set_blocks(handle, nblk):
+    import numpy as np
+    nblk = np.ascontiguousarray(nblk, dtype=np.int32)
+    _check(lib().ss_cache_set_blocks(handle, nblk.ctypes.data))
+
+
+def ss_append_kv(new_kv, len_dev, nblk_dev, B, Hkv, blk, d, nblk_max, open_blocks, meta, overflow=None, stream=None):
+    _check(lib().ss_append_kv(_ptr(new_kv), _ptr(len_dev), _ptr(nblk_dev), B, Hkv, blk, d, nblk_max,
+                              _ptr(open_blocks), _ptr(meta), _ptr(overflow), _stream(stream)))
+
+
+def ss_kv_saver_create(B, Hkv, blk, d, pool_host, pool_off, pool_blocks, max_new_tokens=1, staging_slots=4,
+                       threads=2):
+    """pool_host: host address; pool_off int64 [B*Hkv], pool_blocks int32 [B] (numpy)."""
+    import numpy as np
+    pool_off = np.ascontiguousarray(pool_off, dtype=np.int64)
+    pool_blocks = np.ascontiguousarray(pool_blocks, dtype=np.int32)
+    h = ctypes.c_void_p()
+    _check(lib().ss_kv_saver_create(B, Hkv, blk, d, pool_host, pool_off.ctypes.data, pool_blocks.ctypes.data,
+                                    max_new_tokens, staging_slots, threads, ctypes.byref(h)))
+    return h.value
+
+
+def ss_kv_saver_destroy(saver):
+    lib().ss_kv_saver_destroy(saver)
+
+
+def ss_kv_save(saver, new_kv, n_new, len_host, stream=None):
+    import numpy as np
+    len_host = np.ascontiguousarray(len_host, dtype=np.int32)
+    _check(lib().ss_kv_save(saver, _ptr(new_kv), n_new, len_host.ctypes.data, _stream(stream)))
+
+
+def ss_kv_save_wait(saver):
+    _check(lib().ss_kv_save_wait(saver))

@@ -113,6 +113,7 @@ struct unit_state {
     int32_t head = -1, tail = -1;  // LRU list of cached slots
     int64_t slot_base = 0;         // first slot of this unit in the slot arrays
     int64_t block_base = 0;        // first entry of this unit in block_slot
+    int32_t block_cap = 0;         // entries reserved there (>= nblk)
 };
 
 int default_threads()
@@ -138,7 +139,7 @@ struct ss_cache {
     int64_t total_slots = 0;
     int64_t last_step = INT64_MIN;
     std::vector<unit_state> units;
-    std::vector<int32_t> block_slot;  // [sum nblk] slot holding the block, -1
+    std::vector<int32_t> block_slot;  // [sum block_cap] slot holding the block, -1
     std::vector<int32_t> slot_block;  // [total] block held, -1 empty
     std::vector<int64_t> slot_last;   // [total]
     std::vector<int32_t> prev, next;  // [total] LRU links, slot indices local to the unit
@@ -289,6 +290,7 @@ ss_status ss_cache_create(int B, int Hkv, const int32_t *nblk, const int32_t *ca
             unit_state &st = c->units[u];
             st.cap = cap;
             st.nblk = n;
+            st.block_cap = n;
             st.slot_base = slots;
             st.block_base = blocks;
             slots += cap;
@@ -320,6 +322,49 @@ ss_status ss_cache_region_offsets(const ss_cache *c, int64_t *off)
 {
     SS_CHECK_ARG(c && off, "ss_cache_region_offsets: null pointer");
     for (size_t u = 0; u < c->units.size(); ++u) off[u] = c->units[u].slot_base * (int64_t)c->record_bytes;
+    return SS_OK;
+}
+
+ss_status ss_cache_set_blocks(ss_cache *c, const int32_t *nblk)
+{
+    SS_CHECK_ARG(c && (c->B == 0 || nblk), "ss_cache_set_blocks: null pointer");
+    bool grow = false;
+    for (int b = 0; b < c->B; ++b) {
+        const unit_state &st = c->units[(size_t)b * c->Hkv];
+        SS_CHECK_ARG(nblk[b] >= st.nblk, "ss_cache_set_blocks: sequence %d shrinks from %d to %d blocks", b, st.nblk,
+                     nblk[b]);
+        grow |= nblk[b] > st.block_cap;
+    }
+    if (grow) {
+        // lay the block table out again with room to grow (amortised)
+        try {
+            std::vector<int32_t> bs;
+            std::vector<int64_t> base(c->units.size());
+            std::vector<int32_t> cap(c->units.size());
+            int64_t total = 0;
+            for (size_t u = 0; u < c->units.size(); ++u) {
+                const int32_t n = nblk[u / c->Hkv];
+                const unit_state &st = c->units[u];
+                cap[u] = n > st.block_cap ? n + std::max<int32_t>(16, n / 8) : st.block_cap;
+                base[u] = total;
+                total += cap[u];
+            }
+            bs.assign(total, -1);
+            for (size_t u = 0; u < c->units.size(); ++u) {
+                const unit_state &st = c->units[u];
+                std::copy(c->block_slot.begin() + st.block_base, c->block_slot.begin() + st.block_base + st.nblk,
+                          bs.begin() + base[u]);
+            }
+            c->block_slot.swap(bs);
+            for (size_t u = 0; u < c->units.size(); ++u) {
+                c->units[u].block_base = base[u];
+                c->units[u].block_cap = cap[u];
+            }
+        } catch (const std::bad_alloc &) {
+            return ss::fail(SS_ERR_OOM, "ss_cache_set_blocks: out of memory");
+        }
+    }
+    for (size_t u = 0; u < c->units.size(); ++u) c->units[u].nblk = nblk[u / c->Hkv];
     return SS_OK;
 }
 

@@ -174,3 +174,55 @@ def test_resolve_range_rejects_bad_range():
         with pytest.raises(ss.SparseServeError) as e:
             ss.ss_cache_resolve_range(c.h, 0, b0, b1, sel, 2, np.empty_like(sel), np.empty((4, 4), np.int32), 4)
         assert e.value.status == ss.SS_ERR_INVALID_ARG
+
+
+def test_growing_sequences_match_oracle(oracle_impl):
+    """Sequences gain blocks between steps (ss_cache_set_blocks, several
+    times past the reserved room): with selections drawn from the blocks
+    that exist at each step, slots and misses equal the oracle's LRU, which
+    knows the final block counts from the start (block counts only bound
+    which indices are valid)."""
+    rng = np.random.default_rng(21)
+    B, Hkv, k = 3, 2, 6
+    n0 = np.array([8, 20, 30], np.int32)
+    steps = 40
+    grow = rng.integers(0, 3, size=(steps, B)).astype(np.int32)
+    grow[5] = [40, 0, 0]  # one jump well past the slack
+    nb = [n0.copy()]
+    for s in range(steps):
+        nb.append(nb[-1] + grow[s])
+    final = nb[-1]
+    cap = np.repeat([8, 10, 12], Hkv).astype(np.int32)
+    lib = LibCache(B, Hkv, n0, cap)
+    ora = oracle_impl.lru(B, Hkv, final, cap)
+    for s in range(steps):
+        cur = nb[s]
+        if s:
+            ss.ss_cache_set_blocks(lib.h, cur)
+        sel = np.full((B, Hkv, k), -1, np.int32)
+        for b in range(B):
+            for g in range(Hkv):
+                # favour the newest blocks, as a growing context would
+                pick = np.unique(np.concatenate([rng.integers(max(0, cur[b] - 12), cur[b], size=k - 2),
+                                                 rng.integers(0, cur[b], size=2)]))[:k]
+                sel[b, g, :len(pick)] = pick
+        ls, lm = lib.step(s, sel)
+        os_, om = ora.step(s, sel)
+        np.testing.assert_array_equal(ls, os_, err_msg=f"slots differ at step {s}")
+        np.testing.assert_array_equal(lm, om, err_msg=f"misses differ at step {s}")
+    lb, ll = lib.export()
+    ob, ol = ora.export()
+    np.testing.assert_array_equal(lb, ob)
+    np.testing.assert_array_equal(ll, ol)
+
+
+def test_set_blocks_rejects_shrinking_and_guards_new_blocks():
+    lib = LibCache(2, 1, [4, 4], [4, 4])
+    with pytest.raises(ss.SparseServeError):
+        ss.ss_cache_set_blocks(lib.h, [3, 4])
+    sel = np.array([[[4, -1]], [[0, -1]]], np.int32)
+    with pytest.raises(ss.SparseServeError):  # block 4 does not exist yet
+        lib.step(0, sel)
+    ss.ss_cache_set_blocks(lib.h, [5, 4])
+    slots, miss = lib.step(0, sel)
+    assert slots[0, 0, 0] == 0 and len(miss) == 2
