@@ -103,8 +103,13 @@ class HierLayer:
     """One layer of the hierarchical workload: its DRAM pool slice, HBM
     metadata, HBM block cache and step buffers."""
 
-    def __init__(self, cfg, nblk_host, capacity, pool, pool_off_host, meta, parts=1):
+    def __init__(self, cfg, nblk_host, capacity, pool, pool_off_host, meta, parts=1, reserve=0):
         self.cfg = cfg
+        # blocks each unit may gain (appended tokens) beyond its initial count:
+        # the metadata, the scores and the pool have room for them
+        self.reserve = reserve
+        self.nblk_max = cfg.nblk_max + reserve
+        assert meta.shape[2] == self.nblk_max
         # parts: a group count (equal groups) or a list of group sizes
         if isinstance(parts, (list, tuple)):
             assert sum(parts) == cfg.B and all(p > 0 for p in parts)
@@ -131,7 +136,7 @@ class HierLayer:
         self.cap_dev = _dev(self.capacity, np.int32)
         self.nblk = _dev(self.nblk_host, np.int32)
         self.pool_off = _dev(self.pool_off_host, np.int64)
-        self.scores = torch.empty(B, Hkv, cfg.nblk_max, dtype=torch.float32, device="cuda")
+        self.scores = torch.empty(B, Hkv, self.nblk_max, dtype=torch.float32, device="cuda")
         self.sel = torch.empty(B, Hkv, k, dtype=torch.int32, device="cuda")
         self.slots = torch.empty(B, Hkv, k, dtype=torch.int32, device="cuda")
         self.miss_cap = self.units * k
@@ -148,7 +153,7 @@ class HierLayer:
         self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device="cuda")
         p = ss._ptr
         self.buffers = ss.ss_layer_buffers(
-            B=B, Hq=cfg.Hq, Hkv=Hkv, d=D, blk=cfg.blk, nblk_max=cfg.nblk_max, k=k, scale=1.0 / math.sqrt(D),
+            B=B, Hq=cfg.Hq, Hkv=Hkv, d=D, blk=cfg.blk, nblk_max=self.nblk_max, k=k, scale=1.0 / math.sqrt(D),
             meta=p(meta), nblk_dev=p(self.nblk), pool=pool.dev, pool_off_dev=p(self.pool_off), cache=self.handle,
             cache_base=p(self.cache), cache_off_dev=p(self.cache_off), capacity_dev=p(self.cap_dev),
             slot_limit=int(self.capacity.max()) if self.units else 0, scores=p(self.scores), sel_dev=p(self.sel),
@@ -156,12 +161,58 @@ class HierLayer:
             miss_host=p(self.miss_h), miss_cap=self.miss_cap, attn_ws=p(self.ws), attn_ws_bytes=self.ws_bytes,
             parts=self.parts, part_end=self.part_end.ctypes.data)
         self.last_n_miss = 0
+        self.saver = None
 
     def step(self, t, q, events=None):
         self.last_n_miss = ss.ss_decode_layer(self.buffers, t, q, self.out, None, events)
         return self.out
 
+    # ---------------------------------------------------------- save path
+    def enable_save(self, threads=2, staging_slots=4, save_stream=None):
+        """Appending and saving (FlashD2H) after each step: the open block of
+        every unit in HBM, the token counts on the device, a saver into the
+        pool's reserved blocks."""
+        cfg = self.cfg
+        assert self.reserve > 0, "build the layer with reserve > 0 blocks"
+        B, Hkv = cfg.B, cfg.Hkv
+        self.len_host = self.nblk_host.astype(np.int32) * cfg.blk  # sequences start block-aligned
+        self.len_dev = _dev(self.len_host, np.int32)
+        self.open = torch.empty(B, Hkv, cfg.record_bytes // 2, dtype=torch.int16, device="cuda")
+        self.overflow = torch.zeros(1, dtype=torch.int32, device="cuda")
+        self.pool_blocks = self.nblk_host + self.reserve
+        self.saver = ss.ss_kv_saver_create(B, Hkv, cfg.blk, D, self.pool.host, self.pool_off_host,
+                                           self.pool_blocks, 1, staging_slots, threads)
+        self.save_stream = save_stream
+        self.cache_blocks = self.nblk_host.copy()
+
+    def step_with_save(self, t, q, new_kv, events=None):
+        """One decode step of the layer with its save side.  The previous
+        saves must be in the pool before this step's gather can read a block
+        they completed, so they are waited for first; blocks filled so far
+        become selectable; the step's new tokens (ready on the current
+        stream) start their FlashD2H save, whose copy runs beside the decode
+        when a save stream is set; decode; then the tokens are appended to
+        the open blocks (metadata on a fill) for the next step."""
+        cfg = self.cfg
+        ss.ss_kv_save_wait(self.saver)
+        nb = (self.len_host // cfg.blk).astype(np.int32)
+        if np.any(nb != self.cache_blocks):
+            ss.ss_cache_set_blocks(self.handle, nb)
+            self.cache_blocks = nb
+        if self.save_stream is not None:
+            self.save_stream.wait_stream(torch.cuda.current_stream())
+            new_kv.record_stream(self.save_stream)  # its memory is not reused before the copy ran
+        ss.ss_kv_save(self.saver, new_kv, 1, self.len_host, self.save_stream)
+        self.step(t, q, events)
+        ss.ss_append_kv(new_kv, self.len_dev, self.nblk, cfg.B, cfg.Hkv, cfg.blk, D, self.nblk_max, self.open,
+                        self.meta, self.overflow)
+        self.len_host = self.len_host + 1
+        return self.out
+
     def close(self):
+        if self.saver:
+            ss.ss_kv_saver_destroy(self.saver)
+            self.saver = None
         if self.handle:
             ss.ss_cache_destroy(self.handle)
             self.handle = None
@@ -177,9 +228,10 @@ def cache_capacity(cfg, nblk):
     return np.repeat(per_seq, cfg.Hkv)
 
 
-def pool_layout(cfg, nblk):
-    """Byte offsets of each unit's block array in a compact DRAM pool."""
-    per_unit = np.repeat(np.asarray(nblk, np.int64), cfg.Hkv) * cfg.record_bytes
+def pool_layout(cfg, nblk, reserve=0):
+    """Byte offsets of each unit's block array in a compact DRAM pool
+    (nblk + reserve records per unit)."""
+    per_unit = (np.repeat(np.asarray(nblk, np.int64), cfg.Hkv) + reserve) * cfg.record_bytes
     off = np.concatenate([[0], np.cumsum(per_unit)[:-1]]).astype(np.int64)
     return off, int(per_unit.sum())
 
@@ -195,15 +247,17 @@ def tent_parts(B, n):
     return [int(x) for x in sizes]
 
 
-def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None, parts=1):
+def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None, parts=1, reserve=0):
     """Draws one layer's KV per sequence on the GPU, builds its metadata in
     HBM and copies the records into `pool` at pool_base_off.  Returns the
-    HierLayer (its pool offsets are relative to the pool base)."""
+    HierLayer (its pool offsets are relative to the pool base).  With
+    reserve > 0 every unit has that many more pool records and metadata rows
+    for blocks filled by appended tokens."""
     nblk = np.asarray(nblk, np.int32)
     sK, sV = gen.channel_scales(cfg.Hkv, D, seed, layer, "cuda")
-    off, total = pool_layout(cfg, nblk)
+    off, total = pool_layout(cfg, nblk, reserve)
     off = off + pool_base_off
-    meta = torch.empty(cfg.B, cfg.Hkv, cfg.nblk_max, 2, D, dtype=torch.int16, device="cuda")
+    meta = torch.empty(cfg.B, cfg.Hkv, cfg.nblk_max + reserve, 2, D, dtype=torch.int16, device="cuda")
     for b in range(cfg.B):
         n = int(nblk[b])
         if n == 0:
@@ -212,14 +266,15 @@ def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None,
         rec = rec.contiguous()
         # metadata of this sequence, from the HBM copy of its records
         unit_off = _dev(np.arange(cfg.Hkv, dtype=np.int64) * n * cfg.record_bytes, np.int64)
-        ss.ss_build_metadata(rec, unit_off, _dev([n], np.int32), 1, cfg.Hkv, cfg.nblk_max, cfg.blk, D, meta[b])
-        start = int(off[b * cfg.Hkv])
-        nbytes = cfg.Hkv * n * cfg.record_bytes
-        pool.t[start:start + nbytes].copy_(rec.view(torch.uint8).reshape(-1))
+        ss.ss_build_metadata(rec, unit_off, _dev([n], np.int32), 1, cfg.Hkv, cfg.nblk_max + reserve, cfg.blk, D,
+                             meta[b])
+        for g in range(cfg.Hkv):
+            start = int(off[b * cfg.Hkv + g])
+            pool.t[start:start + n * cfg.record_bytes].copy_(rec[g].view(torch.uint8).reshape(-1))
         if progress and b % 16 == 15:
             progress(f"layer {layer}: {b + 1}/{cfg.B} sequences in the DRAM pool")
     torch.cuda.synchronize()
-    L = HierLayer(cfg, nblk, cache_capacity(cfg, nblk), pool, off, meta, parts)
+    L = HierLayer(cfg, nblk, cache_capacity(cfg, nblk), pool, off, meta, parts, reserve)
     return L
 
 

@@ -95,6 +95,16 @@ def kv_records_seq(b, Hkv, nblk, blk, d, sK, sV, seed, layer=0, device="cpu",
     return torch.cat([Kb, Vb], dim=-1), planted
 
 
+def new_tokens(B, Hkv, d, sK, sV, seed, layer, step, device="cpu"):
+    """The decode step's new token per (sequence, KV head): bf16
+    [B][Hkv][2][d], K then V, drawn like the context (N(0,1) times the
+    layer's channel scales, fp32 rounded to bf16)."""
+    g = generator(device, seed, "new", layer, step)
+    K = torch.randn(B, Hkv, d, generator=g, device=device) * sK[None]
+    V = torch.randn(B, Hkv, d, generator=g, device=device) * sV[None]
+    return torch.stack([K, V], dim=2).to(torch.bfloat16).contiguous()
+
+
 def lengths(cfg, seed):
     """Context length in tokens per sequence: fixed, or for a ragged
     workload T_b = blk * round(U[lo, hi] / blk), clamped to [lo, hi]."""

@@ -38,31 +38,74 @@ class Track:
 
     def __init__(self, oracle_impl, cfg, L, pool, sample_b, name=""):
         self.o, self.cfg, self.L, self.pool, self.name = oracle_impl, cfg, L, pool, name
-        Hkv = cfg.Hkv
+        Hkv, rb = cfg.Hkv, cfg.record_bytes
         self.sb = list(sample_b)
         self.units = [b * Hkv + g for b in self.sb for g in range(Hkv)]
-        self.nb_s = L.nblk_host[self.sb]
+        self.nb_s = L.nblk_host[self.sb].astype(np.int32)
         cap_s = L.capacity[self.units]
-        self.meta = oracle_impl.build_metadata(pool.host, L.pool_off_host[self.units], self.nb_s, len(self.sb), Hkv,
-                                               cfg.nblk_max, cfg.blk, 128)
-        self.lru = oracle_impl.lru(len(self.sb), Hkv, self.nb_s, cap_s)
-        self.img_off = np.concatenate([[0], np.cumsum(cap_s.astype(np.int64))[:-1]]) * cfg.record_bytes
-        self.image = np.zeros(int(cap_s.sum()) * cfg.record_bytes + cfg.record_bytes, np.uint8)
-        self.pool_off = L.pool_off_host[self.units]
+        self.reserve = L.reserve
+        if self.reserve:
+            # with appends the oracle keeps a private copy of the sampled units'
+            # records (the drawn inputs) plus room for the blocks it saves itself
+            blocks = np.repeat(self.nb_s.astype(np.int64) + self.reserve, Hkv)
+            self.src_off = np.concatenate([[0], np.cumsum(blocks)[:-1]]) * rb
+            self.src = np.zeros(int(blocks.sum()) * rb, np.uint8)
+            for i, u in enumerate(self.units):
+                n = int(self.nb_s[i // Hkv]) * rb
+                self.src[self.src_off[i]:self.src_off[i] + n] = pool.u8[L.pool_off_host[u]:L.pool_off_host[u] + n]
+            self.src_blocks = self.nb_s + self.reserve
+            self.open = np.zeros((len(self.sb), Hkv, rb // 2), np.uint16)
+            self.len = self.nb_s * cfg.blk
+            self.nb0 = self.nb_s.copy()
+        else:
+            self.src, self.src_off = pool.host, L.pool_off_host[self.units]
+        self.meta = oracle_impl.build_metadata(self.src, self.src_off, self.nb_s, len(self.sb), Hkv, L.nblk_max,
+                                               cfg.blk, 128)
+        # block counts only bound which indices are valid: give the LRU the final ones
+        self.lru = oracle_impl.lru(len(self.sb), Hkv, self.nb_s + self.reserve, cap_s)
+        self.img_off = np.concatenate([[0], np.cumsum(cap_s.astype(np.int64))[:-1]]) * rb
+        self.image = np.zeros(int(cap_s.sum()) * rb + rb, np.uint8)
         self.diverged = set()
+
+    def append_and_save(self, new_kv):
+        """The oracle's side of a step's saving: the sampled sequences' new
+        tokens go to the private pool copy and to the open blocks."""
+        kv = gu.u16(new_kv)[self.sb]
+        self.o.save(kv[:, None], self.len, self.cfg.blk, self.src, self.src_off, self.src_blocks)
+        self.o.append(kv, self.len, self.nb_s, self.cfg.blk, self.L.nblk_max, self.open, self.meta)
+
+    def check_saved(self):
+        """After the run: block counts, metadata rows and DRAM records of the
+        blocks filled by appends, and the open blocks' filled rows."""
+        cfg, L, Hkv, rb = self.cfg, self.L, self.cfg.Hkv, self.cfg.record_bytes
+        import paper_2509_24626_amd.binding as ssb
+        ssb.ss_kv_save_wait(L.saver)
+        np.testing.assert_array_equal(L.nblk.cpu().numpy()[self.sb], self.nb_s)
+        np.testing.assert_array_equal(L.len_dev.cpu().numpy()[self.sb], self.len)
+        meta_g = L.meta.cpu().numpy().view(np.uint16)
+        open_g = L.open.cpu().numpy().view(np.uint16)
+        for i, b in enumerate(self.sb):
+            n0, n1 = int(self.nb0[i]), int(self.nb_s[i])
+            np.testing.assert_array_equal(meta_g[b, :, n0:n1], self.meta[i, :, n0:n1])
+            p = int(self.len[i]) % cfg.blk
+            for g in range(Hkv):
+                u, iu = b * Hkv + g, i * Hkv + g
+                got = self.pool.u8[L.pool_off_host[u] + n0 * rb:L.pool_off_host[u] + n1 * rb]
+                np.testing.assert_array_equal(got, self.src[self.src_off[iu] + n0 * rb:self.src_off[iu] + n1 * rb])
+                np.testing.assert_array_equal(open_g[b, g, :p * 128], self.open[i, g, :p * 128])
 
     def check(self, t, q):
         """Compares the GPU layer's step t (already run and synchronised)."""
         o, cfg, L, sb = self.o, self.cfg, self.L, self.sb
         Hkv, k, G, rb = cfg.Hkv, cfg.k, cfg.G, cfg.record_bytes
         qh = gu.u16(q)[sb]
-        S = o.score(qh, self.meta, self.nb_s, cfg.Hq, Hkv, cfg.nblk_max, 128)
+        S = o.score(qh, self.meta, self.nb_s, cfg.Hq, Hkv, L.nblk_max, 128)
         osel = o.select(S, self.nb_s, k)
         gsel = L.sel.cpu().numpy()[sb]
         for (i, g) in gu.check_selection(gsel, osel, S, self.nb_s, k):
             self.diverged.add((i, g))
         oslots, omiss = self.lru.step(t, osel)
-        o.gather(omiss, self.pool.host, self.pool_off, self.image, self.img_off, rb, Hkv)
+        o.gather(omiss, self.src, self.src_off, self.image, self.img_off, rb, Hkv)
         oout = o.attention(qh, self.image, self.img_off, oslots, Hkv, cfg.blk)
         gslots = L.slots_h.numpy()[sb]
         gmiss = L.miss_h.numpy()[:L.last_n_miss]
@@ -117,6 +160,46 @@ def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_dive
         pool.close()
 
 
+def lockstep_with_save(oracle_impl, cfg, seed, sample_b, steps, parts=1, save_stream=False):
+    """Decode steps that also append and save each step's new tokens
+    (ss_append_kv, FlashD2H), so blocks fill during the run and become
+    selectable; the oracle follows the sampled sequences on its own copy of
+    their records."""
+    from paper_2509_24626_amd import harness as H
+    lens = synth.gen.lengths(cfg, seed)
+    nblk = (lens // cfg.blk).astype(np.int32)
+    reserve = steps // cfg.blk + 2
+    off, total = H.pool_layout(cfg, nblk, reserve)
+    print(f"[gpu] {cfg.name} with save: pool {total / 2**30:.2f} GiB, {steps} steps, reserve {reserve}, "
+          f"sampled {sample_b}, {parts} group(s), save stream {save_stream}", flush=True)
+    pool = H.HostPool(total)
+    try:
+        L = H.build_hier_layer(cfg, seed, 0, pool, 0, nblk, parts=parts, reserve=reserve)
+        L.enable_save(threads=2, save_stream=torch.cuda.Stream() if save_stream else None)
+        sK, sV = synth.gen.channel_scales(cfg.Hkv, 128, seed, 0, "cuda")
+        qs = H.query_stream(cfg, seed, 0, steps)
+        tr = Track(oracle_impl, cfg, L, pool, sample_b, cfg.name + " +save")
+        new_selected = 0
+        for t in range(steps + 1):
+            kv = synth.gen.new_tokens(cfg.B, cfg.Hkv, 128, sK, sV, seed, 0, t, "cuda")
+            L.step_with_save(t, qs[t][1], kv)
+            torch.cuda.synchronize()
+            tr.check(t, qs[t][1])
+            sel = L.sel.cpu().numpy()
+            new_selected += int(sum((sel[b] >= nblk[b]).sum() for b in range(cfg.B)))
+            tr.append_and_save(kv)
+        tr.check_saved()
+        filled = L.nblk.cpu().numpy() - nblk
+        print(f"[gpu] blocks filled per sequence {sorted(set(filled.tolist()))}; selections of new blocks "
+              f"{new_selected}; diverged {len(tr.diverged)}/{len(tr.units)}", flush=True)
+        assert filled.min() >= 1 and int(L.overflow.item()) == 0
+        assert len(tr.diverged) <= 0.25 * len(tr.units)
+        L.close()
+        return new_selected
+    finally:
+        pool.close()
+
+
 SMALL = Config("hier-small-b3-ctx8k-blk16-k32-cache25", B=3, Hq=8, Hkv=2, d=128, blk=16, k=32, ctx=8192,
                placement="host", cache_frac=0.25, steps=6, drift=0.3)
 
@@ -143,6 +226,32 @@ def test_hier_gqa7_blk8_small(ss, oracle_impl):
 def test_hier_ragged_small(ss, oracle_impl):
     cfg = dataclasses.replace(synth.get(3), name="ragged-small", B=4, ctx_range=(2048, 6144), k=32, layers=1)
     lockstep(oracle_impl, cfg, seed=6, sample_b=range(cfg.B), steps=4)
+
+
+SAVE_SMALL = Config("hier-save-b3-ctx1k-blk16-k16-cache25", B=3, Hq=8, Hkv=2, d=128, blk=16, k=16, ctx=1024,
+                    placement="host", cache_frac=0.25, steps=40, drift=0.3)
+
+
+@pytest.mark.parametrize("save_stream", [False, True])
+def test_hier_small_with_append_and_save(ss, oracle_impl, save_stream):
+    """40 steps on 64-block sequences: every sequence fills 2 blocks, which
+    are then selected and gathered back from the DRAM records FlashD2H
+    wrote."""
+    n = lockstep_with_save(oracle_impl, SAVE_SMALL, seed=12, sample_b=range(SAVE_SMALL.B), steps=40, parts=2,
+                           save_stream=save_stream)
+    assert n > 0
+
+
+def test_hier_ragged_with_append_and_save(ss, oracle_impl):
+    cfg = dataclasses.replace(synth.get(3), name="ragged-save-small", B=4, ctx_range=(1024, 4096), k=16, layers=1)
+    lockstep_with_save(oracle_impl, cfg, seed=13, sample_b=range(cfg.B), steps=36)
+
+
+def test_hier_128k_full_size_with_save_sampled(ss, oracle_impl):
+    """The 128k workload at full size with appends and saves: 20 steps, so
+    every sequence fills one block at step 16."""
+    cfg = synth.get(2)
+    lockstep_with_save(oracle_impl, cfg, seed=0, sample_b=[0, 63], steps=20, parts=8, save_stream=True)
 
 
 def test_hier_128k_full_size_sampled(ss, oracle_impl):
