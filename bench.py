@@ -59,6 +59,13 @@ def parse():
                     help="rocprofv3 --pmc output folders of this script (FETCH_SIZE, WRITE_SIZE) and of "
                          "--calibrate-copy; prints the traffic summary and exits (no GPU)")
     ap.add_argument("--bench-json", help="with --summarize-pmc: the JSON line the profiled run printed")
+    ap.add_argument("--with-save", action="store_true",
+                    help="every step also appends its new tokens (metadata on a fill) and saves them to DRAM "
+                         "(FlashD2H); single-layer workloads")
+    ap.add_argument("--save-stream", choices=["own", "main"], default="own",
+                    help="with --with-save: the FlashD2H copies on a stream of their own or on the main stream")
+    ap.add_argument("--no-save-bandwidth", action="store_true",
+                    help="skip the saving-bandwidth comparison (FlashD2H, per-block copies, GPU-direct)")
     ap.add_argument("--pool-budget-gib", type=float, default=56.0,
                     help="pinned DRAM for KV records; layers beyond it reuse earlier layers' records")
     return ap.parse_args()
@@ -110,9 +117,32 @@ def main():
         parts = [int(x) for x in args.parts.split(",")]
     else:
         parts = int(args.parts)
-    pool, layers, _ = H.build_hier_model(cfg, args.seed, nblk, args.pool_flags, int(args.pool_budget_gib * 2**30),
-                                         progress=log, parts=parts)
+    new_kv = None
+    if args.with_save:
+        if cfg.layers != 1:
+            print("--with-save runs single-layer workloads", file=sys.stderr)
+            sys.exit(2)
+        reserve = (warmup + steps) // cfg.blk + 2
+        off, total = H.pool_layout(cfg, nblk, reserve)
+        pool = H.HostPool(total, args.pool_flags)
+        L = H.build_hier_layer(cfg, args.seed, 0, pool, 0, nblk, progress=log, parts=parts, reserve=reserve)
+        L.enable_save(threads=2, save_stream=torch.cuda.Stream() if args.save_stream == "own" else None)
+        layers = [L]
+        sK, sV = synth.gen.channel_scales(cfg.Hkv, D, args.seed, 0, "cuda")
+        # the steps' new tokens, resident in HBM before timing (the layer's
+        # projection would have produced them)
+        new_kv = [synth.gen.new_tokens(cfg.B, cfg.Hkv, D, sK, sV, args.seed, 0, s, "cuda")
+                  for s in range(warmup + steps)]
+    else:
+        pool, layers, _ = H.build_hier_model(cfg, args.seed, nblk, args.pool_flags,
+                                             int(args.pool_budget_gib * 2**30), progress=log, parts=parts)
     qstreams = [H.query_stream(cfg, args.seed, l, warmup + steps - 1) for l in range(cfg.layers)]
+
+    def run_step(L, l, s, events=None):
+        if new_kv is None:
+            L.step(s, qstreams[l][s][1], events)
+        else:
+            L.step_with_save(s, qstreams[l][s][1], new_kv[s], events)
     # metadata build (setup path), timed on its own for one layer
     L0 = layers[0]
     kv_one = torch.empty(cfg.Hkv * int(nblk[0]) * cfg.record_bytes, dtype=torch.uint8, device="cuda")
@@ -133,7 +163,7 @@ def main():
     # ----------------------------------------------------------- warm-up
     for s in range(warmup):
         for l, L in enumerate(layers):
-            L.step(s, qstreams[l][s][1])
+            run_step(L, l, s)
     torch.cuda.synchronize()
     log(f"warm-up done ({warmup} step(s)); timing {steps} step(s)")
 
@@ -156,8 +186,11 @@ def main():
     for i in range(steps):
         s = warmup + i
         for l, L in enumerate(layers):
-            L.step(s, qstreams[l][s][1], events=[e.cuda_event if used[j] else None for j, e in enumerate(ev[i][l])])
+            run_step(L, l, s, events=[e.cuda_event if used[j] else None for j, e in enumerate(ev[i][l])])
             n_miss[i, l] = L.last_n_miss
+    if new_kv is not None:
+        for L in layers:  # the last step's save is part of the work
+            ss.ss_kv_save_wait(L.saver)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
@@ -213,6 +246,9 @@ def main():
     for name in iso:
         iso[name]["traffic"] = traffic(name, key)
 
+    # ------------------------------------------- saving bandwidth
+    save_bw = None if args.no_save_bandwidth else save_bandwidth(ss, torch, H)
+
     # ------------------------------------------------------ CPU baseline
     cpu = None
     if not args.no_cpu_baseline:
@@ -247,6 +283,15 @@ def main():
                            "note": "setup path (when blocks fill), one sequence, not in the step"},
         "cpu_baseline": cpu,
     }
+    if new_kv is not None:
+        L = layers[0]
+        result["config"]["with_save"] = True
+        result["save_side"] = {"blocks_filled_per_sequence": int((L.nblk.cpu().numpy() - nblk).max()),
+                               "overflow": int(L.overflow.item()),
+                               "note": "each timed step also appends its new tokens (metadata on a fill) and saves "
+                                       "them with FlashD2H; the last save is waited for inside the timed region"}
+    if save_bw is not None:
+        result["save_bandwidth"] = save_bw
     print(json.dumps(result), flush=True)
     for L in layers:
         L.close()
@@ -381,6 +426,81 @@ def summarize_pmc(args):
     print("TRAFFIC = " + json.dumps(table, indent=1))
 
 
+def save_bandwidth(ss, torch, H, B=4, n=8192, Hkv=8, reps=3):
+    """Saving a prefill-sized batch of new KV (B sequences x n tokens x Hkv
+    heads, 128 MiB) to a pinned DRAM pool as block records, for blocks of 8,
+    16 and 32 tokens, three ways (the comparison of Section 3.2.2):
+      flashd2h   one device-to-host copy of the contiguous tensor, then the
+                 library's host threads place the tokens (ss_kv_save)
+      per_block  one hipMemcpyAsync per block record from HBM (issued from
+                 Python; ~1 us of its overhead per call)
+      gpu_direct a kernel stores the records into mapped host memory (the
+                 gather kernel with source and destination swapped)
+    GB/s = new-KV bytes / wall time from issue to completion (median of 3)."""
+    import ctypes
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p]
+    hip.hipMemcpyAsync.restype = ctypes.c_int
+    nbytes = B * n * Hkv * 2 * D * 2
+    kv = torch.randint(-16000, 16000, (B, n, Hkv, 2, D), dtype=torch.int16, device="cuda")
+    rec_dev = torch.randint(-16000, 16000, (nbytes // 2,), dtype=torch.int16, device="cuda")
+    pool = H.HostPool(nbytes)
+    res = {"bytes": nbytes, "threads": 8}
+    try:
+        for blk in (8, 16, 32):
+            rb = 2 * blk * D * 2
+            nb = n // blk
+            units = B * Hkv
+            off = np.arange(units, dtype=np.int64) * nb * rb
+            out = {}
+            saver = ss.ss_kv_saver_create(B, Hkv, blk, D, pool.host, off, np.full(B, nb, np.int32), n, 1, 8)
+            try:
+                ts = []
+                for _ in range(reps):
+                    torch.cuda.synchronize()
+                    t0 = time.perf_counter()
+                    ss.ss_kv_save(saver, kv, n, np.zeros(B, np.int32))
+                    ss.ss_kv_save_wait(saver)
+                    ts.append(time.perf_counter() - t0)
+                out["flashd2h"] = round(nbytes / float(np.median(ts)) / 1e9, 2)
+            finally:
+                ss.ss_kv_saver_destroy(saver)
+            stream = torch.cuda.current_stream().cuda_stream
+            src0 = rec_dev.data_ptr()
+            ts = []
+            for _ in range(reps):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                for u in range(units):
+                    for j in range(nb):
+                        o = int(off[u]) + j * rb
+                        if hip.hipMemcpyAsync(pool.host + o, src0 + o, rb, 2, stream) != 0:
+                            raise RuntimeError("hipMemcpyAsync failed")
+                torch.cuda.synchronize()
+                ts.append(time.perf_counter() - t0)
+            out["per_block"] = round(nbytes / float(np.median(ts)) / 1e9, 2)
+            rows = torch.from_numpy(np.stack(np.meshgrid(np.arange(B), np.arange(Hkv), np.arange(nb), indexing="ij"),
+                                             -1).reshape(-1, 3)).to(torch.int32)
+            miss = torch.cat([rows, rows[:, 2:3]], 1).contiguous().cuda()  # (b, g, block, slot = block)
+            off_dev = torch.from_numpy(off).cuda()
+            nblk_dev = torch.full((B,), nb, dtype=torch.int32, device="cuda")
+            cap_dev = torch.full((units,), nb, dtype=torch.int32, device="cuda")
+            ts = []
+            for _ in range(reps):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                ss.ss_gather_blocks(miss, miss.shape[0], rec_dev, off_dev, pool.dev, off_dev, nblk_dev, cap_dev, B,
+                                    Hkv, rb)
+                torch.cuda.synchronize()
+                ts.append(time.perf_counter() - t0)
+            out["gpu_direct"] = round(nbytes / float(np.median(ts)) / 1e9, 2)
+            res[f"blk{blk}"] = out
+            log(f"saving {nbytes >> 20} MiB, blk {blk}: {out} GB/s")
+    finally:
+        pool.close()
+    return res
+
+
 def isolated_rates(cfg, L, q, ss, torch, reps=10):
     """Median duration of score, top-k and attention over the full batch,
     each launched alone after a cache flush, as a fraction of the HBM peak.
@@ -395,9 +515,9 @@ def isolated_rates(cfg, L, q, ss, torch, reps=10):
     ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
     out = torch.empty(B, Hq, D, dtype=torch.float32, device="cuda")
     runs = {
-        "score": (lambda: ss.ss_score_blocks(q, L.meta, L.nblk, B, Hq, Hkv, cfg.nblk_max, D, L.scores),
+        "score": (lambda: ss.ss_score_blocks(q, L.meta, L.nblk, B, Hq, Hkv, L.nblk_max, D, L.scores),
                   blocks * (2 * D * 2 + 4) + B * Hq * D * 2),
-        "topk": (lambda: ss.ss_select_topk(L.scores, L.nblk, B, Hkv, cfg.nblk_max, k, L.sel),
+        "topk": (lambda: ss.ss_select_topk(L.scores, L.nblk, B, Hkv, L.nblk_max, k, L.sel),
                  blocks * 4 + B * Hkv * k * 4),
         "attention": (lambda: ss.ss_sparse_attention(q, L.cache, L.cache_off, L.slots, int(L.capacity.max()), B, Hq,
                                                      Hkv, D, cfg.blk, k, 1.0 / math.sqrt(D), out, ws, ws_bytes),

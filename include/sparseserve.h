@@ -160,9 +160,10 @@ ss_status ss_cache_set_threads(ss_cache *cache, int n_threads);
 /* New block counts after sequences grew (a block fills when its last token
  * is appended, Section 3.1): nblk host int32 [B], each >= the current
  * count (SS_ERR_INVALID_ARG otherwise).  Capacities and cached blocks are
- * unchanged; the new blocks start uncached.  Cheap unless a sequence
- * outgrows the room reserved so far (then the host block table is laid out
- * again, with slack). */
+ * unchanged; the new blocks start uncached.  Each unit's host block table
+ * keeps room for max(16, nblk/8) more blocks; within it the call costs
+ * O(B*Hkv), beyond it the table is laid out again (O(total blocks), once
+ * per such growth). */
 ss_status ss_cache_set_blocks(ss_cache *cache, const int32_t *nblk);
 
 /* Resolve one step's selection.  Per unit, with sel[u][*] strictly
@@ -251,10 +252,11 @@ ss_status ss_append_kv(const void *new_kv, int32_t *len_dev, int32_t *nblk_dev, 
 
 /* ------------------------------------------------------ FlashD2H saving
  * CPU-assisted saving of new tokens to the DRAM pool (Section 3.2.2): the
- * contiguous new-KV tensor is copied to pinned host staging memory in one
- * transfer on the caller's stream, then this library's host threads place
- * each token in its block record in the pool (the same record layout).  The
- * GPU's compute units take no part.
+ * contiguous new-KV tensor is copied to pinned host staging memory on the
+ * caller's stream (in chunks of consecutive token rows when it is large),
+ * and this library's host threads place each token in its block record in
+ * the pool (the same record layout), each chunk as soon as its copy has
+ * landed.  The GPU's compute units take no part.
  *   pool_host: host address of the pool; block j of unit u = b*Hkv + g is
  *       the record at pool_host + pool_off[u] + j*record_bytes
  *   pool_off: host int64 [B*Hkv]; pool_blocks: host int32 [B] records the

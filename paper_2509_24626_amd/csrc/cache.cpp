@@ -116,6 +116,9 @@ struct unit_state {
     int32_t block_cap = 0;         // entries reserved there (>= nblk)
 };
 
+// host block-table entries a unit reserves beyond its blocks (sequences grow)
+int32_t block_slack(int32_t n) { return std::max<int32_t>(16, n / 8); }
+
 int default_threads()
 {
     unsigned n = std::thread::hardware_concurrency();
@@ -290,11 +293,11 @@ ss_status ss_cache_create(int B, int Hkv, const int32_t *nblk, const int32_t *ca
             unit_state &st = c->units[u];
             st.cap = cap;
             st.nblk = n;
-            st.block_cap = n;
+            st.block_cap = n + block_slack(n);  // room to grow without laying the table out again
             st.slot_base = slots;
             st.block_base = blocks;
             slots += cap;
-            blocks += n;
+            blocks += st.block_cap;
         }
         c->total_slots = slots;
         c->block_slot.assign(blocks, -1);
@@ -345,7 +348,7 @@ ss_status ss_cache_set_blocks(ss_cache *c, const int32_t *nblk)
             for (size_t u = 0; u < c->units.size(); ++u) {
                 const int32_t n = nblk[u / c->Hkv];
                 const unit_state &st = c->units[u];
-                cap[u] = n > st.block_cap ? n + std::max<int32_t>(16, n / 8) : st.block_cap;
+                cap[u] = n > st.block_cap ? n + block_slack(n) : st.block_cap;
                 base[u] = total;
                 total += cap[u];
             }

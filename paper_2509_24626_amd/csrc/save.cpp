@@ -1,16 +1,19 @@
 // FlashD2H, CPU-assisted saving of new KV to the DRAM pool (Section 3.2.2).
 //
 // The new tokens of a layer form one contiguous tensor on the GPU.  Saving
-// them is split in two, as the paper does: one device-to-host copy of the
-// whole tensor into a pinned staging buffer on the caller's (save) stream,
-// then host threads place every token into its block record in the pool.
-// The GPU spends no compute on it: the copy runs on a copy engine, and the
-// scatter on this library's own threads, so it overlaps the next layers'
-// work.  Staging buffers form a ring; a save whose buffer is still being
-// scattered waits for it.
+// them is split in two, as the paper does: device-to-host copies of the
+// contiguous tensor into a pinned staging buffer on the caller's (save)
+// stream, then host threads place every token into its block record in the
+// pool.  The GPU spends no compute on it: the copies run on a copy engine,
+// and the scatter on this library's own threads, so it overlaps the next
+// layers' work.  A large save is copied in chunks of consecutive token rows
+// (at least 1 MiB, about four per thread), each with its own event, so the
+// scatter of one chunk overlaps the copy of the next.  Staging buffers form
+// a ring; a save whose buffer is still being scattered waits for it.
 //
 // Record layout: K tile [blk][d] row-major, then V tile channel-major
 // [d][blk] (bf16), so a token is one 256-byte K row and d strided V values.
+#include <algorithm>
 #include <atomic>
 #include <condition_variable>
 #include <cstring>
@@ -23,31 +26,40 @@
 
 namespace {
 
+constexpr int kMaxChunks = 64;            // copies (and events) per save
+constexpr size_t kMinChunkBytes = 1 << 20;
+
 struct job {
     int slot;
     int n_new;
     std::vector<int32_t> len;
-    std::atomic<int> parts_left{0};
+    std::atomic<int> chunks_left{0};
+};
+
+struct chunk {
+    job *jb;
+    int ev;          // event index within the slot
+    int64_t r0, r1;  // token rows [r0, r1) of the [B][n_new] order
 };
 
 }  // namespace
 
 struct ss_kv_saver {
     int B = 0, Hkv = 0, blk = 0, d = 0, max_new = 0;
-    size_t record_bytes = 0, slot_bytes = 0;
+    size_t record_bytes = 0, row_bytes = 0, slot_bytes = 0;
     uint8_t *pool = nullptr;
     std::vector<int64_t> pool_off;
     std::vector<int32_t> pool_blocks;
     std::vector<void *> staging;
-    std::vector<hipEvent_t> copied;
+    std::vector<std::vector<hipEvent_t>> copied;  // [slot][chunk]
     std::vector<bool> busy;
     int next = 0;
     int threads = 1;
 
     std::mutex mu;
     std::condition_variable cv_work, cv_done;
-    std::deque<std::pair<job *, int>> queue;  // (job, part)
-    int in_flight = 0;                        // jobs queued or running
+    std::deque<chunk> queue;
+    int in_flight = 0;  // saves queued or running
     bool quit = false;
     ss_status error = SS_OK;
     std::string error_msg;
@@ -61,25 +73,24 @@ struct ss_kv_saver {
         }
         cv_work.notify_all();
         for (auto &t : workers) t.join();
-        for (hipEvent_t e : copied)
-            if (e) (void)hipEventDestroy(e);
+        for (auto &evs : copied)
+            for (hipEvent_t e : evs)
+                if (e) (void)hipEventDestroy(e);
         for (void *p : staging)
             if (p) (void)hipHostFree(p);
     }
 
-    // the units [u0, u1) of a job: every token of every (sequence, head)
-    void scatter(const job &jb, int part)
+    // every (sequence, head) of the token rows [r0, r1)
+    void scatter(const job &jb, int64_t r0, int64_t r1)
     {
-        const int units = B * Hkv;
-        const int u0 = (int)((int64_t)units * part / threads), u1 = (int)((int64_t)units * (part + 1) / threads);
         const uint16_t *src = static_cast<const uint16_t *>(staging[jb.slot]);
-        for (int u = u0; u < u1; ++u) {
-            const int b = u / Hkv, g = u - b * Hkv;
-            for (int i = 0; i < jb.n_new; ++i) {
-                const int T = jb.len[b] + i;
-                const int j = T / blk, p = T - j * blk;
-                const uint16_t *kv = src + (((int64_t)b * jb.n_new + i) * Hkv + g) * 2 * d;
-                uint8_t *rec = pool + pool_off[u] + (int64_t)j * (int64_t)record_bytes;
+        for (int64_t r = r0; r < r1; ++r) {
+            const int b = (int)(r / jb.n_new), i = (int)(r - (int64_t)b * jb.n_new);
+            const int T = jb.len[b] + i;
+            const int j = T / blk, p = T - j * blk;
+            for (int g = 0; g < Hkv; ++g) {
+                const uint16_t *kv = src + (r * Hkv + g) * 2 * d;
+                uint8_t *rec = pool + pool_off[(size_t)b * Hkv + g] + (int64_t)j * (int64_t)record_bytes;
                 std::memcpy(rec + (size_t)p * d * 2, kv, (size_t)d * 2);
                 uint16_t *vt = reinterpret_cast<uint16_t *>(rec + (size_t)blk * d * 2);
                 for (int c = 0; c < d; ++c) vt[c * blk + p] = kv[d + c];
@@ -90,7 +101,7 @@ struct ss_kv_saver {
     void worker()
     {
         for (;;) {
-            std::pair<job *, int> w;
+            chunk w;
             {
                 std::unique_lock<std::mutex> lk(mu);
                 cv_work.wait(lk, [&] { return quit || !queue.empty(); });
@@ -98,16 +109,17 @@ struct ss_kv_saver {
                 w = queue.front();
                 queue.pop_front();
             }
-            job *jb = w.first;
-            hipError_t e = hipEventSynchronize(copied[jb->slot]);
-            if (e == hipSuccess) scatter(*jb, w.second);
-            if (jb->parts_left.fetch_sub(1) == 1 || e != hipSuccess) {
+            job *jb = w.jb;
+            hipError_t e = hipEventSynchronize(copied[jb->slot][w.ev]);
+            if (e == hipSuccess) scatter(*jb, w.r0, w.r1);
+            const bool last = jb->chunks_left.fetch_sub(1) == 1;
+            if (last || e != hipSuccess) {
                 std::lock_guard<std::mutex> g(mu);
                 if (e != hipSuccess && error == SS_OK) {
                     error = SS_ERR_HIP;
                     error_msg = std::string("ss_kv_save: wait for the copy: ") + hipGetErrorString(e);
                 }
-                if (jb->parts_left.load() == 0) {
+                if (last) {
                     busy[jb->slot] = false;
                     --in_flight;
                     delete jb;
@@ -153,13 +165,14 @@ ss_status ss_kv_saver_create(int B, int Hkv, int blk, int d, void *pool_host, co
     sv->pool_off.assign(pool_off, pool_off + (size_t)B * Hkv);
     sv->pool_blocks.assign(pool_blocks, pool_blocks + B);
     sv->threads = threads;
+    sv->row_bytes = (size_t)Hkv * 2 * d * 2;
     sv->staging.assign(staging_slots, nullptr);
-    sv->copied.assign(staging_slots, nullptr);
+    sv->copied.assign(staging_slots, std::vector<hipEvent_t>(kMaxChunks, nullptr));
     sv->busy.assign(staging_slots, false);
     for (int i = 0; i < staging_slots; ++i) {
         hipError_t e = hipHostMalloc(&sv->staging[i], sv->slot_bytes, hipHostMallocDefault);
-        if (e == hipSuccess)
-            e = hipEventCreateWithFlags(&sv->copied[i], hipEventDisableTiming | hipEventBlockingSync);
+        for (int c = 0; c < kMaxChunks && e == hipSuccess; ++c)
+            e = hipEventCreateWithFlags(&sv->copied[i][c], hipEventDisableTiming | hipEventBlockingSync);
         if (e != hipSuccess) {
             (void)hipGetLastError();
             delete sv;
@@ -199,21 +212,39 @@ ss_status ss_kv_save(ss_kv_saver *sv, const void *new_kv, int n_new, const int32
     if (sv->error != SS_OK) return ss::fail(sv->error, "%s", sv->error_msg.c_str());
     const int slot = sv->next;
     sv->wait_locked(lk, slot);  // its previous scatter must be finished
-    const size_t bytes = (size_t)sv->B * n_new * sv->Hkv * 2 * sv->d * 2;
-    hipError_t e = hipMemcpyAsync(sv->staging[slot], new_kv, bytes, hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipEventRecord(sv->copied[slot], s);
-    if (e != hipSuccess) {
-        (void)hipGetLastError();
-        return ss::fail(SS_ERR_HIP, "ss_kv_save: copy to staging: %s", hipGetErrorString(e));
+    // chunks of whole token rows, copied one after another on `stream`; each
+    // is scattered as soon as its own copy has landed, so scattering overlaps
+    // the copies still running
+    const int64_t rows = (int64_t)sv->B * n_new;
+    const size_t total = (size_t)rows * sv->row_bytes;
+    size_t target = std::max(kMinChunkBytes, total / (size_t)(4 * sv->threads));
+    int64_t per = std::max<int64_t>(1, (int64_t)((target + sv->row_bytes - 1) / sv->row_bytes));
+    if ((rows + per - 1) / per > kMaxChunks) per = (rows + kMaxChunks - 1) / kMaxChunks;
+    const int n_chunks = (int)((rows + per - 1) / per);
+    const uint8_t *src = static_cast<const uint8_t *>(new_kv);
+    uint8_t *dst = static_cast<uint8_t *>(sv->staging[slot]);
+    for (int c = 0; c < n_chunks; ++c) {
+        const int64_t r0 = c * per, r1 = std::min(rows, r0 + per);
+        hipError_t e = hipMemcpyAsync(dst + r0 * sv->row_bytes, src + r0 * sv->row_bytes,
+                                      (size_t)(r1 - r0) * sv->row_bytes, hipMemcpyDeviceToHost, s);
+        if (e == hipSuccess) e = hipEventRecord(sv->copied[slot][c], s);
+        if (e != hipSuccess) {
+            (void)hipGetLastError();
+            // copies enqueued so far are harmless: the slot is not marked busy
+            return ss::fail(SS_ERR_HIP, "ss_kv_save: copy to staging: %s", hipGetErrorString(e));
+        }
     }
     job *jb = new job;
     jb->slot = slot;
     jb->n_new = n_new;
     jb->len.assign(len, len + sv->B);
-    jb->parts_left.store(sv->threads);
+    jb->chunks_left.store(n_chunks);
     sv->busy[slot] = true;
     ++sv->in_flight;
-    for (int part = 0; part < sv->threads; ++part) sv->queue.emplace_back(jb, part);
+    for (int c = 0; c < n_chunks; ++c) {
+        const int64_t r0 = c * per, r1 = std::min(rows, r0 + per);
+        sv->queue.push_back(chunk{jb, c, r0, r1});
+    }
     sv->next = (slot + 1) % (int)sv->staging.size();
     lk.unlock();
     sv->cv_work.notify_all();
