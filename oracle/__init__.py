@@ -49,8 +49,13 @@ def load(path):
     L.oracle_attention.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, ctypes.c_double, vp]
     L.oracle_append.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, vp, vp]
     L.oracle_save.argtypes = [vp, i32, vp, i32, i32, i32, i32, vp, vp, vp]
+    L.oracle_ws_decode.argtypes = [vp, i32, i32, i32, i32, i32, i32, sz]
+    L.oracle_ws_decode.restype = i64
+    L.oracle_ws_prefill.argtypes = [i64, i64, i64, i32, i32, i32, sz, i32]
+    L.oracle_ws_prefill.restype = i64
+    L.oracle_schedule.argtypes = [vp, i32, i64, vp, vp]
     for f in ("oracle_build_metadata", "oracle_score", "oracle_select", "oracle_lru_step",
-              "oracle_gather", "oracle_attention", "oracle_append", "oracle_save"):
+              "oracle_gather", "oracle_attention", "oracle_append", "oracle_save", "oracle_schedule"):
         getattr(L, f).restype = i32
     return L
 
@@ -165,6 +170,32 @@ class Oracle:
         if rc == 2:
             raise OverflowError("a token lies past the unit's pool blocks")
         _check(rc, "save")
+
+    # O8
+    def ws_decode(self, sel_hist, w, record_bytes, fallback=0):
+        """sel_hist int32 [m][layers][Hkv][k], oldest step first."""
+        h = _c(sel_hist, np.int32)
+        m, layers, Hkv, k = h.shape
+        r = self.L.oracle_ws_decode(_addr(h), m, layers, Hkv, k, w, fallback, record_bytes)
+        if r < 0:
+            raise RuntimeError("oracle ws_decode failed")
+        return int(r)
+
+    # O9
+    def ws_prefill(self, prompt, done, chunk, layers, Hkv, blk, record_bytes, layer_segmented):
+        r = self.L.oracle_ws_prefill(prompt, done, chunk, layers, Hkv, blk, record_bytes, int(bool(layer_segmented)))
+        if r < 0:
+            raise RuntimeError("oracle ws_prefill failed")
+        return int(r)
+
+    # O10
+    def schedule(self, ws, m_avl):
+        ws = _c(ws, np.int64)
+        admit = np.empty(ws.size, np.int32)
+        used = ctypes.c_int64(0)
+        _check(self.L.oracle_schedule(_addr(ws), ws.size, int(m_avl), _addr(admit), ctypes.addressof(used)),
+               "schedule")
+        return admit, used.value
 
     def lru(self, B, Hkv, nblk, cap):
         return LRU(self.L, B, Hkv, nblk, cap)

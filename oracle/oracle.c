@@ -2,8 +2,9 @@
  * CPU oracle for the decode-step hot path of SparseServe (arXiv 2509.24626):
  * block metadata, block criticality scoring, top-k block selection, the LRU
  * HBM block cache, the miss gather and sparse attention over the selected
- * blocks; and on the saving side, appending new tokens to the open blocks
- * (with metadata when a block fills) and saving them to the DRAM pool.
+ * blocks; on the saving side, appending new tokens to the open blocks
+ * (with metadata when a block fills) and saving them to the DRAM pool; and
+ * the working-set estimates and batch control of the scheduler.
  *
  * TEST INFRASTRUCTURE ONLY.  Nothing in the product library calls, links or
  * loads this file; only the tests, the smoke check and the benchmark's CPU
@@ -527,5 +528,106 @@ int oracle_save(const uint16_t *new_kv, int n_new, const int32_t *len, int B, in
                 put_token(rec, blk, d, p, new_kv + (((int64_t)b * n_new + i) * Hkv + g) * 2 * d);
             }
         }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------
+ * O8  Working set of a decoding request (Section 3.3, decoding working
+ * set): per (layer, KV head), the union of the blocks selected in the last
+ * w decoding steps; the request's working set is the HBM the union takes,
+ *     record_bytes * sum over (layer, head) of |union|.
+ *   sel_hist : [m][layers][Hkv][k] the request's selections of its m
+ *              observed steps, oldest first; -1 entries are padding
+ *   fallback : blocks per (layer, head) counted when m == 0 (no history)
+ * Steps taken: the last min(w, m) steps, all their entries per (layer,
+ * head) collected, sorted, and the distinct non-negative values counted.
+ * ---------------------------------------------------------------------- */
+static int ascending_i32(const void *pa, const void *pb)
+{
+    int32_t a = *(const int32_t *)pa, b = *(const int32_t *)pb;
+    return (a > b) - (a < b);
+}
+
+int64_t oracle_ws_decode(const int32_t *sel_hist, int m, int layers, int Hkv, int k, int w,
+                         int fallback, size_t record_bytes)
+{
+    if (m < 0 || layers <= 0 || Hkv <= 0 || k <= 0 || w <= 0)
+        return -1;
+    if (m == 0)
+        return (int64_t)fallback * layers * Hkv * (int64_t)record_bytes;
+    int n_steps = m < w ? m : w;
+    int32_t *all = malloc(sizeof(int32_t) * (size_t)n_steps * k);
+    if (!all)
+        return -1;
+    int64_t blocks = 0;
+    for (int l = 0; l < layers; ++l)
+        for (int g = 0; g < Hkv; ++g) {
+            int n = 0;
+            for (int s = m - n_steps; s < m; ++s)
+                for (int i = 0; i < k; ++i) {
+                    int32_t j = sel_hist[(((int64_t)s * layers + l) * Hkv + g) * k + i];
+                    if (j >= 0)
+                        all[n++] = j;
+                }
+            qsort(all, (size_t)n, sizeof(int32_t), ascending_i32);
+            for (int i = 0; i < n; ++i)
+                if (i == 0 || all[i] != all[i - 1])
+                    ++blocks;
+        }
+    free(all);
+    return blocks * (int64_t)record_bytes;
+}
+
+/* ------------------------------------------------------------------------
+ * O9  Working set of a prefill request (Section 3.3, prefill working set):
+ * the HBM its KV needs in the current iteration, which is exact.
+ *   layer-segmented prefill: one layer of KV of the whole prompt,
+ *       ceil(prompt / blk) blocks per KV head;
+ *   chunked prefill: the KV of every chunk so far, this one included, in
+ *       every layer, ceil(min(prompt, done + chunk) / blk) blocks per KV head
+ *       per layer.
+ * ---------------------------------------------------------------------- */
+int64_t oracle_ws_prefill(int64_t prompt, int64_t done, int64_t chunk, int layers, int Hkv, int blk,
+                          size_t record_bytes, int layer_segmented)
+{
+    if (prompt < 0 || done < 0 || chunk < 0 || layers <= 0 || Hkv <= 0 || blk <= 0)
+        return -1;
+    int64_t tokens, layer_count;
+    if (layer_segmented) {
+        tokens = prompt;
+        layer_count = 1;
+    } else {
+        tokens = done + chunk < prompt ? done + chunk : prompt;
+        layer_count = layers;
+    }
+    int64_t blocks = (tokens + blk - 1) / blk;
+    return blocks * Hkv * layer_count * (int64_t)record_bytes;
+}
+
+/* ------------------------------------------------------------------------
+ * O10  Working-set-aware batch control (Section 3.3, Algorithm 1): walk the
+ * initial batch in its order; a request joins the batch if the HBM used so
+ * far plus its working set stays within m_avl, otherwise it is reset
+ * (rejected for this iteration).
+ *   ws     : [n] working-set bytes of the initial batch's requests, in order
+ *   admit  : [n] 1 if the request joins the batch, 0 if it is reset
+ *   m_used : the HBM the admitted requests take
+ * ---------------------------------------------------------------------- */
+int oracle_schedule(const int64_t *ws, int n, int64_t m_avl, int32_t *admit, int64_t *m_used)
+{
+    if (n < 0)
+        return 1;
+    int64_t used = 0;
+    for (int i = 0; i < n; ++i) {
+        if (ws[i] < 0)
+            return 1;
+        if (used + ws[i] <= m_avl) {
+            admit[i] = 1;
+            used += ws[i];
+        } else {
+            admit[i] = 0;
+        }
+    }
+    *m_used = used;
     return 0;
 }

@@ -616,6 +616,76 @@ def pin_save_capacity_error(O):
     raise AssertionError("saving past the pool did not fail")
 
 
+# ------------------------------------------- O8-O10 working sets, Alg. 1
+def pin_ws_fixture(O):
+    """Hand-worked fixture (golden/working_set.txt): a 4-step history with
+    w = 2, and the prefill working sets of both prefill strategies."""
+    fx = read_fixture("working_set.txt")
+    hist = np.array([[int(x) for x in fx[f"dec_sel{s}"]] for s in range(4)], np.int32).reshape(4, 1, 1, 3)
+    want = [int(x) for x in fx["dec_bytes"]]
+    got = [O.ws_decode(hist[:m + 1], 2, 8192) for m in range(4)]
+    assert got == want, (got, want)
+    assert O.ws_prefill(1000, 512, 256, 32, 8, 16, 8192, True) == int(fx["pre_seg"][0])
+    assert O.ws_prefill(1000, 512, 256, 32, 8, 16, 8192, False) == int(fx["pre_chunk"][0])
+    assert O.ws_prefill(1000, 768, 512, 32, 8, 16, 8192, False) == int(fx["pre_chunk_last"][0])
+
+
+def pin_ws_bruteforce(O):
+    """Random histories vs Python sets: per (layer, head) the union of the
+    last w steps' non-negative entries."""
+    rng = np.random.default_rng(31)
+    for trial in range(20):
+        m, layers, Hkv, k, w = int(rng.integers(1, 9)), int(rng.integers(1, 4)), int(rng.integers(1, 4)), \
+            int(rng.integers(1, 6)), int(rng.integers(1, 6))
+        hist = rng.integers(-1, 12, size=(m, layers, Hkv, k)).astype(np.int32)
+        want = 0
+        for l in range(layers):
+            for g in range(Hkv):
+                u = set()
+                for s in range(max(0, m - w), m):
+                    u |= {int(x) for x in hist[s, l, g] if x >= 0}
+                want += len(u)
+        assert O.ws_decode(hist, w, 4096) == want * 4096, trial
+
+
+def pin_ws_closed_forms(O):
+    """The same selection every step gives k blocks per (layer, head);
+    disjoint selections give min(w, m) * k; no history uses the fallback."""
+    layers, Hkv, k, rb = 2, 3, 4, 8192
+    same = np.tile(np.arange(k, dtype=np.int32), (7, layers, Hkv, 1))
+    assert O.ws_decode(same, 12, rb) == k * layers * Hkv * rb
+    disj = (np.arange(7 * k, dtype=np.int32).reshape(7, 1, 1, k) + np.zeros((1, layers, Hkv, 1), np.int32))
+    for w in (1, 3, 7, 12):
+        assert O.ws_decode(disj, w, rb) == min(w, 7) * k * layers * Hkv * rb, w
+    assert O.ws_decode(np.zeros((0, layers, Hkv, k), np.int32), 12, rb, fallback=5) == 5 * layers * Hkv * rb
+
+
+def pin_schedule_fixture(O):
+    """Hand-worked fixture (golden/schedule_alg1.txt)."""
+    fx = read_fixture("schedule_alg1.txt")
+    for case in "abc":
+        admit, used = O.schedule([int(x) for x in fx[f"{case}_ws"]], int(fx[f"{case}_avl"][0]))
+        assert admit.tolist() == [int(x) for x in fx[f"{case}_admit"]], case
+        assert used == int(fx[f"{case}_used"][0]), case
+
+
+def pin_schedule_invariants(O):
+    """Random batches: the admitted requests fit M_avl; every reset request
+    would not have fitted at its turn (greedy in the given order)."""
+    rng = np.random.default_rng(32)
+    for _ in range(50):
+        ws = rng.integers(0, 100, size=int(rng.integers(0, 20)))
+        avl = int(rng.integers(0, 600))
+        admit, used = O.schedule(ws, avl)
+        assert used == int(ws[admit == 1].sum()) <= avl
+        run = 0
+        for x, a in zip(ws, admit):
+            if a:
+                run += x
+            else:
+                assert run + x > avl
+
+
 GROUPS = {
     "meta": [pin_meta_bruteforce, pin_meta_ragged_untouched, pin_meta_signed_zero, pin_meta_record_offsets],
     "score": [pin_score_fixture, pin_score_upper_bound, pin_score_point_block, pin_score_corner_tight,
@@ -626,5 +696,7 @@ GROUPS = {
     "attention": [pin_attention_fixture, pin_attention_dense, pin_attention_subset, pin_attention_empty],
     "append": [pin_append_record_layout, pin_append_ragged_positions, pin_append_capacity_error],
     "save": [pin_save_spans_blocks, pin_save_full_block_record, pin_save_capacity_error],
+    "ws": [pin_ws_fixture, pin_ws_bruteforce, pin_ws_closed_forms],
+    "schedule": [pin_schedule_fixture, pin_schedule_invariants],
 }
 ALL_PINS = [p for ps in GROUPS.values() for p in ps]

@@ -69,6 +69,16 @@ MUTANTS = [
     ("save-ignores-len", "save", "int T = len[b] + i;", "int T = i;"),
     ("save-token-major-input", "save", "new_kv + (((int64_t)b * n_new + i) * Hkv + g) * 2 * d",
      "new_kv + (((int64_t)i * B + b) * Hkv + g) * 2 * d"),
+    ("ws-whole-history", "ws", "int n_steps = m < w ? m : w;", "int n_steps = m;"),
+    ("ws-counts-duplicates", "ws", "if (i == 0 || all[i] != all[i - 1])", "if (1)"),
+    ("ws-counts-padding", "ws", "                    if (j >= 0)\n                        all[n++] = j;",
+     "                    all[n++] = j;"),
+    ("ws-oldest-steps", "ws", "for (int s = m - n_steps; s < m; ++s)", "for (int s = 0; s < n_steps; ++s)"),
+    ("ws-chunked-one-layer", "ws", "        layer_count = layers;", "        layer_count = 1;"),
+    ("ws-prefill-floor", "ws", "int64_t blocks = (tokens + blk - 1) / blk;", "int64_t blocks = tokens / blk;"),
+    ("schedule-strict", "schedule", "if (used + ws[i] <= m_avl) {", "if (used + ws[i] < m_avl) {"),
+    ("schedule-stops-at-first-reject", "schedule", "            admit[i] = 0;\n",
+     "            admit[i] = 0;\n            m_avl = -1;\n"),
     ("save-ignores-offsets", "save", "(char *)pool + pool_off[u] + (int64_t)j",
      "(char *)pool + (int64_t)u * pool_blocks[b] * (int64_t)record_bytes + (int64_t)j"),
 ]
