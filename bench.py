@@ -246,6 +246,11 @@ def main():
     for name in iso:
         iso[name]["traffic"] = traffic(name, key)
 
+    # ------------------------------------------- working sets (Section 3.3)
+    ws_study = None
+    if new_kv is None and cfg.layers == 1:
+        ws_study = working_set_study(cfg, layers[0], qstreams[0][-1][0], warmup + steps, args.seed, ss, torch)
+
     # ------------------------------------------- saving bandwidth
     save_bw = None if args.no_save_bandwidth else save_bandwidth(ss, torch, H)
 
@@ -292,6 +297,8 @@ def main():
                                        "them with FlashD2H; the last save is waited for inside the timed region"}
     if save_bw is not None:
         result["save_bandwidth"] = save_bw
+    if ws_study is not None:
+        result["working_set"] = ws_study
     print(json.dumps(result), flush=True)
     for L in layers:
         L.close()
@@ -426,6 +433,64 @@ def summarize_pmc(args):
     print("TRAFFIC = " + json.dumps(table, indent=1))
 
 
+def working_set_study(cfg, L, q32, first_step, seed, ss, torch, steps=28, window=12):
+    """Decoding working sets on the workload itself (Section 3.3), after the
+    timed region: `steps` more decode steps with the query drift continuing.
+    Each step's selection (its host copy) goes to a working-set tracker; the
+    figures are the tracker's cost per layer-step and per estimate, the
+    working sets (window 12), Algorithm 1 against the layer's HBM cache, and
+    the mean overlap between each step's selection and the union of the
+    preceding w steps' selections (the paper's Figure 7 measurement, on
+    synthetic data), for steps after the first 16."""
+    from synth import gen
+    B, Hkv, k = cfg.B, cfg.Hkv, cfg.k
+    ids = np.arange(B, dtype=np.int64)
+    tr = ss.ss_ws_create(1, Hkv, window, cfg.record_bytes)
+    hist = []
+    obs_ms = []
+    try:
+        for i in range(steps):
+            q32, q = gen.drift(q32, cfg.drift, seed, 0, first_step + i)
+            L.step(first_step + i, q)
+            torch.cuda.synchronize()
+            sel = L.sel_h.numpy().copy()
+            hist.append(sel)
+            t0 = time.perf_counter()
+            ss.ss_ws_observe(tr, 0, first_step + i, ids, sel)
+            obs_ms.append((time.perf_counter() - t0) * 1e3)
+        t0 = time.perf_counter()
+        ws = ss.ss_ws_decode_bytes(tr, ids)
+        est_ms = (time.perf_counter() - t0) * 1e3
+        cache_bytes = int(L.capacity.astype(np.int64).sum()) * cfg.record_bytes
+        admit, used = ss.ss_schedule_batch(ws, cache_bytes)
+        # a tighter HBM budget: a quarter of the cache
+        admit_q, used_q = ss.ss_schedule_batch(ws, cache_bytes // 4)
+    finally:
+        ss.ss_ws_destroy(tr)
+    overlap = {}
+    H = np.stack(hist)  # [steps][B][Hkv][k]
+    for w in (1, 2, 4, 8, 12, 16):
+        fr = []
+        for t in range(16, steps):
+            for b in range(B):
+                for g in range(Hkv):
+                    cur = H[t, b, g]
+                    cur = cur[cur >= 0]
+                    prev = np.unique(H[max(0, t - w):t, b, g])
+                    fr.append(np.isin(cur, prev).mean() if cur.size else 1.0)
+        overlap[str(w)] = round(float(np.mean(fr)), 4)
+    blocks = ws / cfg.record_bytes / Hkv
+    res = {"window": window, "observe_ms_per_layer_step": round(float(np.median(obs_ms[2:])), 4),
+           "estimate_ms_for_batch": round(est_ms, 4),
+           "ws_blocks_per_head": {"mean": round(float(blocks.mean()), 1), "min": int(blocks.min()),
+                                  "max": int(blocks.max()), "k": k},
+           "ws_bytes_total": int(ws.sum()), "hbm_cache_bytes": cache_bytes,
+           "alg1_admitted_full_cache": int(admit.sum()), "alg1_admitted_quarter_cache": int(admit_q.sum()),
+           "overlap_with_preceding_window": overlap, "steps": steps}
+    log(f"working sets: {res}")
+    return res
+
+
 def save_bandwidth(ss, torch, H, B=4, n=8192, Hkv=8, reps=3):
     """Saving a prefill-sized batch of new KV (B sequences x n tokens x Hkv
     heads, 128 MiB) to a pinned DRAM pool as block records, for blocks of 8,
@@ -456,12 +521,13 @@ def save_bandwidth(ss, torch, H, B=4, n=8192, Hkv=8, reps=3):
             saver = ss.ss_kv_saver_create(B, Hkv, blk, D, pool.host, off, np.full(B, nb, np.int32), n, 1, 8)
             try:
                 ts = []
-                for _ in range(reps):
+                for r in range(reps + 1):  # the first, untimed, also lets idle worker threads settle
                     torch.cuda.synchronize()
                     t0 = time.perf_counter()
                     ss.ss_kv_save(saver, kv, n, np.zeros(B, np.int32))
                     ss.ss_kv_save_wait(saver)
-                    ts.append(time.perf_counter() - t0)
+                    if r:
+                        ts.append(time.perf_counter() - t0)
                 out["flashd2h"] = round(nbytes / float(np.median(ts)) / 1e9, 2)
             finally:
                 ss.ss_kv_saver_destroy(saver)

@@ -283,6 +283,46 @@ ss_status ss_kv_save(ss_kv_saver *saver, const void *new_kv, int n_new, const in
  * met by the asynchronous part (SS_ERR_HIP). */
 ss_status ss_kv_save_wait(ss_kv_saver *saver);
 
+/* ------------------------------------------- working sets, batch control
+ * Working-set-aware batch size control (Section 3.3).  A decoding
+ * request's working set is, per (layer, KV head), the union of the blocks
+ * selected over its last `window` observed decoding steps (Section 3.3
+ * uses 12), times record_bytes; the tracker follows it incrementally.
+ * Requests are named by caller-chosen int64 ids.  Host-only; not
+ * thread-safe per tracker. */
+typedef struct ss_ws ss_ws;
+/* window: 1..255 observations */
+ss_status ss_ws_create(int layers, int Hkv, int window, size_t record_bytes, ss_ws **out);
+void ss_ws_destroy(ss_ws *ws);
+/* One decoding step of one layer for a batch: req_ids host int64 [B]
+ * (distinct); sel host int32 [B][Hkv][k] (-1 entries ignored; block
+ * indices below 2^24).  k must be the same in every call.  Steps of a
+ * (request, layer) must increase (SS_ERR_INVALID_ARG otherwise, nothing
+ * recorded).  Unknown ids start a history. */
+ss_status ss_ws_observe(ss_ws *ws, int layer, int64_t step, const int64_t *req_ids, int B, const int32_t *sel,
+                        int k);
+/* bytes[i] = working set of request req_ids[i]: record_bytes times the sum
+ * over (layer, head) of its union size; a (layer, head) with no
+ * observation yet counts fallback_blocks[i] blocks (NULL: 0), e.g. one
+ * step's selection, min(k, blocks), for a request that just left
+ * prefill. */
+ss_status ss_ws_decode_bytes(const ss_ws *ws, const int64_t *req_ids, int n, const int32_t *fallback_blocks,
+                             int64_t *bytes);
+/* Drops a request's history (finished or reset). */
+ss_status ss_ws_forget(ss_ws *ws, int64_t req_id);
+/* A prefill request's working set (exact): layer-segmented prefill needs
+ * one layer of the prompt's KV, ceil(prompt/blk) blocks per KV head;
+ * chunked prefill the KV of every chunk so far in every layer,
+ * ceil(min(prompt, done + chunk)/blk) blocks per KV head and layer.
+ * Returns bytes, or -1 for invalid arguments. */
+int64_t ss_ws_prefill_bytes(int64_t prompt_tokens, int64_t done_tokens, int64_t chunk_tokens, int layers, int Hkv,
+                            int blk, size_t record_bytes, int layer_segmented);
+/* Algorithm 1 (Section 3.3): walks the initial batch in its order and
+ * admits request i (admit[i] = 1) if the working sets admitted so far plus
+ * ws_bytes[i] stay within m_avl, else resets it (admit[i] = 0).
+ * ws_bytes host int64 [n] (>= 0); *m_used = bytes admitted. */
+ss_status ss_schedule_batch(const int64_t *ws_bytes, int n, int64_t m_avl, int32_t *admit, int64_t *m_used);
+
 /* ------------------------------------------------------- one layer's step
  * The decode step of one layer over the HBM/DRAM hierarchy (Section 3.1's
  * executor / cache-manager exchange): score and select on the GPU, copy the

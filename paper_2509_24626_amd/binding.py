@@ -73,6 +73,13 @@ _SIGNATURES = {
     "ss_kv_saver_destroy": (None, [_vp]),
     "ss_kv_save": (_i32, [_vp, _vp, _i32, _vp, _vp]),
     "ss_kv_save_wait": (_i32, [_vp]),
+    "ss_ws_create": (_i32, [_i32, _i32, _i32, _sz, _vp]),
+    "ss_ws_destroy": (None, [_vp]),
+    "ss_ws_observe": (_i32, [_vp, _i32, _i64, _vp, _i32, _vp, _i32]),
+    "ss_ws_decode_bytes": (_i32, [_vp, _vp, _i32, _vp, _vp]),
+    "ss_ws_forget": (_i32, [_vp, _i64]),
+    "ss_ws_prefill_bytes": (_i64, [_i64, _i64, _i64, _i32, _i32, _i32, _sz, _i32]),
+    "ss_schedule_batch": (_i32, [_vp, _i32, _i64, _vp, _vp]),
 }
 
 
@@ -275,3 +282,54 @@ def ss_kv_save(saver, new_kv, n_new, len_host, stream=None):
 
 def ss_kv_save_wait(saver):
     _check(lib().ss_kv_save_wait(saver))
+
+
+def ss_ws_create(layers, Hkv, window, record_bytes):
+    h = ctypes.c_void_p()
+    _check(lib().ss_ws_create(layers, Hkv, window, record_bytes, ctypes.byref(h)))
+    return h.value
+
+
+def ss_ws_destroy(ws):
+    lib().ss_ws_destroy(ws)
+
+
+def ss_ws_observe(ws, layer, step, req_ids, sel):
+    """req_ids int64 [B]; sel int32 [B][Hkv][k] (host)."""
+    import numpy as np
+    req_ids = np.ascontiguousarray(req_ids, dtype=np.int64)
+    sel = np.ascontiguousarray(sel, dtype=np.int32)
+    _check(lib().ss_ws_observe(ws, layer, step, req_ids.ctypes.data, req_ids.size, sel.ctypes.data, sel.shape[-1]))
+
+
+def ss_ws_decode_bytes(ws, req_ids, fallback_blocks=None):
+    import numpy as np
+    req_ids = np.ascontiguousarray(req_ids, dtype=np.int64)
+    out = np.empty(req_ids.size, np.int64)
+    fb = None if fallback_blocks is None else np.ascontiguousarray(fallback_blocks, dtype=np.int32)
+    _check(lib().ss_ws_decode_bytes(ws, req_ids.ctypes.data, req_ids.size, None if fb is None else fb.ctypes.data,
+                                    out.ctypes.data))
+    return out
+
+
+def ss_ws_forget(ws, req_id):
+    _check(lib().ss_ws_forget(ws, req_id))
+
+
+def ss_ws_prefill_bytes(prompt_tokens, done_tokens, chunk_tokens, layers, Hkv, blk, record_bytes, layer_segmented):
+    r = lib().ss_ws_prefill_bytes(prompt_tokens, done_tokens, chunk_tokens, layers, Hkv, blk, record_bytes,
+                                  int(bool(layer_segmented)))
+    if r < 0:
+        raise SparseServeError(SS_ERR_INVALID_ARG, "ss_ws_prefill_bytes: invalid arguments")
+    return r
+
+
+def ss_schedule_batch(ws_bytes, m_avl):
+    """Returns (admit int32 [n], m_used)."""
+    import numpy as np
+    ws_bytes = np.ascontiguousarray(ws_bytes, dtype=np.int64)
+    admit = np.empty(ws_bytes.size, np.int32)
+    used = ctypes.c_int64(0)
+    _check(lib().ss_schedule_batch(ws_bytes.ctypes.data, ws_bytes.size, m_avl, admit.ctypes.data,
+                                   ctypes.byref(used)))
+    return admit, used.value

@@ -136,6 +136,25 @@ pool &shared_pool()
 
 }  // namespace
 
+namespace ss {
+// Runs f(begin, end) over [0, n) split across the process's resolve
+// workers (at most max_threads of them); returns when all parts are done.
+void parallel_for(int64_t n, int max_threads, const std::function<void(int64_t, int64_t)> &f)
+{
+    if (n <= 0) return;
+    std::lock_guard<std::mutex> lock(g_pool_mu);
+    pool &workers = shared_pool();
+    const int T = (int)std::max<int64_t>(1, std::min<int64_t>({(int64_t)workers.size(), (int64_t)max_threads, n}));
+    if (T == 1) {
+        f(0, n);
+        return;
+    }
+    workers.run([&](int w) {
+        if (w < T) f(n * w / T, n * (w + 1) / T);
+    });
+}
+}  // namespace ss
+
 struct ss_cache {
     int B = 0, Hkv = 0;
     size_t record_bytes = 0;

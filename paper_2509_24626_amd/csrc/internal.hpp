@@ -9,6 +9,7 @@
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
+#include <functional>
 
 #include "../../include/sparseserve.h"
 
@@ -27,6 +28,9 @@ constexpr int kMaxGroup = 16;
 constexpr int kMaxBlocks = 65536;
 
 inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
+
+// f(begin, end) over [0, n) on the library's host worker threads
+void parallel_for(int64_t n, int max_threads, const std::function<void(int64_t, int64_t)> &f);
 
 // Start/stop events that a measurement attaches to the next kernel the
 // calling thread launches (ss_time_next_kernel); the launch takes and
