@@ -49,6 +49,10 @@ def load(path):
     L.oracle_attention.argtypes = [vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, ctypes.c_double, vp]
     L.oracle_append.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, vp, vp]
     L.oracle_save.argtypes = [vp, i32, vp, i32, i32, i32, i32, vp, vp, vp]
+    L.oracle_build_metadata_mean.argtypes = [vp, vp, vp, i32, i32, i32, i32, i32, sz, vp]
+    L.oracle_score_variant.argtypes = [vp, vp, i32, i32, vp, i32, i32, i32, i32, i32, vp]
+    L.oracle_build_metadata_mean.restype = i32
+    L.oracle_score_variant.restype = i32
     L.oracle_ws_decode.argtypes = [vp, i32, i32, i32, i32, i32, i32, sz]
     L.oracle_ws_decode.restype = i64
     L.oracle_ws_prefill.argtypes = [i64, i64, i64, i32, i32, i32, sz, i32]
@@ -170,6 +174,28 @@ class Oracle:
         if rc == 2:
             raise OverflowError("a token lies past the unit's pool blocks")
         _check(rc, "save")
+
+    # O11
+    def build_metadata_mean(self, base, unit_off, nblk, B, Hkv, nblk_max, blk, d, meta=None):
+        unit_off = _c(unit_off, np.int64)
+        nblk = _c(nblk, np.int32)
+        if meta is None:
+            meta = np.zeros((B, Hkv, nblk_max, d), dtype=np.uint16)
+        _check(self.L.oracle_build_metadata_mean(_addr(base), _addr(unit_off), _addr(nblk), B, Hkv, nblk_max, blk,
+                                                 d, record_bytes(blk, d), _addr(meta)), "build_metadata_mean")
+        return meta
+
+    # O12
+    def score_variant(self, q, meta, kind, agg, nblk, Hq, Hkv, nblk_max, d):
+        """kind 0 cuboid / 1 mean-key metadata; agg 0 max / 1 sum over the group's heads."""
+        q = _c(q, np.uint16)
+        meta = _c(meta, np.uint16)
+        nblk = _c(nblk, np.int32)
+        B = q.shape[0]
+        S = np.empty((B, Hkv, nblk_max), dtype=np.float64)
+        _check(self.L.oracle_score_variant(_addr(q), _addr(meta), kind, agg, _addr(nblk), B, Hq, Hkv, nblk_max, d,
+                                           _addr(S)), "score_variant")
+        return S
 
     # O8
     def ws_decode(self, sel_hist, w, record_bytes, fallback=0):

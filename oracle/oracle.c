@@ -4,7 +4,8 @@
  * HBM block cache, the miss gather and sparse attention over the selected
  * blocks; on the saving side, appending new tokens to the open blocks
  * (with metadata when a block fills) and saving them to the DRAM pool; and
- * the working-set estimates and batch control of the scheduler.
+ * the working-set estimates and batch control of the scheduler; and the
+ * mean-key metadata and score variants the paper names.
  *
  * TEST INFRASTRUCTURE ONLY.  Nothing in the product library calls, links or
  * loads this file; only the tests, the smoke check and the benchmark's CPU
@@ -629,5 +630,101 @@ int oracle_schedule(const int64_t *ws, int n, int64_t m_avl, int32_t *admit, int
         }
     }
     *m_used = used;
+    return 0;
+}
+
+/* ------------------------------------------------------------------------
+ * O11  Mean-key block metadata (Section 2.2: the simplest metadata of the
+ * DSAs the paper cites is the mean of the block's token keys).  One d-vector
+ * per block, bf16.  The mean is rounded to bf16, a quantisation decision, so
+ * it is taken in the precision a GPU kernel works in: the channel's keys are
+ * summed in fp32 in token order, the sum divided by blk (a power of two, so
+ * exactly), and the result rounded to the nearest bf16, ties to even.
+ * meta layout [B*Hkv][nblk_max][d]; blocks j >= nblk[b] are not written.
+ * ---------------------------------------------------------------------- */
+static uint16_t f32_to_bf16_rne(float f)
+{
+    uint32_t u;
+    memcpy(&u, &f, sizeof u);
+    uint32_t lsb = (u >> 16) & 1u;
+    u += 0x7FFFu + lsb;
+    return (uint16_t)(u >> 16);
+}
+
+int oracle_build_metadata_mean(const void *base, const int64_t *unit_off, const int32_t *nblk, int B, int Hkv,
+                               int nblk_max, int blk, int d, size_t record_bytes, uint16_t *meta)
+{
+    if (B < 0 || Hkv <= 0 || nblk_max < 0 || blk <= 0 || d <= 0)
+        return 1;
+    for (int b = 0; b < B; ++b) {
+        int n = nblk[b] < nblk_max ? nblk[b] : nblk_max;
+        for (int g = 0; g < Hkv; ++g) {
+            int u = b * Hkv + g;
+            for (int j = 0; j < n; ++j) {
+                const char *unit_base = (const char *)base + unit_off[u];
+                const uint16_t *rec = (const uint16_t *)(unit_base + (int64_t)j * (int64_t)record_bytes);
+                uint16_t *m = meta + ((int64_t)u * nblk_max + j) * d;
+                for (int c = 0; c < d; ++c) {
+                    float s = 0.0f;
+                    for (int t = 0; t < blk; ++t)
+                        s = s + (float)bf(rec[t * d + c]);
+                    m[c] = f32_to_bf16_rne(s / (float)blk);
+                }
+            }
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------
+ * O12  Block scores for the metadata kinds and GQA aggregations (Section
+ * 2.2: a dot product of the block metadata with the query estimates the
+ * block's attention score; the paper's DSAs differ in the metadata).
+ *   kind 0 (cuboid, [lo, hi]): s_h(j) = sum_c max(q_h[c]*lo[c], q_h[c]*hi[c])
+ *   kind 1 (mean key m):       s_h(j) = sum_c q_h[c] * m[c]
+ *   agg 0: S = max over the group's query heads of s_h
+ *   agg 1: S = sum over the group's query heads of s_h (the mean over the
+ *          heads ranks the blocks the same way)
+ * meta layout: kind 0 [B*Hkv][nblk_max][2][d], kind 1 [B*Hkv][nblk_max][d].
+ * fp64 arithmetic; entries j >= nblk[b] are -inf.
+ * ---------------------------------------------------------------------- */
+int oracle_score_variant(const uint16_t *q, const uint16_t *meta, int kind, int agg, const int32_t *nblk, int B,
+                         int Hq, int Hkv, int nblk_max, int d, double *S)
+{
+    if (B < 0 || Hkv <= 0 || Hq <= 0 || Hq % Hkv != 0 || nblk_max < 0 || d <= 0 || kind < 0 || kind > 1 ||
+        agg < 0 || agg > 1)
+        return 1;
+    int G = Hq / Hkv;
+    int row = kind == 0 ? 2 * d : d;
+    for (int b = 0; b < B; ++b) {
+        int n = nblk[b] < nblk_max ? nblk[b] : nblk_max;
+        for (int g = 0; g < Hkv; ++g) {
+            int u = b * Hkv + g;
+            for (int j = 0; j < nblk_max; ++j) {
+                if (j >= n) {
+                    S[(int64_t)u * nblk_max + j] = -INFINITY;
+                    continue;
+                }
+                const uint16_t *mj = meta + ((int64_t)u * nblk_max + j) * row;
+                double best = -INFINITY, total = 0.0;
+                for (int i = 0; i < G; ++i) {
+                    const uint16_t *qh = q + ((int64_t)b * Hq + g * G + i) * d;
+                    double s = 0.0;
+                    for (int c = 0; c < d; ++c) {
+                        if (kind == 0) {
+                            double at_lo = bf(qh[c]) * bf(mj[c]);
+                            double at_hi = bf(qh[c]) * bf(mj[d + c]);
+                            s += at_lo > at_hi ? at_lo : at_hi;
+                        } else {
+                            s += bf(qh[c]) * bf(mj[c]);
+                        }
+                    }
+                    best = s > best ? s : best;
+                    total += s;
+                }
+                S[(int64_t)u * nblk_max + j] = agg == 0 ? best : total;
+            }
+        }
+    }
     return 0;
 }

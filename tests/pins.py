@@ -686,6 +686,110 @@ def pin_schedule_invariants(O):
                 assert run + x > avl
 
 
+# ------------------------------------------- O11/O12 metadata and score variants
+def _bf16_rne_from_f64(x):
+    """Library routine: torch's float64 -> bfloat16 conversion (round to nearest even)."""
+    return torch.tensor(np.asarray(x, np.float64)).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def pin_meta_mean_exact_cases(O):
+    """Inputs whose fp32 token sums are exact (small integers times 1/8):
+    the mean key equals the exact mean rounded by torch's bf16 conversion;
+    a block of identical tokens has exactly that token as its mean."""
+    rng = np.random.default_rng(41)
+    B, Hkv, nmax, d = 2, 2, 5, 16
+    for blk in (1, 4, 16, 32):
+        Kf = rng.integers(-40, 41, size=(B, Hkv, nmax, blk, d)) / 8.0
+        Kf[1, 1, 2] = Kf[1, 1, 2, :1]  # identical tokens
+        Kb = f64_to_bits(Kf)
+        rec = make_records(Kb, rand_bf16(Kb.shape, 49 + blk))  # V differs from K
+        off = dense_offsets(B * Hkv, nmax, blk, d)
+        nblk = np.array([nmax, 3], np.int32)
+        meta = O.build_metadata_mean(rec, off, nblk, B, Hkv, nmax, blk, d)
+        want = _bf16_rne_from_f64(Kf.mean(axis=3))
+        for b in range(B):
+            np.testing.assert_array_equal(meta[b, :, :nblk[b]], want[b, :, :nblk[b]])
+            assert np.all(meta[b, :, nblk[b]:] == 0)
+        np.testing.assert_array_equal(meta[1, 1, 2], Kb[1, 1, 2, 0])
+
+
+def pin_meta_mean_rounding(O):
+    """Random keys: the mean key is the exact mean rounded to bf16, except
+    where the exact mean lies within fp32 rounding of a bf16 rounding
+    midpoint (then it may be the neighbour)."""
+    B, Hkv, nmax, blk, d = 1, 4, 64, 16, 128
+    Kb = rand_bf16((B, Hkv, nmax, blk, d), 42)
+    rec = make_records(Kb, rand_bf16((B, Hkv, nmax, blk, d), 50))
+    meta = O.build_metadata_mean(rec, dense_offsets(B * Hkv, nmax, blk, d), np.array([nmax], np.int32), B, Hkv,
+                                 nmax, blk, d)
+    exact = bits_to_f64(Kb).mean(axis=3)
+    want = _bf16_rne_from_f64(exact)
+    diff = meta != want
+    assert diff.mean() < 1e-3
+    got = bits_to_f64(meta)
+    ulp = np.abs(bits_to_f64(want) - bits_to_f64(want ^ 1))  # spacing near the value
+    assert np.all(np.abs(got - exact) <= 0.5 * ulp * (1 + 2.0 ** -7) + 1e-30)
+
+
+def pin_score_variant_fixture(O):
+    """Hand-worked fixture (golden/score_box.txt): both kinds, both
+    aggregations, and the mean-key metadata of the two tokens."""
+    fx = read_fixture("score_box.txt")
+    K = np.array([[float(x) for x in fx["key_t0"]], [float(x) for x in fx["key_t1"]]])
+    q = f64_to_bits(np.array([[float(x) for x in fx["q_h0"]], [float(x) for x in fx["q_h1"]]]))[None]
+    cub = _meta_from_keys(K)[None, None, None]
+    Kb = f64_to_bits(K)[None, None, None]
+    mean = O.build_metadata_mean(make_records(Kb, Kb), np.zeros(1, np.int64), np.array([1], np.int32), 1, 1, 1, 2, 4)
+    np.testing.assert_array_equal(bits_to_f64(mean[0, 0, 0]), [float(x) for x in fx["mean_key"]])
+    one = np.array([1], np.int32)
+    for meta, kind, agg, key in ((cub, 0, 0, "score"), (cub, 0, 1, "cuboid_sum"), (mean, 1, 0, "mean_max"),
+                                 (mean, 1, 1, "mean_sum")):
+        S = O.score_variant(q, meta, kind, agg, one, 2, 1, 1, 4)
+        assert S[0, 0, 0] == float(fx[key][0]), (key, S)
+
+
+def pin_score_mean_is_mean_of_dots(O):
+    """With exact mean keys the mean-key score is the average of the token
+    scores q.k_t (linearity), computed here with numpy's matmul."""
+    rng = np.random.default_rng(43)
+    Hq, Hkv, nmax, blk, d = 4, 2, 6, 8, 32
+    Kf = rng.integers(-16, 17, size=(1, Hkv, nmax, blk, d)) / 4.0
+    qf = rng.integers(-8, 9, size=(1, Hq, d)) / 4.0
+    meta = f64_to_bits(Kf.mean(axis=3))  # exact: sums of quarters over 8 tokens
+    S = O.score_variant(f64_to_bits(qf), meta, 1, 0, np.array([nmax], np.int32), Hq, Hkv, nmax, d)
+    G = Hq // Hkv
+    for g in range(Hkv):
+        dots = np.einsum("hc,jtc->hjt", qf[0, g * G:(g + 1) * G], Kf[0, g])  # [G][nblk][blk]
+        np.testing.assert_allclose(S[0, g], dots.mean(axis=2).max(axis=0), rtol=0, atol=1e-12)
+
+
+def pin_score_aggregations_reduce_to_heads(O):
+    """max and sum over the group equal numpy's max and sum of the per-head
+    scores obtained with groups of one head (G = 1), for both kinds."""
+    rng = np.random.default_rng(44)
+    Hq, Hkv, nmax, d = 6, 2, 9, 16
+    G = Hq // Hkv
+    q = rand_bf16((2, Hq, d), 45)
+    nblk = np.array([nmax, 4], np.int32)
+    for kind in (0, 1):
+        if kind == 0:
+            a, b2 = rand_bf16((2, Hkv, nmax, d), 46), rand_bf16((2, Hkv, nmax, d), 47)
+            lo = np.where(bits_to_f64(a) <= bits_to_f64(b2), a, b2)
+            hi = np.where(bits_to_f64(a) <= bits_to_f64(b2), b2, a)
+            meta = np.stack([lo, hi], axis=3)
+        else:
+            meta = rand_bf16((2, Hkv, nmax, d), 48)
+        per_head_meta = np.repeat(meta, G, axis=1)  # head h uses its group's metadata
+        per = O.score_variant(q, per_head_meta, kind, 0, nblk, Hq, Hq, nmax, d)  # [2][Hq][nmax]
+        for agg, fn in ((0, np.max), (1, np.sum)):
+            S = O.score_variant(q, meta, kind, agg, nblk, Hq, Hkv, nmax, d)
+            for b in range(2):
+                n = nblk[b]
+                want = fn(per[b, :, :n].reshape(Hkv, G, n), axis=1)
+                np.testing.assert_allclose(S[b, :, :n], want, rtol=1e-13, atol=1e-12)
+                assert np.all(np.isneginf(S[b, :, n:]))
+
+
 GROUPS = {
     "meta": [pin_meta_bruteforce, pin_meta_ragged_untouched, pin_meta_signed_zero, pin_meta_record_offsets],
     "score": [pin_score_fixture, pin_score_upper_bound, pin_score_point_block, pin_score_corner_tight,
@@ -697,6 +801,8 @@ GROUPS = {
     "append": [pin_append_record_layout, pin_append_ragged_positions, pin_append_capacity_error],
     "save": [pin_save_spans_blocks, pin_save_full_block_record, pin_save_capacity_error],
     "ws": [pin_ws_fixture, pin_ws_bruteforce, pin_ws_closed_forms],
+    "meta_mean": [pin_meta_mean_exact_cases, pin_meta_mean_rounding],
+    "score_variant": [pin_score_variant_fixture, pin_score_mean_is_mean_of_dots, pin_score_aggregations_reduce_to_heads],
     "schedule": [pin_schedule_fixture, pin_schedule_invariants],
 }
 ALL_PINS = [p for ps in GROUPS.values() for p in ps]

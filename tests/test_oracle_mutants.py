@@ -79,6 +79,20 @@ MUTANTS = [
     ("schedule-strict", "schedule", "if (used + ws[i] <= m_avl) {", "if (used + ws[i] < m_avl) {"),
     ("schedule-stops-at-first-reject", "schedule", "            admit[i] = 0;\n",
      "            admit[i] = 0;\n            m_avl = -1;\n"),
+    ("mean-divides-by-blk-minus-1", "meta_mean", "m[c] = f32_to_bf16_rne(s / (float)blk);",
+     "m[c] = f32_to_bf16_rne(s / (float)(blk > 1 ? blk - 1 : 1));"),
+    ("mean-skips-first-token", "meta_mean", "for (int t = 0; t < blk; ++t)\n                        s = s +",
+     "for (int t = 1; t < blk; ++t)\n                        s = s +"),
+    ("mean-truncates", "meta_mean", "    u += 0x7FFFu + lsb;\n", "    u += 0u * lsb;\n"),
+    ("mean-reads-v", "meta_mean", "s = s + (float)bf(rec[t * d + c]);", "s = s + (float)bf(rec[blk * d + c * blk + t]);"),
+    ("variant-mean-reads-hi", "score_variant", "s += bf(qh[c]) * bf(mj[c]);", "s += bf(qh[c]) * bf(mj[d + c]);"),
+    ("variant-sum-is-max", "score_variant", "= agg == 0 ? best : total;", "= best;"),
+    ("variant-sum-drops-last-head", "score_variant", "                    total += s;\n",
+     "                    if (i < G - 1) total += s;\n"),
+    ("variant-cuboid-min-corner", "score_variant", "s += at_lo > at_hi ? at_lo : at_hi;",
+     "s += at_lo < at_hi ? at_lo : at_hi;"),
+    ("variant-ragged-ignored", "score_variant", "if (j >= n) {", "if (j >= nblk_max) {"),
+    ("variant-mean-row-stride", "score_variant", "int row = kind == 0 ? 2 * d : d;", "int row = 2 * d;"),
     ("save-ignores-offsets", "save", "(char *)pool + pool_off[u] + (int64_t)j",
      "(char *)pool + (int64_t)u * pool_blocks[b] * (int64_t)record_bytes + (int64_t)j"),
 ]
