@@ -66,7 +66,7 @@ typedef int ss_status;
 #define SS_ERR_OOM 4         /* host allocation failed, or a caller buffer is too small */
 #define SS_ERR_HIP 5         /* a HIP runtime call or kernel launch failed */
 
-#define SS_ABI_VERSION 1
+#define SS_ABI_VERSION 2
 
 int ss_abi_version(void);
 const char *ss_status_string(ss_status status);
@@ -111,6 +111,20 @@ ss_status ss_time_next_kernel(void *start_event, void *stop_event);
 ss_status ss_build_metadata(const void *kv_base, const int64_t *unit_off, const int32_t *nblk,
                             int B, int Hkv, int nblk_max, int blk, int d, void *meta, void *stream);
 
+/* Metadata kinds and GQA aggregations of the scoring variants. */
+#define SS_META_CUBOID 0 /* [lo, hi] per block, 2*d bf16 (ss_build_metadata) */
+#define SS_META_MEAN 1   /* mean key per block, d bf16 (ss_build_metadata_mean) */
+#define SS_AGG_MAX 0     /* a KV head's score: the largest of its query heads' scores */
+#define SS_AGG_SUM 1     /* ... their sum (ranks as their mean does) */
+
+/* Mean-key metadata, the variant the paper cites first in Section 2.2: per
+ * block and channel, the mean of K over the blk tokens, summed in fp32 in
+ * token order, scaled by 1/blk and rounded to bf16 (nearest, ties to even).
+ * Arguments as ss_build_metadata, except meta: device bf16
+ * [B][Hkv][nblk_max][d] (4-byte aligned). */
+ss_status ss_build_metadata_mean(const void *kv_base, const int64_t *unit_off, const int32_t *nblk, int B, int Hkv,
+                                 int nblk_max, int blk, int d, void *meta, void *stream);
+
 /* ------------------------------------------------------ scoring, selection
  * Criticality of block j for KV head g of sequence b (Section 2.2, the dot
  * product of the query with the block metadata, taken as the largest value
@@ -124,6 +138,17 @@ ss_status ss_build_metadata(const void *kv_base, const int64_t *unit_off, const 
  *       written. */
 ss_status ss_score_blocks(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv,
                           int nblk_max, int d, float *scores, void *stream);
+
+/* Scoring variants (Section 2.2: the DSAs the paper cites differ in their
+ * metadata; the dot product with the query is common to them):
+ *   meta_kind SS_META_CUBOID: s_h(j) = sum_c max(q_h[c]*lo[c], q_h[c]*hi[c])
+ *   meta_kind SS_META_MEAN:   s_h(j) = sum_c q_h[c] * m[c]  (mean key m)
+ *   agg SS_AGG_MAX: S = max over the group's heads; SS_AGG_SUM: their sum.
+ * meta in the layout of its kind; other arguments as ss_score_blocks, which
+ * is the (SS_META_CUBOID, SS_AGG_MAX) case.  SS_ERR_INVALID_ARG for an
+ * unknown kind or aggregation. */
+ss_status ss_score_blocks_variant(const void *q, const void *meta, int meta_kind, int agg, const int32_t *nblk,
+                                  int B, int Hq, int Hkv, int nblk_max, int d, float *scores, void *stream);
 
 /* Top-k block selection per unit (Section 2.2: the k most critical blocks,
  * chosen per head).  Order: higher score first, equal scores -> lower block
@@ -240,15 +265,19 @@ ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t 
  *   nblk_dev: device int32 [B] full blocks; set to j + 1 when block j fills
  *   open_blocks: device [B][Hkv] block records (2*blk*d bf16 each: K tile
  *       row-major, V tile channel-major); row / column p is written
- *   meta: device bf16 [B][Hkv][nblk_max][2][d]; on a fill, block j's lo/hi
- *       (channel-wise min/max of the record's K rows, IEEE totalOrder)
+ *   meta, meta_kind: on a fill, block j's metadata of that kind:
+ *       SS_META_CUBOID, meta bf16 [B][Hkv][nblk_max][2][d]: lo/hi
+ *       (channel-wise min/max of the record's K rows, IEEE totalOrder);
+ *       SS_META_MEAN, meta bf16 [B][Hkv][nblk_max][d]: the mean key, as
+ *       ss_build_metadata_mean computes it
  *   overflow: device int32 or NULL; set to 1 if a block fills at
  *       j >= nblk_max (its metadata is then not written and nblk_dev not
  *       advanced; the token is still written and len_dev advanced)
  * Buffers 4-byte aligned.  d must be 128, blk 8, 16 or 32.  One kernel on
  * `stream`, one workgroup per sequence. */
 ss_status ss_append_kv(const void *new_kv, int32_t *len_dev, int32_t *nblk_dev, int B, int Hkv, int blk, int d,
-                       int nblk_max, void *open_blocks, void *meta, int32_t *overflow, void *stream);
+                       int nblk_max, void *open_blocks, void *meta, int meta_kind, int32_t *overflow,
+                       void *stream);
 
 /* ------------------------------------------------------ FlashD2H saving
  * CPU-assisted saving of new tokens to the DRAM pool (Section 3.2.2): the
@@ -366,7 +395,7 @@ ss_status ss_schedule_batch(const int64_t *ws_bytes, int n, int64_t m_avl, int32
 typedef struct ss_layer_buffers {
     int B, Hq, Hkv, d, blk, nblk_max, k;
     float scale;
-    const void *meta;           /* device bf16 [B][Hkv][nblk_max][2][d] */
+    const void *meta;           /* device bf16 metadata in meta_kind's layout */
     const int32_t *nblk_dev;    /* device int32 [B] */
     const void *pool;           /* device address of the DRAM pool */
     const int64_t *pool_off_dev; /* device int64 [B*Hkv] */
@@ -383,6 +412,8 @@ typedef struct ss_layer_buffers {
     size_t attn_ws_bytes;
     int parts;
     const int32_t *part_end;    /* host int32 [parts] or NULL */
+    int meta_kind;              /* SS_META_CUBOID or SS_META_MEAN (layout of meta) */
+    int agg;                    /* SS_AGG_MAX or SS_AGG_SUM */
 } ss_layer_buffers;
 
 ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, const void *q, float *out, void *stream,

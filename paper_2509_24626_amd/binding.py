@@ -41,7 +41,7 @@ class ss_layer_buffers(ctypes.Structure):
                 ("capacity_dev", _vp), ("slot_limit", _i32), ("scores", _vp), ("sel_dev", _vp),
                 ("slots_dev", _vp), ("miss_dev", _vp), ("sel_host", _vp), ("slots_host", _vp),
                 ("miss_host", _vp), ("miss_cap", _i64), ("attn_ws", _vp), ("attn_ws_bytes", _sz), ("parts", _i32),
-                ("part_end", _vp)]
+                ("part_end", _vp), ("meta_kind", _i32), ("agg", _i32)]
 
 _SIGNATURES = {
     "ss_abi_version": (_i32, []),
@@ -68,7 +68,9 @@ _SIGNATURES = {
                                    _sz, _vp]),
     "ss_decode_layer": (_i32, [ctypes.POINTER(ss_layer_buffers), _i64, _vp, _vp, _vp, _vp, _vp]),
     "ss_cache_set_blocks": (_i32, [_vp, _vp]),
-    "ss_append_kv": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp]),
+    "ss_append_kv": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp]),
+    "ss_build_metadata_mean": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),
+    "ss_score_blocks_variant": (_i32, [_vp, _vp, _i32, _i32, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),
     "ss_kv_saver_create": (_i32, [_i32, _i32, _i32, _i32, _vp, _vp, _vp, _i32, _i32, _i32, _vp]),
     "ss_kv_saver_destroy": (None, [_vp]),
     "ss_kv_save": (_i32, [_vp, _vp, _i32, _vp, _vp]),
@@ -253,9 +255,24 @@ def ss_cache_set_blocks(handle, nblk):
     _check(lib().ss_cache_set_blocks(handle, nblk.ctypes.data))
 
 
-def ss_append_kv(new_kv, len_dev, nblk_dev, B, Hkv, blk, d, nblk_max, open_blocks, meta, overflow=None, stream=None):
+def ss_append_kv(new_kv, len_dev, nblk_dev, B, Hkv, blk, d, nblk_max, open_blocks, meta, overflow=None, stream=None,
+                 meta_kind=0):
     _check(lib().ss_append_kv(_ptr(new_kv), _ptr(len_dev), _ptr(nblk_dev), B, Hkv, blk, d, nblk_max,
-                              _ptr(open_blocks), _ptr(meta), _ptr(overflow), _stream(stream)))
+                              _ptr(open_blocks), _ptr(meta), meta_kind, _ptr(overflow), _stream(stream)))
+
+
+SS_META_CUBOID, SS_META_MEAN = 0, 1
+SS_AGG_MAX, SS_AGG_SUM = 0, 1
+
+
+def ss_build_metadata_mean(kv_base, unit_off, nblk, B, Hkv, nblk_max, blk, d, meta, stream=None):
+    _check(lib().ss_build_metadata_mean(_ptr(kv_base), _ptr(unit_off), _ptr(nblk), B, Hkv, nblk_max, blk, d,
+                                        _ptr(meta), _stream(stream)))
+
+
+def ss_score_blocks_variant(q, meta, meta_kind, agg, nblk, B, Hq, Hkv, nblk_max, d, scores, stream=None):
+    _check(lib().ss_score_blocks_variant(_ptr(q), _ptr(meta), meta_kind, agg, _ptr(nblk), B, Hq, Hkv, nblk_max, d,
+                                         _ptr(scores), _stream(stream)))
 
 
 def ss_kv_saver_create(B, Hkv, blk, d, pool_host, pool_off, pool_blocks, max_new_tokens=1, staging_slots=4,

@@ -7,7 +7,8 @@
 // and its V values in column p of the channel-major V tile.  When p is the
 // block's last row, the wave takes the channel-wise min/max of the tile's K
 // rows (rows written by earlier launches, plus the new row from registers)
-// and writes the block's metadata row.  After all heads, one thread
+// and writes the block's metadata row; for mean-key metadata it sums the
+// rows in fp32 in token order instead.  After all heads, one thread
 // advances the sequence's token count and, on a fill, its block count; only
 // this workgroup touches them, so there is no race.  The work is a few
 // hundred bytes per head: the kernel is latency-bound by design and runs on
@@ -23,7 +24,7 @@ constexpr int WAVES = 4;
 __device__ __forceinline__ uint32_t key16(uint32_t h) { return (h & 0x8000u) ? (~h & 0xFFFFu) : (h | 0x8000u); }
 __device__ __forceinline__ uint32_t unkey16(uint32_t k) { return (k & 0x8000u) ? (k & 0x7FFFu) : (~k & 0xFFFFu); }
 
-template <int BLK>
+template <int BLK, int KIND>
 __global__ __launch_bounds__(WAVES * 64) void append_kernel(const uint32_t *__restrict__ new_kv, int32_t *len,
                                                             int32_t *nblk, int Hkv, int nblk_max,
                                                             uint8_t *__restrict__ open, uint8_t *__restrict__ meta,
@@ -48,7 +49,21 @@ __global__ __launch_bounds__(WAVES * 64) void append_kernel(const uint32_t *__re
         uint16_t *vt = reinterpret_cast<uint16_t *>(rec + (size_t)BLK * D * 2);
         vt[(2 * lane) * BLK + p] = (uint16_t)(v2 & 0xFFFFu);
         vt[(2 * lane + 1) * BLK + p] = (uint16_t)(v2 >> 16);
-        if (record_meta) {
+        if (record_meta && KIND == SS_META_MEAN) {
+            // the block's keys summed in fp32 in token order (the new token is the last row)
+            const uint32_t *rows = reinterpret_cast<const uint32_t *>(rec);
+            float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll 4
+            for (int t = 0; t < BLK - 1; ++t) {
+                const uint32_t w = rows[t * (D / 2) + lane];
+                s0 = s0 + __uint_as_float(w << 16);
+                s1 = s1 + __uint_as_float(w & 0xFFFF0000u);
+            }
+            s0 = s0 + __uint_as_float(k2 << 16);
+            s1 = s1 + __uint_as_float(k2 & 0xFFFF0000u);
+            uint32_t *m = reinterpret_cast<uint32_t *>(meta + (u * nblk_max + j) * (size_t)(D * 2));
+            m[lane] = ss::pack_bf16_rne(s0 * (1.0f / BLK), s1 * (1.0f / BLK));
+        } else if (record_meta) {
             uint32_t lo0 = key16(k2 & 0xFFFFu), lo1 = key16(k2 >> 16);
             uint32_t hi0 = lo0, hi1 = lo1;
             const uint32_t *rows = reinterpret_cast<const uint32_t *>(rec);
@@ -74,11 +89,25 @@ __global__ __launch_bounds__(WAVES * 64) void append_kernel(const uint32_t *__re
     }
 }
 
+template <int KIND>
+void launch_append(int blk, dim3 grid, dim3 block, hipStream_t s, const uint32_t *kv, int32_t *len, int32_t *nblk,
+                   int Hkv, int nblk_max, uint8_t *o, uint8_t *m, int32_t *overflow)
+{
+    switch (blk) {
+    case 8: ss::launch(append_kernel<8, KIND>, grid, block, s, kv, len, nblk, Hkv, nblk_max, o, m, overflow); break;
+    case 16: ss::launch(append_kernel<16, KIND>, grid, block, s, kv, len, nblk, Hkv, nblk_max, o, m, overflow); break;
+    default: ss::launch(append_kernel<32, KIND>, grid, block, s, kv, len, nblk, Hkv, nblk_max, o, m, overflow); break;
+    }
+}
+
 }  // namespace
 
 extern "C" ss_status ss_append_kv(const void *new_kv, int32_t *len_dev, int32_t *nblk_dev, int B, int Hkv, int blk,
-                                  int d, int nblk_max, void *open_blocks, void *meta, int32_t *overflow, void *stream)
+                                  int d, int nblk_max, void *open_blocks, void *meta, int meta_kind, int32_t *overflow,
+                                  void *stream)
 {
+    SS_CHECK_ARG(meta_kind == SS_META_CUBOID || meta_kind == SS_META_MEAN, "ss_append_kv: metadata kind %d",
+                 meta_kind);
     SS_CHECK_ARG(B >= 0 && Hkv > 0 && nblk_max >= 0, "ss_append_kv: bad shape B=%d Hkv=%d nblk_max=%d", B, Hkv,
                  nblk_max);
     SS_CHECK_SUPPORTED(d == ss::kHeadDim, "ss_append_kv: d=%d (only 128)", d);
@@ -92,10 +121,9 @@ extern "C" ss_status ss_append_kv(const void *new_kv, int32_t *len_dev, int32_t 
     auto *o = static_cast<uint8_t *>(open_blocks);
     auto *m = static_cast<uint8_t *>(meta);
     const dim3 grid(B), block(WAVES * 64);
-    switch (blk) {
-    case 8: ss::launch(append_kernel<8>, grid, block, s, kv, len_dev, nblk_dev, Hkv, nblk_max, o, m, overflow); break;
-    case 16: ss::launch(append_kernel<16>, grid, block, s, kv, len_dev, nblk_dev, Hkv, nblk_max, o, m, overflow); break;
-    default: ss::launch(append_kernel<32>, grid, block, s, kv, len_dev, nblk_dev, Hkv, nblk_max, o, m, overflow); break;
-    }
+    if (meta_kind == SS_META_MEAN)
+        launch_append<SS_META_MEAN>(blk, grid, block, s, kv, len_dev, nblk_dev, Hkv, nblk_max, o, m, overflow);
+    else
+        launch_append<SS_META_CUBOID>(blk, grid, block, s, kv, len_dev, nblk_dev, Hkv, nblk_max, o, m, overflow);
     return ss::check_launch("ss_append_kv");
 }

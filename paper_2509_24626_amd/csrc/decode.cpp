@@ -155,6 +155,9 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
     const size_t rec = (size_t)2 * L->blk * d * 2;
     const char *q8 = static_cast<const char *>(q);
     const char *meta8 = static_cast<const char *>(L->meta);
+    SS_CHECK_ARG(L->meta_kind == SS_META_CUBOID || L->meta_kind == SS_META_MEAN, "ss_decode_layer: metadata kind %d",
+                 L->meta_kind);
+    const size_t meta_row = (size_t)(L->meta_kind == SS_META_MEAN ? 1 : 2) * d * 2;  // bytes per block
     const int32_t *pe = L->part_end;
     auto b_of = [&](int p) { return p == 0 ? 0 : (pe ? pe[p - 1] : (int)((int64_t)B * p / P)); };
 
@@ -174,9 +177,9 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
     for (int p = 0; p < P; ++p) {
         const int b0 = b_of(p), Bp = b_of(p + 1) - b0;
         if ((st = record(events, 7 * p + 0, s))) return st;
-        st = ss_score_blocks(q8 + (size_t)b0 * Hq * d * 2, meta8 + (size_t)b0 * Hkv * L->nblk_max * 2 * d * 2,
-                             L->nblk_dev + b0, Bp, Hq, Hkv, L->nblk_max, d, L->scores + (size_t)b0 * Hkv * L->nblk_max,
-                             stream);
+        st = ss_score_blocks_variant(q8 + (size_t)b0 * Hq * d * 2, meta8 + (size_t)b0 * Hkv * L->nblk_max * meta_row,
+                                     L->meta_kind, L->agg, L->nblk_dev + b0, Bp, Hq, Hkv, L->nblk_max, d,
+                                     L->scores + (size_t)b0 * Hkv * L->nblk_max, stream);
         if (st) return st;
         if ((st = record(events, 7 * p + 1, s))) return st;
         st = ss::launch_topk(L->scores + (size_t)b0 * Hkv * L->nblk_max, L->nblk_dev + b0, Bp, Hkv, L->nblk_max, k,

@@ -29,6 +29,12 @@ constexpr int kMaxBlocks = 65536;
 
 inline hipStream_t as_stream(void *s) { return reinterpret_cast<hipStream_t>(s); }
 
+// block scoring (score.hip): argument checks and the launch
+ss_status check_score_args(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv,
+                           int nblk_max, int d, const void *scores, const char *who, int meta_kind, int agg);
+ss_status launch_score(const void *q, const void *meta, int meta_kind, int agg, const int32_t *nblk, int B, int Hq,
+                       int Hkv, int nblk_max, float *scores, hipStream_t s);
+
 // f(begin, end) over [0, n) on the library's host worker threads
 void parallel_for(int64_t n, int max_threads, const std::function<void(int64_t, int64_t)> &f);
 
@@ -54,6 +60,18 @@ inline void launch(void (*k)(P...), dim3 grid, dim3 block, hipStream_t s, A... a
         k<<<grid, block, 0, s>>>(static_cast<P>(args)...);
 }
 
+}  // namespace ss
+
+namespace ss {
+// two fp32 values rounded to bf16 (nearest, ties to even; inputs finite),
+// packed low then high
+__device__ __forceinline__ uint32_t pack_bf16_rne(float a, float b)
+{
+    uint32_t x = __float_as_uint(a), y = __float_as_uint(b);
+    x += 0x7FFFu + ((x >> 16) & 1u);
+    y += 0x7FFFu + ((y >> 16) & 1u);
+    return (x >> 16) | (y & 0xFFFF0000u);
+}
 }  // namespace ss
 
 // 8 x bf16 operand fragment of v_mfma_f32_16x16x32_bf16 and its fp32 accumulator.

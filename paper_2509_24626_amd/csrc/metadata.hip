@@ -1,5 +1,6 @@
-// Block metadata: the bounding cuboid (channel-wise min and max) of the keys
-// of each KV block (Section 2.2; built when a block fills, Section 3.1).
+// Block metadata (Section 2.2; built when a block fills, Section 3.1): the
+// bounding cuboid (channel-wise min and max) of the keys of each KV block,
+// or, as the mean-key variant, the mean of the block's keys.
 //
 // One wave per block record.  A K tile is blk rows of 128 bf16 channels
 // (256 B per row); each lane loads 16 B (8 channels) of one row per step, so
@@ -92,7 +93,66 @@ __global__ __launch_bounds__(256) void meta_kernel(const uint8_t *__restrict__ k
     }
 }
 
+// Mean key of each block: one wave per block record, each lane two
+// channels; rows are summed in fp32 in token order (each wave-wide load is
+// one contiguous 256-byte row), scaled by 1/blk (exact) and rounded to bf16,
+// ties to even.
+template <int BLK>
+__global__ __launch_bounds__(256) void meta_mean_kernel(const uint8_t *__restrict__ kv_base,
+                                                        const int64_t *__restrict__ unit_off,
+                                                        const int32_t *__restrict__ nblk, int Hkv, int nblk_max,
+                                                        int64_t total_blocks, uint32_t *__restrict__ meta)
+{
+    constexpr int D = ss::kHeadDim;
+    constexpr int64_t REC = 2LL * BLK * D * 2;
+    const int lane = threadIdx.x & 63;
+    const int64_t id = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (id >= total_blocks) return;
+    const int64_t u = id / nblk_max;
+    const int j = (int)(id - u * nblk_max);
+    int n = nblk[u / Hkv];
+    n = n < 0 ? 0 : (n > nblk_max ? nblk_max : n);
+    if (j >= n) return;
+    const uint32_t *rows = reinterpret_cast<const uint32_t *>(kv_base + unit_off[u] + (int64_t)j * REC);
+    uint32_t w[BLK];
+#pragma unroll
+    for (int t = 0; t < BLK; ++t) w[t] = rows[t * (D / 2) + lane];
+    float s0 = 0.0f, s1 = 0.0f;
+#pragma unroll
+    for (int t = 0; t < BLK; ++t) {
+        s0 = s0 + __uint_as_float(w[t] << 16);
+        s1 = s1 + __uint_as_float(w[t] & 0xFFFF0000u);
+    }
+    meta[(u * nblk_max + j) * (D / 2) + lane] = ss::pack_bf16_rne(s0 * (1.0f / BLK), s1 * (1.0f / BLK));
+}
+
 }  // namespace
+
+extern "C" ss_status ss_build_metadata_mean(const void *kv_base, const int64_t *unit_off, const int32_t *nblk,
+                                            int B, int Hkv, int nblk_max, int blk, int d, void *meta, void *stream)
+{
+    SS_CHECK_ARG(B >= 0 && Hkv > 0 && nblk_max >= 0, "ss_build_metadata_mean: bad shape B=%d Hkv=%d nblk_max=%d",
+                 B, Hkv, nblk_max);
+    SS_CHECK_SUPPORTED(d == ss::kHeadDim, "ss_build_metadata_mean: d=%d (only 128)", d);
+    SS_CHECK_SUPPORTED(ss::supported_blk(blk), "ss_build_metadata_mean: blk=%d (8, 16 or 32)", blk);
+    SS_CHECK_SUPPORTED(nblk_max <= ss::kMaxBlocks, "ss_build_metadata_mean: nblk_max=%d > %d", nblk_max,
+                       ss::kMaxBlocks);
+    const int64_t total = (int64_t)B * Hkv * nblk_max;
+    if (total == 0) return SS_OK;
+    SS_CHECK_ARG(kv_base && unit_off && nblk && meta, "ss_build_metadata_mean: null pointer");
+    SS_CHECK_ARG(((uintptr_t)meta & 3) == 0, "ss_build_metadata_mean: meta must be 4-byte aligned");
+    const int64_t grid = (total + 3) / 4;
+    SS_CHECK_SUPPORTED(grid <= 0x7FFFFFFF, "ss_build_metadata_mean: too many blocks");
+    hipStream_t s = ss::as_stream(stream);
+    const uint8_t *kv = static_cast<const uint8_t *>(kv_base);
+    uint32_t *m = static_cast<uint32_t *>(meta);
+    switch (blk) {
+    case 8: ss::launch(meta_mean_kernel<8>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
+    case 16: ss::launch(meta_mean_kernel<16>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
+    default: ss::launch(meta_mean_kernel<32>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
+    }
+    return ss::check_launch("ss_build_metadata_mean");
+}
 
 extern "C" ss_status ss_build_metadata(const void *kv_base, const int64_t *unit_off, const int32_t *nblk, int B,
                                        int Hkv, int nblk_max, int blk, int d, void *meta, void *stream)

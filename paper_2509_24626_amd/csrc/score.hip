@@ -20,7 +20,6 @@
 namespace {
 
 constexpr int D = ss::kHeadDim;
-constexpr int ROW_BYTES = 2 * D * 2;  // lo + hi, bf16
 constexpr int TILE = 16;              // blocks per MFMA tile
 constexpr int WAVES = 4;
 constexpr int TILES_PER_WAVE = 4;
@@ -32,17 +31,24 @@ union frag_t {
     uint16_t h[8];
 };
 
-// Lane (L = lane/16, col = lane%16) takes 16-byte chunks c = L*8 + m of a
-// metadata row for the 8 MFMAs m of a tile (chunks 0..15 are lo, 16..31
-// hi): each lane streams 128 contiguous bytes of its row.  (A mapping where
-// each load instruction covers a contiguous 64-byte piece of every row
-// instead measured 6% slower on MI355X.)  The A fragments hold the matching
-// weights of head `col`.
+// Lane (L = lane/16, col = lane%16) takes 16-byte chunks c = L*NCH + m of a
+// metadata row for the NCH MFMAs m of a tile: each lane streams NCH*16
+// contiguous bytes of its row.  (A mapping where each load instruction
+// covers a contiguous 64-byte piece of every row instead measured 6% slower
+// on MI355X.)  The A fragments hold the matching weights of head `col`.
+//
+// KIND 0, cuboid rows [lo, hi] (512 B, NCH = 8): chunks 0..15 are lo and
+// multiply min(q, 0), chunks 16..31 are hi and multiply max(q, 0).
+// KIND 1, mean-key rows (256 B, NCH = 4): each chunk multiplies q itself.
+// AGG 0 takes the maximum over the group's heads, AGG 1 their sum.
+template <int KIND, int AGG>
 __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__ q,
                                                     const uint8_t *__restrict__ meta,
                                                     const int32_t *__restrict__ nblk, int Hq, int Hkv, int G,
                                                     int nblk_max, int chunks_per_unit, float *__restrict__ scores)
 {
+    constexpr int NCH = KIND == 0 ? 8 : 4;
+    constexpr int ROW = NCH * 4 * 16;  // 512 or 256 bytes
     const int u = blockIdx.x / chunks_per_unit;
     const int chunk = blockIdx.x - u * chunks_per_unit;
     const int b = u / Hkv, g = u - b * Hkv;
@@ -56,38 +62,40 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__
     const int L = lane >> 4;
     const int col = lane & 15;
 
-    // weights of head g*G + col for chunks L*8 .. L*8+7
-    frag_t w[8];
+    // weights of head g*G + col for chunks L*NCH .. L*NCH+NCH-1
+    frag_t w[NCH];
     {
         const bool live = col < G;
         const uint16_t *qh = q + ((int64_t)b * Hq + g * G + (live ? col : 0)) * D;
 #pragma unroll
-        for (int m = 0; m < 8; ++m) {
-            const bool hi_half = L >= 2;            // chunks 16..31 multiply hi
-            const int c = ((L * 8 + m) & 15) * 8;  // channel of the chunk
+        for (int m = 0; m < NCH; ++m) {
+            const int c = L * NCH + m;
             frag_t x;
-            x.u = *reinterpret_cast<const uint4 *>(qh + c);
+            x.u = *reinterpret_cast<const uint4 *>(qh + (c & 15) * 8);
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const bool neg = (x.h[e] & 0x8000u) != 0;
-                // hi half keeps the non-negative part, lo half the negative part
-                w[m].h[e] = (live && (neg != hi_half)) ? x.h[e] : (uint16_t)0;
+                bool keep = live;
+                if (KIND == 0) {
+                    const bool neg = (x.h[e] & 0x8000u) != 0;
+                    keep = keep && (neg != (c >= 16));  // hi half keeps q >= 0, lo half q < 0
+                }
+                w[m].h[e] = keep ? x.h[e] : (uint16_t)0;
             }
         }
     }
 
-    const uint8_t *mu = meta + (int64_t)u * nblk_max * ROW_BYTES;
+    const uint8_t *mu = meta + (int64_t)u * nblk_max * ROW;
     float *su = scores + (int64_t)u * nblk_max;
-    const int lane_off = L * 128;  // byte offset of chunk L*8
+    const int lane_off = L * NCH * 16;
 
     // interleave waves over tiles so the WG walks memory front to back
-    frag_t cur[8], nxt[8];
+    frag_t cur[NCH], nxt[NCH];
     auto load_tile = [&](int t, frag_t *f) {
         int j = j0 + (t * WAVES + wave) * TILE + col;
         j = j < n ? j : n - 1;  // rows past the end are loaded in range and not stored
-        const uint8_t *row = mu + (int64_t)j * ROW_BYTES + lane_off;
+        const uint8_t *row = mu + (int64_t)j * ROW + lane_off;
 #pragma unroll
-        for (int m = 0; m < 8; ++m) f[m].u = *reinterpret_cast<const uint4 *>(row + m * 16);
+        for (int m = 0; m < NCH; ++m) f[m].u = *reinterpret_cast<const uint4 *>(row + m * 16);
     };
 
     int ntiles = 0;
@@ -100,19 +108,26 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__
         if (t + 1 < ntiles) load_tile(t + 1, nxt);
         f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int m = 0; m < 8; ++m) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[m].v, cur[m].v, acc, 0, 0, 0);
+        for (int m = 0; m < NCH; ++m) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[m].v, cur[m].v, acc, 0, 0, 0);
         // lane holds heads L*4 .. L*4+3 of block column `col`
-        float s = -INFINITY;
+        float s;
+        if (AGG == 0) {
+            s = -INFINITY;
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            if (L * 4 + i < G) s = fmaxf(s, acc[i]);
-        s = fmaxf(s, __shfl_xor(s, 16));
-        s = fmaxf(s, __shfl_xor(s, 32));
+            for (int i = 0; i < 4; ++i)
+                if (L * 4 + i < G) s = fmaxf(s, acc[i]);
+            s = fmaxf(s, __shfl_xor(s, 16));
+            s = fmaxf(s, __shfl_xor(s, 32));
+        } else {
+            s = (acc[0] + acc[1]) + (acc[2] + acc[3]);  // padded heads hold exact zeros
+            s += __shfl_xor(s, 16);
+            s += __shfl_xor(s, 32);
+        }
         const int j = j0 + (t * WAVES + wave) * TILE + col;
         if (L == 0 && j < n) su[j] = s;
         if (t + 1 < ntiles) {
 #pragma unroll
-            for (int m = 0; m < 8; ++m) cur[m] = nxt[m];
+            for (int m = 0; m < NCH; ++m) cur[m] = nxt[m];
         }
     }
 }
@@ -121,21 +136,33 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__
 
 namespace ss {
 
-ss_status launch_score(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv, int nblk_max,
-                       float *scores, hipStream_t s)
+ss_status launch_score(const void *q, const void *meta, int meta_kind, int agg, const int32_t *nblk, int B, int Hq,
+                       int Hkv, int nblk_max, float *scores, hipStream_t s)
 {
     const int chunks = (nblk_max + BLOCKS_PER_WG - 1) / BLOCKS_PER_WG;
     const int64_t grid = (int64_t)B * Hkv * chunks;
     if (grid == 0) return SS_OK;
     SS_CHECK_SUPPORTED(grid <= 0x7FFFFFFF, "score: grid too large");
-    ss::launch(score_kernel, dim3((unsigned)grid), dim3(256), s, static_cast<const uint16_t *>(q),
-               static_cast<const uint8_t *>(meta), nblk, Hq, Hkv, Hq / Hkv, nblk_max, chunks, scores);
+    const auto *qq = static_cast<const uint16_t *>(q);
+    const auto *mm = static_cast<const uint8_t *>(meta);
+    const dim3 gr((unsigned)grid), bl(256);
+    const int G = Hq / Hkv;
+    if (meta_kind == SS_META_CUBOID && agg == SS_AGG_MAX)
+        ss::launch(score_kernel<0, 0>, gr, bl, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
+    else if (meta_kind == SS_META_CUBOID)
+        ss::launch(score_kernel<0, 1>, gr, bl, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
+    else if (agg == SS_AGG_MAX)
+        ss::launch(score_kernel<1, 0>, gr, bl, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
+    else
+        ss::launch(score_kernel<1, 1>, gr, bl, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
     return check_launch("ss_score_blocks");
 }
 
 ss_status check_score_args(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv,
-                           int nblk_max, int d, const void *scores, const char *who)
+                           int nblk_max, int d, const void *scores, const char *who, int meta_kind, int agg)
 {
+    SS_CHECK_ARG(meta_kind == SS_META_CUBOID || meta_kind == SS_META_MEAN, "%s: metadata kind %d", who, meta_kind);
+    SS_CHECK_ARG(agg == SS_AGG_MAX || agg == SS_AGG_SUM, "%s: aggregation %d", who, agg);
     SS_CHECK_ARG(B >= 0 && Hq > 0 && Hkv > 0 && nblk_max >= 0, "%s: bad shape B=%d Hq=%d Hkv=%d nblk_max=%d", who, B,
                  Hq, Hkv, nblk_max);
     SS_CHECK_ARG(Hq % Hkv == 0, "%s: Hq=%d not a multiple of Hkv=%d", who, Hq, Hkv);
@@ -151,7 +178,16 @@ ss_status check_score_args(const void *q, const void *meta, const int32_t *nblk,
 extern "C" ss_status ss_score_blocks(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv,
                                      int nblk_max, int d, float *scores, void *stream)
 {
-    ss_status st = ss::check_score_args(q, meta, nblk, B, Hq, Hkv, nblk_max, d, scores, "ss_score_blocks");
+    return ss_score_blocks_variant(q, meta, SS_META_CUBOID, SS_AGG_MAX, nblk, B, Hq, Hkv, nblk_max, d, scores,
+                                   stream);
+}
+
+extern "C" ss_status ss_score_blocks_variant(const void *q, const void *meta, int meta_kind, int agg,
+                                             const int32_t *nblk, int B, int Hq, int Hkv, int nblk_max, int d,
+                                             float *scores, void *stream)
+{
+    ss_status st = ss::check_score_args(q, meta, nblk, B, Hq, Hkv, nblk_max, d, scores, "ss_score_blocks", meta_kind,
+                                        agg);
     if (st != SS_OK) return st;
-    return ss::launch_score(q, meta, nblk, B, Hq, Hkv, nblk_max, scores, ss::as_stream(stream));
+    return ss::launch_score(q, meta, meta_kind, agg, nblk, B, Hq, Hkv, nblk_max, scores, ss::as_stream(stream));
 }

@@ -216,11 +216,6 @@ ss_status launch_topk(const float *scores, const int32_t *nblk, int B, int Hkv, 
     return check_launch("ss_select_topk");
 }
 
-ss_status check_score_args(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv,
-                           int nblk_max, int d, const void *scores, const char *who);
-ss_status launch_score(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv, int nblk_max,
-                       float *scores, hipStream_t s);
-
 }  // namespace ss
 
 extern "C" ss_status ss_select_topk(const float *scores, const int32_t *nblk, int B, int Hkv, int nblk_max, int k,
@@ -237,13 +232,14 @@ extern "C" ss_status ss_select_topk(const float *scores, const int32_t *nblk, in
 extern "C" ss_status ss_score_topk(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv,
                                    int nblk_max, int d, int k, float *scores, int32_t *sel, void *stream)
 {
-    ss_status st = ss::check_score_args(q, meta, nblk, B, Hq, Hkv, nblk_max, d, scores, "ss_score_topk");
+    ss_status st = ss::check_score_args(q, meta, nblk, B, Hq, Hkv, nblk_max, d, scores, "ss_score_topk",
+                                        SS_META_CUBOID, SS_AGG_MAX);
     if (st != SS_OK) return st;
     SS_CHECK_ARG(k > 0, "ss_score_topk: k=%d", k);
     if (B == 0) return SS_OK;
     SS_CHECK_ARG(sel, "ss_score_topk: null sel");
     hipStream_t s = ss::as_stream(stream);
-    st = ss::launch_score(q, meta, nblk, B, Hq, Hkv, nblk_max, scores, s);
+    st = ss::launch_score(q, meta, SS_META_CUBOID, SS_AGG_MAX, nblk, B, Hq, Hkv, nblk_max, scores, s);
     if (st != SS_OK) return st;
     return ss::launch_topk(scores, nblk, B, Hkv, nblk_max, k, sel, nullptr, s);
 }

@@ -103,8 +103,9 @@ class HierLayer:
     """One layer of the hierarchical workload: its DRAM pool slice, HBM
     metadata, HBM block cache and step buffers."""
 
-    def __init__(self, cfg, nblk_host, capacity, pool, pool_off_host, meta, parts=1, reserve=0):
+    def __init__(self, cfg, nblk_host, capacity, pool, pool_off_host, meta, parts=1, reserve=0, meta_kind=0, agg=0):
         self.cfg = cfg
+        self.meta_kind, self.agg = meta_kind, agg
         # blocks each unit may gain (appended tokens) beyond its initial count:
         # the metadata, the scores and the pool have room for them
         self.reserve = reserve
@@ -159,7 +160,7 @@ class HierLayer:
             slot_limit=int(self.capacity.max()) if self.units else 0, scores=p(self.scores), sel_dev=p(self.sel),
             slots_dev=p(self.slots), miss_dev=p(self.miss), sel_host=p(self.sel_h), slots_host=p(self.slots_h),
             miss_host=p(self.miss_h), miss_cap=self.miss_cap, attn_ws=p(self.ws), attn_ws_bytes=self.ws_bytes,
-            parts=self.parts, part_end=self.part_end.ctypes.data)
+            parts=self.parts, part_end=self.part_end.ctypes.data, meta_kind=meta_kind, agg=agg)
         self.last_n_miss = 0
         self.saver = None
 
@@ -205,7 +206,7 @@ class HierLayer:
         ss.ss_kv_save(self.saver, new_kv, 1, self.len_host, self.save_stream)
         self.step(t, q, events)
         ss.ss_append_kv(new_kv, self.len_dev, self.nblk, cfg.B, cfg.Hkv, cfg.blk, D, self.nblk_max, self.open,
-                        self.meta, self.overflow)
+                        self.meta, self.overflow, meta_kind=self.meta_kind)
         self.len_host = self.len_host + 1
         return self.out
 
@@ -247,7 +248,8 @@ def tent_parts(B, n):
     return [int(x) for x in sizes]
 
 
-def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None, parts=1, reserve=0):
+def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None, parts=1, reserve=0, meta_kind=0,
+                     agg=0):
     """Draws one layer's KV per sequence on the GPU, builds its metadata in
     HBM and copies the records into `pool` at pool_base_off.  Returns the
     HierLayer (its pool offsets are relative to the pool base).  With
@@ -257,7 +259,9 @@ def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None,
     sK, sV = gen.channel_scales(cfg.Hkv, D, seed, layer, "cuda")
     off, total = pool_layout(cfg, nblk, reserve)
     off = off + pool_base_off
-    meta = torch.empty(cfg.B, cfg.Hkv, cfg.nblk_max + reserve, 2, D, dtype=torch.int16, device="cuda")
+    rows = (2,) if meta_kind == ss.SS_META_CUBOID else ()
+    meta = torch.empty(cfg.B, cfg.Hkv, cfg.nblk_max + reserve, *rows, D, dtype=torch.int16, device="cuda")
+    build = ss.ss_build_metadata if meta_kind == ss.SS_META_CUBOID else ss.ss_build_metadata_mean
     for b in range(cfg.B):
         n = int(nblk[b])
         if n == 0:
@@ -266,15 +270,14 @@ def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None,
         rec = rec.contiguous()
         # metadata of this sequence, from the HBM copy of its records
         unit_off = _dev(np.arange(cfg.Hkv, dtype=np.int64) * n * cfg.record_bytes, np.int64)
-        ss.ss_build_metadata(rec, unit_off, _dev([n], np.int32), 1, cfg.Hkv, cfg.nblk_max + reserve, cfg.blk, D,
-                             meta[b])
+        build(rec, unit_off, _dev([n], np.int32), 1, cfg.Hkv, cfg.nblk_max + reserve, cfg.blk, D, meta[b])
         for g in range(cfg.Hkv):
             start = int(off[b * cfg.Hkv + g])
             pool.t[start:start + n * cfg.record_bytes].copy_(rec[g].view(torch.uint8).reshape(-1))
         if progress and b % 16 == 15:
             progress(f"layer {layer}: {b + 1}/{cfg.B} sequences in the DRAM pool")
     torch.cuda.synchronize()
-    L = HierLayer(cfg, nblk, cache_capacity(cfg, nblk), pool, off, meta, parts, reserve)
+    L = HierLayer(cfg, nblk, cache_capacity(cfg, nblk), pool, off, meta, parts, reserve, meta_kind, agg)
     return L
 
 

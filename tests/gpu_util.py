@@ -124,3 +124,28 @@ def run_attention(ss, w, slots_dev, slot_limit=None):
     ss.ss_sparse_attention(w.q, w.kv, w.unit_off, slots_dev, w.nblk_max if slot_limit is None else slot_limit, w.B,
                            w.Hq, w.Hkv, w.d, w.blk, slots_dev.shape[-1], 1.0 / math.sqrt(w.d), out, ws, wsb)
     return out
+
+
+def check_scores_variant(gpu, ora, q_host, meta_host, nblk, G, kind, agg):
+    """Elementwise score check for the metadata kinds and aggregations: the
+    GPU sums exact bf16 products in fp32 (and, for agg 1, the G head
+    scores), so |gpu - oracle| <= (2*d + G) * 2^-24 * sum over the group's
+    heads of sum_c |q_c| * |m_c| (m = max(|lo|, |hi|) for cuboid rows)."""
+    B, Hkv, nblk_max = ora.shape
+    qf = np.abs(bits_to_f64(q_host))
+    if kind == 0:
+        mag = np.maximum(np.abs(bits_to_f64(meta_host[..., 0, :])), np.abs(bits_to_f64(meta_host[..., 1, :])))
+    else:
+        mag = np.abs(bits_to_f64(meta_host))
+    d = qf.shape[-1]
+    worst = 0.0
+    for b in range(B):
+        n = int(nblk[b])
+        for g in range(Hkv):
+            per_head = qf[b, g * G:(g + 1) * G] @ mag[b, g, :n].T  # [G][n]
+            bound = (2 * d + G) * 2.0 ** -24 * per_head.sum(axis=0)
+            err = np.abs(gpu[b, g, :n].astype(np.float64) - ora[b, g, :n])
+            assert np.all(err <= bound), (b, g, float((err - bound).max()))
+            if n:
+                worst = max(worst, float((err / np.maximum(np.abs(ora[b, g, :n]), 1e-30)).max()))
+    return worst

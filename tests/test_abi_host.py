@@ -24,7 +24,8 @@ def declared_functions():
 
 def test_library_builds_and_loads():
     assert os.path.exists(ss.LIB_PATH)
-    assert ss.ss_abi_version() == 1
+    header = open(os.path.join(ROOT, "include", "sparseserve.h")).read()
+    assert ss.ss_abi_version() == int(re.search(r"#define SS_ABI_VERSION (\d+)", header).group(1)) == 2
 
 
 def test_every_declared_symbol_is_exported():

@@ -85,6 +85,49 @@ def test_scores_and_selection(ss, oracle_impl, name):
 
 
 @pytest.mark.parametrize("name", list(CASES))
+def test_metadata_mean_bitexact(ss, oracle_impl, name):
+    """Mean-key metadata: fp32 token-order sums rounded to bf16, bit-exact."""
+    w = workload(name)
+    meta = torch.empty(w.B, w.Hkv, w.nblk_max, w.d, dtype=torch.int16, device="cuda")
+    ss.ss_build_metadata_mean(w.kv, w.unit_off, w.nblk, w.B, w.Hkv, w.nblk_max, w.blk, w.d, meta)
+    torch.cuda.synchronize()
+    om = oracle_impl.build_metadata_mean(w.kv_host, w.unit_off_host, w.nblk_host, w.B, w.Hkv, w.nblk_max, w.blk, w.d)
+    valid_rows_equal(gu.u16(meta), om, w.nblk_host)
+
+
+@pytest.mark.parametrize("kind,agg", [(0, 1), (1, 0), (1, 1)], ids=["cuboid-sum", "mean-max", "mean-sum"])
+@pytest.mark.parametrize("name", list(CASES))
+def test_score_variants_and_selection(ss, oracle_impl, name, kind, agg):
+    w = workload(name)
+    if kind == 0:
+        meta = gu.run_metadata(ss, w)
+        om = oracle_meta(oracle_impl, w)
+    else:
+        meta = torch.empty(w.B, w.Hkv, w.nblk_max, w.d, dtype=torch.int16, device="cuda")
+        ss.ss_build_metadata_mean(w.kv, w.unit_off, w.nblk, w.B, w.Hkv, w.nblk_max, w.blk, w.d, meta)
+        om = oracle_impl.build_metadata_mean(w.kv_host, w.unit_off_host, w.nblk_host, w.B, w.Hkv, w.nblk_max, w.blk,
+                                             w.d)
+    scores = torch.empty(w.B, w.Hkv, w.nblk_max, dtype=torch.float32, device="cuda")
+    sel = torch.empty(w.B, w.Hkv, w.k, dtype=torch.int32, device="cuda")
+    ss.ss_score_blocks_variant(w.q, meta, kind, agg, w.nblk, w.B, w.Hq, w.Hkv, w.nblk_max, w.d, scores)
+    ss.ss_select_topk(scores, w.nblk, w.B, w.Hkv, w.nblk_max, w.k, sel)
+    torch.cuda.synchronize()
+    S = oracle_impl.score_variant(w.q_host, om, kind, agg, w.nblk_host, w.Hq, w.Hkv, w.nblk_max, w.d)
+    osel = oracle_impl.select(S, w.nblk_host, w.k)
+    worst = gu.check_scores_variant(scores.cpu().numpy(), S, w.q_host, om, w.nblk_host, w.Hq // w.Hkv, kind, agg)
+    diff = gu.check_selection(sel.cpu().numpy(), osel, S, w.nblk_host, w.k)
+    print(f"[gpu] {name} kind={kind} agg={agg}: worst relative score error {worst:.2e}; tie-band units {len(diff)}")
+
+
+def test_score_variant_rejects_unknown_kind(ss):
+    w = workload("tiny-b2-h8kv2-ctx4k")
+    scores = torch.empty(w.B, w.Hkv, w.nblk_max, dtype=torch.float32, device="cuda")
+    for kind, agg in ((2, 0), (0, 2), (-1, 0)):
+        with pytest.raises(ss.SparseServeError):
+            ss.ss_score_blocks_variant(w.q, scores, kind, agg, w.nblk, w.B, w.Hq, w.Hkv, w.nblk_max, w.d, scores)
+
+
+@pytest.mark.parametrize("name", list(CASES))
 def test_attention_on_oracle_selection(ss, oracle_impl, name):
     w = workload(name)
     om = oracle_meta(oracle_impl, w)

@@ -59,8 +59,11 @@ class Track:
             self.nb0 = self.nb_s.copy()
         else:
             self.src, self.src_off = pool.host, L.pool_off_host[self.units]
-        self.meta = oracle_impl.build_metadata(self.src, self.src_off, self.nb_s, len(self.sb), Hkv, L.nblk_max,
-                                               cfg.blk, 128)
+        self.kind, self.agg = L.meta_kind, L.agg
+        build = oracle_impl.build_metadata if self.kind == 0 else oracle_impl.build_metadata_mean
+        self.meta = build(self.src, self.src_off, self.nb_s, len(self.sb), Hkv, L.nblk_max, cfg.blk, 128)
+        if self.kind != 0:  # the oracle's append writes cuboid rows; mean rows are made from its open records
+            self.meta_cuboid = np.zeros((len(self.sb), Hkv, L.nblk_max, 2, 128), np.uint16)
         # block counts only bound which indices are valid: give the LRU the final ones
         self.lru = oracle_impl.lru(len(self.sb), Hkv, self.nb_s + self.reserve, cap_s)
         self.img_off = np.concatenate([[0], np.cumsum(cap_s.astype(np.int64))[:-1]]) * rb
@@ -72,7 +75,17 @@ class Track:
         tokens go to the private pool copy and to the open blocks."""
         kv = gu.u16(new_kv)[self.sb]
         self.o.save(kv[:, None], self.len, self.cfg.blk, self.src, self.src_off, self.src_blocks)
-        self.o.append(kv, self.len, self.nb_s, self.cfg.blk, self.L.nblk_max, self.open, self.meta)
+        if self.kind == 0:
+            self.o.append(kv, self.len, self.nb_s, self.cfg.blk, self.L.nblk_max, self.open, self.meta)
+            return
+        before = self.nb_s.copy()
+        self.o.append(kv, self.len, self.nb_s, self.cfg.blk, self.L.nblk_max, self.open, self.meta_cuboid)
+        for i in np.nonzero(self.nb_s != before)[0]:
+            j = int(self.nb_s[i]) - 1
+            for g in range(self.cfg.Hkv):
+                m = self.o.build_metadata_mean(self.open[i, g], np.zeros(1, np.int64), np.ones(1, np.int32), 1, 1, 1,
+                                               self.cfg.blk, 128)
+                self.meta[i, g, j] = m[0, 0, 0]
 
     def check_saved(self):
         """After the run: block counts, metadata rows and DRAM records of the
@@ -99,7 +112,10 @@ class Track:
         o, cfg, L, sb = self.o, self.cfg, self.L, self.sb
         Hkv, k, G, rb = cfg.Hkv, cfg.k, cfg.G, cfg.record_bytes
         qh = gu.u16(q)[sb]
-        S = o.score(qh, self.meta, self.nb_s, cfg.Hq, Hkv, L.nblk_max, 128)
+        if self.kind == 0 and self.agg == 0:
+            S = o.score(qh, self.meta, self.nb_s, cfg.Hq, Hkv, L.nblk_max, 128)
+        else:
+            S = o.score_variant(qh, self.meta, self.kind, self.agg, self.nb_s, cfg.Hq, Hkv, L.nblk_max, 128)
         osel = o.select(S, self.nb_s, k)
         gsel = L.sel.cpu().numpy()[sb]
         for (i, g) in gu.check_selection(gsel, osel, S, self.nb_s, k):
@@ -130,7 +146,8 @@ class Track:
                 assert err <= gu.ATTN_TOL, (where, err)
 
 
-def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_diverged_frac=0.25, parts=1):
+def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_diverged_frac=0.25, parts=1, meta_kind=0,
+             agg=0):
     from paper_2509_24626_amd import harness as H
     lens = synth.gen.lengths(cfg, seed)
     nblk = (lens // cfg.blk).astype(np.int32)
@@ -140,7 +157,7 @@ def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_dive
     pool = H.HostPool(total, flags)
     try:
         L = H.build_hier_layer(cfg, seed, layer, pool, 0, nblk, progress=lambda m: print("[gpu]", m, flush=True),
-                               parts=parts)
+                               parts=parts, meta_kind=meta_kind, agg=agg)
         qs = H.query_stream(cfg, seed, layer, steps)
         tr = Track(oracle_impl, cfg, L, pool, sample_b, cfg.name)
         misses = []
@@ -160,7 +177,7 @@ def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_dive
         pool.close()
 
 
-def lockstep_with_save(oracle_impl, cfg, seed, sample_b, steps, parts=1, save_stream=False):
+def lockstep_with_save(oracle_impl, cfg, seed, sample_b, steps, parts=1, save_stream=False, meta_kind=0, agg=0):
     """Decode steps that also append and save each step's new tokens
     (ss_append_kv, FlashD2H), so blocks fill during the run and become
     selectable; the oracle follows the sampled sequences on its own copy of
@@ -174,7 +191,7 @@ def lockstep_with_save(oracle_impl, cfg, seed, sample_b, steps, parts=1, save_st
           f"sampled {sample_b}, {parts} group(s), save stream {save_stream}", flush=True)
     pool = H.HostPool(total)
     try:
-        L = H.build_hier_layer(cfg, seed, 0, pool, 0, nblk, parts=parts, reserve=reserve)
+        L = H.build_hier_layer(cfg, seed, 0, pool, 0, nblk, parts=parts, reserve=reserve, meta_kind=meta_kind, agg=agg)
         L.enable_save(threads=2, save_stream=torch.cuda.Stream() if save_stream else None)
         sK, sV = synth.gen.channel_scales(cfg.Hkv, 128, seed, 0, "cuda")
         qs = H.query_stream(cfg, seed, 0, steps)
@@ -240,6 +257,28 @@ def test_hier_small_with_append_and_save(ss, oracle_impl, save_stream):
     n = lockstep_with_save(oracle_impl, SAVE_SMALL, seed=12, sample_b=range(SAVE_SMALL.B), steps=40, parts=2,
                            save_stream=save_stream)
     assert n > 0
+
+
+@pytest.mark.parametrize("kind,agg", [(1, 0), (0, 1), (1, 1)], ids=["mean-max", "cuboid-sum", "mean-sum"])
+def test_hier_small_score_variants(ss, oracle_impl, kind, agg):
+    """Whole decode steps with the mean-key metadata and the sum over the
+    GQA group: selections, slots, misses, gathered bytes and attention."""
+    lockstep(oracle_impl, SMALL, seed=14, sample_b=range(SMALL.B), steps=6, parts=2, meta_kind=kind, agg=agg)
+
+
+def test_hier_small_mean_metadata_with_save(ss, oracle_impl):
+    """Appends build mean-key rows when blocks fill; those blocks are then
+    selected through the mean-key scores."""
+    n = lockstep_with_save(oracle_impl, SAVE_SMALL, seed=15, sample_b=range(SAVE_SMALL.B), steps=40, parts=2,
+                           meta_kind=1, agg=1)
+    assert n > 0
+
+
+def test_hier_128k_full_size_mean_sum_sampled(ss, oracle_impl):
+    """The 128k workload at full size with mean-key metadata and the sum
+    aggregation (8 steps)."""
+    cfg = synth.get(2)
+    lockstep(oracle_impl, cfg, seed=0, sample_b=[5, 40], steps=8, parts=8, meta_kind=1, agg=1)
 
 
 def test_hier_ragged_with_append_and_save(ss, oracle_impl):
