@@ -64,6 +64,7 @@ def parse():
                          "(FlashD2H); single-layer workloads")
     ap.add_argument("--save-stream", choices=["own", "main"], default="own",
                     help="with --with-save: the FlashD2H copies on a stream of their own or on the main stream")
+    ap.add_argument("--no-variants", action="store_true", help="skip the scoring-variant comparison")
     ap.add_argument("--no-save-bandwidth", action="store_true",
                     help="skip the saving-bandwidth comparison (FlashD2H, per-block copies, GPU-direct)")
     ap.add_argument("--pool-budget-gib", type=float, default=56.0,
@@ -251,6 +252,11 @@ def main():
     if new_kv is None and cfg.layers == 1:
         ws_study = working_set_study(cfg, layers[0], qstreams[0][-1][0], warmup + steps, args.seed, ss, torch)
 
+    # ------------------------------------------- scoring variants
+    variants = None
+    if new_kv is None and cfg.layers == 1 and not args.no_variants:
+        variants = score_variants_study(cfg, layers[0], qstreams[0][-1][1], pool, ss, torch)
+
     # ------------------------------------------- saving bandwidth
     save_bw = None if args.no_save_bandwidth else save_bandwidth(ss, torch, H)
 
@@ -299,6 +305,8 @@ def main():
         result["save_bandwidth"] = save_bw
     if ws_study is not None:
         result["working_set"] = ws_study
+    if variants is not None:
+        result["score_variants"] = variants
     print(json.dumps(result), flush=True)
     for L in layers:
         L.close()
@@ -431,6 +439,96 @@ def summarize_pmc(args):
     print("\n".join(lines))
     print()
     print("TRAFFIC = " + json.dumps(table, indent=1))
+
+
+def score_variants_study(cfg, L, q, pool, ss, torch, reps=5):
+    """The metadata kinds and GQA aggregations (Section 2.2).
+
+    Speed: each scoring kernel alone over this layer's whole batch and
+    query (after a cache flush; kernel-attached events).
+
+    Quality: on the Llama-3-8B-shaped all-HBM layer (32 sequences, 32k
+    context, 64 planted critical blocks per KV head; the timed workload's
+    random keys have no critical blocks to find), the top-k of each variant
+    against (a) the planted blocks and (b) the exact softmax attention mass
+    of sampled (sequence, KV head) units (all tokens, each query head,
+    averaged) that falls in the selected blocks; the exact top-k by block
+    maximum max_h max_t q_h.k_t is the reference selection."""
+    import synth
+    from synth import gen
+    import paper_2509_24626_amd.harness as Hm
+    if L.meta_kind != 0:
+        return None
+    B, Hq, Hkv, k, blk = cfg.B, cfg.Hq, cfg.Hkv, cfg.k, cfg.blk
+    nmax = L.nblk_max
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    flush.fill_(1.0)
+    mean = torch.empty(B, Hkv, nmax, D, dtype=torch.int16, device="cuda")
+    ss.ss_build_metadata_mean(pool.dev, L.pool_off, L.nblk, B, Hkv, nmax, blk, D, mean)  # from mapped DRAM
+    metas = {0: L.meta, 1: mean}
+    scores = torch.empty(B, Hkv, nmax, dtype=torch.float32, device="cuda")
+    res = {}
+    for kind, kname in ((0, "cuboid"), (1, "mean")):
+        row_bytes = (2 if kind == 0 else 1) * D * 2
+        nbytes = int(L.nblk_host.sum()) * Hkv * (row_bytes + 4) + B * Hq * D * 2
+        for agg, aname in ((0, "max"), (1, "sum")):
+            ts = []
+            for _ in range(reps):
+                flush.sum()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                e1.record()
+                ss.ss_time_next_kernel(e0, e1)
+                ss.ss_score_blocks_variant(q, metas[kind], kind, agg, L.nblk, B, Hq, Hkv, nmax, D, scores)
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            ms = float(np.median(ts))
+            res[f"{kname}-{aname}"] = {"ms": round(ms, 4), "GBps": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                                       "frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+    del mean, metas, scores, flush
+
+    qc = synth.get(1)
+    seed = 0
+    HL, _, qq = Hm.build_hbm_layer(qc, seed)
+    Bq, G = qc.B, qc.G
+    nq = qc.nblk_max
+    mean = torch.empty(Bq, qc.Hkv, nq, D, dtype=torch.int16, device="cuda")
+    ss.ss_build_metadata_mean(HL.kv, HL.unit_off, HL.nblk, Bq, qc.Hkv, nq, qc.blk, D, mean)
+    metas = {0: HL.meta, 1: mean}
+    sc = torch.empty(Bq, qc.Hkv, nq, dtype=torch.float32, device="cuda")
+    sel = torch.empty(Bq, qc.Hkv, qc.k, dtype=torch.int32, device="cuda")
+    qh = qq.float().cpu().numpy()
+    refs = []
+    for b, g in ((0, 0), (7, 3), (15, 5), (23, 1), (31, 7)):
+        K = HL.kv[b, g, :, :qc.blk * D].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+        Kf = (K.astype(np.uint32) << 16).view(np.float32).reshape(nq * qc.blk, D)
+        z = qh[b, g * G:(g + 1) * G] @ Kf.T
+        p = np.exp((z - z.max(axis=1, keepdims=True)) / math.sqrt(D))
+        mass = (p / p.sum(axis=1, keepdims=True)).reshape(G, nq, qc.blk).sum(axis=2)
+        best = z.reshape(G, nq, qc.blk).max(axis=2).max(axis=0)
+        top = set(np.argsort(-best, kind="stable")[:qc.k].tolist())
+        exact_mass = float(mass[:, sorted(top)].sum(axis=1).mean())
+        refs.append((b, g, mass, top, exact_mass))
+    planted = {(b, g): set(gen.planted_blocks(nq, qc.n_plant, seed, 0, b, g, "cuda").cpu().tolist())
+               for b in range(Bq) for g in range(qc.Hkv)}
+    for kind, kname in ((0, "cuboid"), (1, "mean")):
+        for agg, aname in ((0, "max"), (1, "sum")):
+            ss.ss_score_blocks_variant(qq, metas[kind], kind, agg, HL.nblk, Bq, qc.Hq, qc.Hkv, nq, D, sc)
+            ss.ss_select_topk(sc, HL.nblk, Bq, qc.Hkv, nq, qc.k, sel)
+            sh = sel.cpu().numpy()
+            rec_planted = float(np.mean([len(planted[(b, g)] & set(sh[b, g].tolist())) / qc.n_plant
+                                         for b in range(Bq) for g in range(qc.Hkv)]))
+            mass_rec = [float(m[:, sh[b, g][sh[b, g] >= 0]].sum(axis=1).mean()) for b, g, m, _, _ in refs]
+            top_rec = [len(t & set(sh[b, g].tolist())) / len(t) for b, g, _, t, _ in refs]
+            res[f"{kname}-{aname}"].update({"planted_recall": round(rec_planted, 4),
+                                            "attention_mass_in_selection": round(float(np.mean(mass_rec)), 4),
+                                            "exact_topk_overlap": round(float(np.mean(top_rec)), 4)})
+    res["exact_topk_attention_mass"] = round(float(np.mean([r[4] for r in refs])), 4)
+    res["quality_workload"] = f"{qc.name}, seed {seed}; attention mass over {len(refs)} sampled units"
+    del HL, mean, metas, sc, sel
+    torch.cuda.empty_cache()
+    log(f"score variants: {res}")
+    return res
 
 
 def working_set_study(cfg, L, q32, first_step, seed, ss, torch, steps=28, window=12):

@@ -62,25 +62,29 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__
     const int L = lane >> 4;
     const int col = lane & 15;
 
-    // weights of head g*G + col for chunks L*NCH .. L*NCH+NCH-1
+    // weights of head g*G + col for chunks L*NCH .. L*NCH+NCH-1, selected
+    // branch-free with masks on the 32-bit words (two bf16 each)
     frag_t w[NCH];
     {
         const bool live = col < G;
         const uint16_t *qh = q + ((int64_t)b * Hq + g * G + (live ? col : 0)) * D;
+        const uint32_t live_mask = live ? 0xFFFFFFFFu : 0u;
+        const bool hi_half = KIND == 0 && L >= 2;  // cuboid chunks 16..31 (L >= 2) multiply hi
 #pragma unroll
         for (int m = 0; m < NCH; ++m) {
-            const int c = L * NCH + m;
-            frag_t x;
-            x.u = *reinterpret_cast<const uint4 *>(qh + (c & 15) * 8);
+            const int c = (L * NCH + m) & 15;  // q channels c*8 .. c*8+7
+            const uint4 x = *reinterpret_cast<const uint4 *>(qh + c * 8);
+            uint32_t v[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                bool keep = live;
+            for (int i = 0; i < 4; ++i) {
+                uint32_t keep = live_mask;
                 if (KIND == 0) {
-                    const bool neg = (x.h[e] & 0x8000u) != 0;
-                    keep = keep && (neg != (c >= 16));  // hi half keeps q >= 0, lo half q < 0
+                    const uint32_t neg = ((v[i] >> 15) & 0x00010001u) * 0xFFFFu;  // 0xFFFF per negative half
+                    keep &= hi_half ? ~neg : neg;  // hi keeps max(q, 0), lo keeps min(q, 0)
                 }
-                w[m].h[e] = keep ? x.h[e] : (uint16_t)0;
+                v[i] &= keep;
             }
+            w[m].u = make_uint4(v[0], v[1], v[2], v[3]);
         }
     }
 
