@@ -53,6 +53,8 @@ def load(path):
     L.oracle_score_variant.argtypes = [vp, vp, i32, i32, vp, i32, i32, i32, i32, i32, vp]
     L.oracle_build_metadata_mean.restype = i32
     L.oracle_score_variant.restype = i32
+    L.oracle_prefill_plan.argtypes = [i64, i32, i64, vp, i64]
+    L.oracle_prefill_plan.restype = i64
     L.oracle_ws_decode.argtypes = [vp, i32, i32, i32, i32, i32, i32, sz]
     L.oracle_ws_decode.restype = i64
     L.oracle_ws_prefill.argtypes = [i64, i64, i64, i32, i32, i32, sz, i32]
@@ -196,6 +198,15 @@ class Oracle:
         _check(self.L.oracle_score_variant(_addr(q), _addr(meta), kind, agg, _addr(nblk), B, Hq, Hkv, nblk_max, d,
                                            _addr(S)), "score_variant")
         return S
+
+    # O13
+    def prefill_plan(self, T, layers, max_inject, cap=1 << 20):
+        """Items int32 [n][4] = (batch, layer, tok_begin, tok_end)."""
+        items = np.empty((cap, 4), np.int32)
+        n = self.L.oracle_prefill_plan(T, layers, max_inject, _addr(items), cap)
+        if n < 0:
+            raise ValueError("oracle prefill_plan: invalid arguments")
+        return items[:n].copy()
 
     # O8
     def ws_decode(self, sel_hist, w, record_bytes, fallback=0):

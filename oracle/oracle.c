@@ -5,7 +5,8 @@
  * blocks; on the saving side, appending new tokens to the open blocks
  * (with metadata when a block fills) and saving them to the DRAM pool; and
  * the working-set estimates and batch control of the scheduler; and the
- * mean-key metadata and score variants the paper names.
+ * mean-key metadata and score variants the paper names; and the plan of a
+ * layer-segmented prefill.
  *
  * TEST INFRASTRUCTURE ONLY.  Nothing in the product library calls, links or
  * loads this file; only the tests, the smoke check and the benchmark's CPU
@@ -727,4 +728,52 @@ int oracle_score_variant(const uint16_t *q, const uint16_t *meta, int kind, int 
         }
     }
     return 0;
+}
+
+/* ------------------------------------------------------------------------
+ * O13  Layer-segmented prefill plan (Section 3.4): the prompt's layers are
+ * run in consecutive batches, each injecting at most max_inject prompt
+ * tokens (the maxInjectToken bound; a layer over T prompt tokens injects T).
+ *   T <= max_inject: a batch runs s = floor(max_inject / T) whole layers
+ *       (the last batch the remaining ones);
+ *   T > max_inject: each layer is split into chunks of max_inject tokens
+ *       (the last chunk shorter), one chunk per batch, layer after layer
+ *       (the combination with chunked prefill).
+ * Output: one item per (batch, layer, token range), in execution order:
+ *   items[i] = {batch, layer, tok_begin, tok_end}.
+ * Returns the number of items, or -1 for invalid arguments or when more
+ * than cap items would be needed.
+ * ---------------------------------------------------------------------- */
+int64_t oracle_prefill_plan(int64_t T, int layers, int64_t max_inject, int32_t *items, int64_t cap)
+{
+    if (T <= 0 || layers <= 0 || max_inject <= 0)
+        return -1;
+    int64_t n = 0;
+    if (T <= max_inject) {
+        int64_t s = max_inject / T;
+        for (int l = 0; l < layers; ++l) {
+            if (n >= cap)
+                return -1;
+            items[4 * n + 0] = (int32_t)(l / s);
+            items[4 * n + 1] = l;
+            items[4 * n + 2] = 0;
+            items[4 * n + 3] = (int32_t)T;
+            ++n;
+        }
+    } else {
+        int64_t chunks = (T + max_inject - 1) / max_inject;
+        for (int l = 0; l < layers; ++l)
+            for (int64_t c = 0; c < chunks; ++c) {
+                if (n >= cap)
+                    return -1;
+                int64_t b = c * max_inject;
+                int64_t e = b + max_inject < T ? b + max_inject : T;
+                items[4 * n + 0] = (int32_t)(l * chunks + c);
+                items[4 * n + 1] = l;
+                items[4 * n + 2] = (int32_t)b;
+                items[4 * n + 3] = (int32_t)e;
+                ++n;
+            }
+    }
+    return n;
 }

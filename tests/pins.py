@@ -790,6 +790,38 @@ def pin_score_aggregations_reduce_to_heads(O):
                 assert np.all(np.isneginf(S[b, :, n:]))
 
 
+# ----------------------------------------------- O13 layer-segmented prefill
+def pin_prefill_plan_fixture(O):
+    """Hand-worked fixture (golden/prefill_plan.txt)."""
+    fx = read_fixture("prefill_plan.txt")
+    for case, (T, layers, M) in {"a": (1000, 5, 2500), "b": (1000, 2, 400), "c": (3, 4, 3)}.items():
+        want = [[int(x) for x in fx[k]] for k in sorted((k for k in fx if k.startswith(case + "_item")),
+                                                       key=lambda k: int(k.split("item")[1]))]
+        assert O.prefill_plan(T, layers, M).tolist() == want, case
+
+
+def pin_prefill_plan_invariants(O):
+    """Every (layer, token) is covered exactly once, layers run in order, a
+    batch injects at most maxInjectToken tokens, and batches are as full as
+    the rule allows: whole layers when the prompt fits, else chunks."""
+    rng = np.random.default_rng(51)
+    for _ in range(60):
+        T, layers, M = int(rng.integers(1, 3000)), int(rng.integers(1, 9)), int(rng.integers(1, 5000))
+        it = O.prefill_plan(T, layers, M)
+        cover = np.zeros((layers, T), np.int32)
+        for b, l, t0, t1 in it:
+            cover[l, t0:t1] += 1
+        assert np.all(cover == 1), (T, layers, M)
+        assert np.all(np.diff(it[:, 1]) >= 0) and np.all(np.diff(it[:, 0]) >= 0)
+        per_batch = np.bincount(it[:, 0], weights=it[:, 3] - it[:, 2])
+        assert per_batch.max() <= M
+        n_batches = it[-1, 0] + 1
+        if T <= M:
+            assert n_batches == -(-layers // (M // T))
+        else:
+            assert n_batches == layers * -(-T // M)
+
+
 GROUPS = {
     "meta": [pin_meta_bruteforce, pin_meta_ragged_untouched, pin_meta_signed_zero, pin_meta_record_offsets],
     "score": [pin_score_fixture, pin_score_upper_bound, pin_score_point_block, pin_score_corner_tight,
@@ -802,6 +834,7 @@ GROUPS = {
     "save": [pin_save_spans_blocks, pin_save_full_block_record, pin_save_capacity_error],
     "ws": [pin_ws_fixture, pin_ws_bruteforce, pin_ws_closed_forms],
     "meta_mean": [pin_meta_mean_exact_cases, pin_meta_mean_rounding],
+    "prefill_plan": [pin_prefill_plan_fixture, pin_prefill_plan_invariants],
     "score_variant": [pin_score_variant_fixture, pin_score_mean_is_mean_of_dots, pin_score_aggregations_reduce_to_heads],
     "schedule": [pin_schedule_fixture, pin_schedule_invariants],
 }

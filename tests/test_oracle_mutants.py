@@ -93,6 +93,12 @@ MUTANTS = [
      "s += at_lo < at_hi ? at_lo : at_hi;"),
     ("variant-ragged-ignored", "score_variant", "if (j >= n) {", "if (j >= nblk_max) {"),
     ("variant-mean-row-stride", "score_variant", "int row = kind == 0 ? 2 * d : d;", "int row = 2 * d;"),
+    ("plan-one-layer-per-batch", "prefill_plan", "int64_t s = max_inject / T;", "int64_t s = 1;"),
+    ("plan-chunk-floor", "prefill_plan", "int64_t chunks = (T + max_inject - 1) / max_inject;",
+     "int64_t chunks = T / max_inject;"),
+    ("plan-chunk-overruns", "prefill_plan", "int64_t e = b + max_inject < T ? b + max_inject : T;",
+     "int64_t e = b + max_inject;"),
+    ("plan-segment-off-by-one", "prefill_plan", "int64_t s = max_inject / T;", "int64_t s = max_inject / T + 1;"),
     ("save-ignores-offsets", "save", "(char *)pool + pool_off[u] + (int64_t)j",
      "(char *)pool + (int64_t)u * pool_blocks[b] * (int64_t)record_bytes + (int64_t)j"),
 ]
