@@ -65,6 +65,7 @@ def parse():
     ap.add_argument("--save-stream", choices=["own", "main"], default="own",
                     help="with --with-save: the FlashD2H copies on a stream of their own or on the main stream")
     ap.add_argument("--no-variants", action="store_true", help="skip the scoring-variant comparison")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the layer-segmented prefill measurement")
     ap.add_argument("--no-save-bandwidth", action="store_true",
                     help="skip the saving-bandwidth comparison (FlashD2H, per-block copies, GPU-direct)")
     ap.add_argument("--pool-budget-gib", type=float, default=56.0,
@@ -260,6 +261,9 @@ def main():
     # ------------------------------------------- saving bandwidth
     save_bw = None if args.no_save_bandwidth else save_bandwidth(ss, torch, H)
 
+    # ------------------------------------------- layer-segmented prefill
+    prefill = None if args.no_prefill else prefill_study(ss, torch, H)
+
     # ------------------------------------------------------ CPU baseline
     cpu = None
     if not args.no_cpu_baseline:
@@ -307,6 +311,8 @@ def main():
         result["working_set"] = ws_study
     if variants is not None:
         result["score_variants"] = variants
+    if prefill is not None:
+        result["prefill"] = prefill
     print(json.dumps(result), flush=True)
     for L in layers:
         L.close()
@@ -586,6 +592,32 @@ def working_set_study(cfg, L, q32, first_step, seed, ss, torch, steps=28, window
            "alg1_admitted_full_cache": int(admit.sum()), "alg1_admitted_quarter_cache": int(admit_q.sum()),
            "overlap_with_preceding_window": overlap, "steps": steps}
     log(f"working sets: {res}")
+    return res
+
+
+def prefill_study(ss, torch, H, T=131072, layers=8, Hkv=8, blk=16):
+    """The saving side of a layer-segmented prefill (Section 3.4) of one
+    128k-token prompt: per plan item, metadata of the completed blocks built
+    from the layer's token-major KV in HBM and a FlashD2H save of its tokens
+    (8 host threads); every layer takes the same KV so that only this side
+    is timed.  One layer's KV (T x Hkv x 512 B) is in HBM at a time."""
+    res = {"prompt_tokens": T, "layers": layers, "kv_heads": Hkv, "block": blk,
+           "hbm_kv_bytes_one_layer": T * Hkv * 2 * D * 2, "hbm_kv_bytes_all_layers": T * Hkv * 2 * D * 2 * layers}
+    for max_inject in (T, T // 4):
+        ex = H.PrefillExecutor(T, layers, Hkv, blk, max_inject, seed=1, threads=8, same_kv=True)
+        try:
+            ex.run()  # warm-up (first touch of the staging memory)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            batches = ex.run()
+            wall = time.perf_counter() - t0
+        finally:
+            ex.close()
+        kv_bytes = res["hbm_kv_bytes_all_layers"]
+        res[f"max_inject_{max_inject}"] = {"batches": batches, "ms": round(wall * 1e3, 2),
+                                           "GBps_saved": round(kv_bytes / wall / 1e9, 2),
+                                           "layer_tokens_per_s": round(T * layers / wall, 1)}
+    log(f"prefill: {res}")
     return res
 
 

@@ -125,6 +125,19 @@ ss_status ss_build_metadata(const void *kv_base, const int64_t *unit_off, const 
 ss_status ss_build_metadata_mean(const void *kv_base, const int64_t *unit_off, const int32_t *nblk, int B, int Hkv,
                                  int nblk_max, int blk, int d, void *meta, void *stream);
 
+/* Metadata of either kind from keys in any layout: block j of unit u
+ * starts at kv_base + unit_off[u] + j*block_stride, and its token t's d
+ * keys at + t*row_stride (the V part is not read).  Block records are
+ * block_stride = 2*blk*d*2, row_stride = d*2 (ss_build_metadata and
+ * ss_build_metadata_mean call this); a token-major KV tensor [tokens][Hkv]
+ * [2][d], e.g. a prompt's new KV during prefill, is block_stride =
+ * blk*Hkv*2*d*2, row_stride = Hkv*2*d*2, unit_off[g] = g*2*d*2.  Strides
+ * positive multiples of 16; kv_base, unit_off values and meta 16-byte
+ * aligned.  meta layout as for meta_kind. */
+ss_status ss_build_metadata_strided(const void *kv_base, const int64_t *unit_off, const int32_t *nblk, int B,
+                                    int Hkv, int nblk_max, int blk, int d, int64_t block_stride, int64_t row_stride,
+                                    int meta_kind, void *meta, void *stream);
+
 /* ------------------------------------------------------ scoring, selection
  * Criticality of block j for KV head g of sequence b (Section 2.2, the dot
  * product of the query with the block metadata, taken as the largest value
@@ -308,6 +321,11 @@ void ss_kv_saver_destroy(ss_kv_saver *saver);
  * stay unchanged until the copy has run (stream order).  SS_ERR_INVALID_ARG
  * if a token lies past its unit's pool blocks.  Not thread-safe per saver. */
 ss_status ss_kv_save(ss_kv_saver *saver, const void *new_kv, int n_new, const int32_t *len, void *stream);
+/* Points the saver at other records of the pool (e.g. the next layer's
+ * during a layer-segmented prefill): pool_off host int64 [B*Hkv],
+ * pool_blocks host int32 [B], copied.  Saves already issued keep the
+ * records they were issued for; the staging memory and threads are kept. */
+ss_status ss_kv_saver_retarget(ss_kv_saver *saver, const int64_t *pool_off, const int32_t *pool_blocks);
 /* Blocks until every save so far is in the pool; returns the first error
  * met by the asynchronous part (SS_ERR_HIP). */
 ss_status ss_kv_save_wait(ss_kv_saver *saver);
@@ -351,6 +369,18 @@ int64_t ss_ws_prefill_bytes(int64_t prompt_tokens, int64_t done_tokens, int64_t 
  * ws_bytes[i] stay within m_avl, else resets it (admit[i] = 0).
  * ws_bytes host int64 [n] (>= 0); *m_used = bytes admitted. */
 ss_status ss_schedule_batch(const int64_t *ws_bytes, int n, int64_t m_avl, int32_t *admit, int64_t *m_used);
+
+/* ------------------------------------------------ layer-segmented prefill
+ * The plan of a layer-segmented prefill (Section 3.4): a prompt of T
+ * tokens runs its `layers` layers in consecutive batches, each injecting at
+ * most max_inject prompt tokens (maxInjectToken; a layer over the prompt
+ * injects T).  If T <= max_inject a batch runs floor(max_inject / T) whole
+ * layers; otherwise every layer is split into chunks of max_inject tokens
+ * (the last shorter), one chunk per batch (the combination with chunked
+ * prefill).  items: host int32 [cap][4] rows (batch, layer, tok_begin,
+ * tok_end) in execution order; *n_items rows written.  SS_ERR_OOM if cap
+ * rows are not enough, SS_ERR_INVALID_ARG for non-positive arguments. */
+ss_status ss_prefill_plan(int64_t T, int layers, int64_t max_inject, int32_t *items, int64_t cap, int64_t *n_items);
 
 /* ------------------------------------------------------- one layer's step
  * The decode step of one layer over the HBM/DRAM hierarchy (Section 3.1's

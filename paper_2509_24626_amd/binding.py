@@ -75,6 +75,7 @@ _SIGNATURES = {
     "ss_kv_saver_destroy": (None, [_vp]),
     "ss_kv_save": (_i32, [_vp, _vp, _i32, _vp, _vp]),
     "ss_kv_save_wait": (_i32, [_vp]),
+    "ss_kv_saver_retarget": (_i32, [_vp, _vp, _vp]),
     "ss_ws_create": (_i32, [_i32, _i32, _i32, _sz, _vp]),
     "ss_ws_destroy": (None, [_vp]),
     "ss_ws_observe": (_i32, [_vp, _i32, _i64, _vp, _i32, _vp, _i32]),
@@ -82,6 +83,8 @@ _SIGNATURES = {
     "ss_ws_forget": (_i32, [_vp, _i64]),
     "ss_ws_prefill_bytes": (_i64, [_i64, _i64, _i64, _i32, _i32, _i32, _sz, _i32]),
     "ss_schedule_batch": (_i32, [_vp, _i32, _i64, _vp, _vp]),
+    "ss_build_metadata_strided": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i64, _i64, _i32, _vp, _vp]),
+    "ss_prefill_plan": (_i32, [_i64, _i32, _i64, _vp, _i64, _vp]),
 }
 
 
@@ -350,3 +353,28 @@ def ss_schedule_batch(ws_bytes, m_avl):
     _check(lib().ss_schedule_batch(ws_bytes.ctypes.data, ws_bytes.size, m_avl, admit.ctypes.data,
                                    ctypes.byref(used)))
     return admit, used.value
+
+
+def ss_build_metadata_strided(kv_base, unit_off, nblk, B, Hkv, nblk_max, blk, d, block_stride, row_stride, meta_kind,
+                              meta, stream=None):
+    _check(lib().ss_build_metadata_strided(_ptr(kv_base), _ptr(unit_off), _ptr(nblk), B, Hkv, nblk_max, blk, d,
+                                           block_stride, row_stride, meta_kind, _ptr(meta), _stream(stream)))
+
+
+def ss_prefill_plan(T, layers, max_inject):
+    """Returns int32 [n][4] rows (batch, layer, tok_begin, tok_end)."""
+    import numpy as np
+    valid = T > 0 and layers > 0 and max_inject > 0  # otherwise the library reports the error
+    per_layer = 1 if not valid or T <= max_inject else -(-T // max_inject)
+    cap = max(1, per_layer * max(layers, 0))
+    items = np.empty((cap, 4), np.int32)
+    n = ctypes.c_int64(0)
+    _check(lib().ss_prefill_plan(T, layers, max_inject, items.ctypes.data, cap, ctypes.byref(n)))
+    return items[:n.value].copy()
+
+
+def ss_kv_saver_retarget(saver, pool_off, pool_blocks):
+    import numpy as np
+    pool_off = np.ascontiguousarray(pool_off, dtype=np.int64)
+    pool_blocks = np.ascontiguousarray(pool_blocks, dtype=np.int32)
+    _check(lib().ss_kv_saver_retarget(saver, pool_off.ctypes.data, pool_blocks.ctypes.data))

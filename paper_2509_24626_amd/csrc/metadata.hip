@@ -43,10 +43,10 @@ template <int BLK>
 __global__ __launch_bounds__(256) void meta_kernel(const uint8_t *__restrict__ kv_base,
                                                    const int64_t *__restrict__ unit_off,
                                                    const int32_t *__restrict__ nblk, int Hkv, int nblk_max,
-                                                   int64_t total_blocks, uint16_t *__restrict__ meta)
+                                                   int64_t total_blocks, int64_t block_stride, int64_t row_stride,
+                                                   uint16_t *__restrict__ meta)
 {
     constexpr int D = ss::kHeadDim;
-    constexpr int64_t REC = 2LL * BLK * D * 2;
     const int lane = threadIdx.x & 63;
     const int64_t id = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (id >= total_blocks) return;
@@ -56,12 +56,12 @@ __global__ __launch_bounds__(256) void meta_kernel(const uint8_t *__restrict__ k
     n = n < 0 ? 0 : (n > nblk_max ? nblk_max : n);
     if (j >= n) return;
 
-    const uint8_t *rec = kv_base + unit_off[u] + (int64_t)j * REC;
+    const uint8_t *rec = kv_base + unit_off[u] + (int64_t)j * block_stride;
     const int row0 = lane >> 4;         // 0..3
     const int cbyte = (lane & 15) * 16;  // 8 channels
     uint32_t lo[4], hi[4];
     {
-        uint4 v = *reinterpret_cast<const uint4 *>(rec + row0 * (D * 2) + cbyte);
+        uint4 v = *reinterpret_cast<const uint4 *>(rec + row0 * row_stride + cbyte);
         lo[0] = hi[0] = to_key2(v.x);
         lo[1] = hi[1] = to_key2(v.y);
         lo[2] = hi[2] = to_key2(v.z);
@@ -69,7 +69,7 @@ __global__ __launch_bounds__(256) void meta_kernel(const uint8_t *__restrict__ k
     }
 #pragma unroll
     for (int r = 4; r < BLK; r += 4) {
-        uint4 v = *reinterpret_cast<const uint4 *>(rec + (r + row0) * (D * 2) + cbyte);
+        uint4 v = *reinterpret_cast<const uint4 *>(rec + (r + row0) * row_stride + cbyte);
         uint32_t k0 = to_key2(v.x), k1 = to_key2(v.y), k2 = to_key2(v.z), k3 = to_key2(v.w);
         lo[0] = min2(lo[0], k0); hi[0] = max2(hi[0], k0);
         lo[1] = min2(lo[1], k1); hi[1] = max2(hi[1], k1);
@@ -101,10 +101,10 @@ template <int BLK>
 __global__ __launch_bounds__(256) void meta_mean_kernel(const uint8_t *__restrict__ kv_base,
                                                         const int64_t *__restrict__ unit_off,
                                                         const int32_t *__restrict__ nblk, int Hkv, int nblk_max,
-                                                        int64_t total_blocks, uint32_t *__restrict__ meta)
+                                                        int64_t total_blocks, int64_t block_stride,
+                                                        int64_t row_stride, uint32_t *__restrict__ meta)
 {
     constexpr int D = ss::kHeadDim;
-    constexpr int64_t REC = 2LL * BLK * D * 2;
     const int lane = threadIdx.x & 63;
     const int64_t id = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (id >= total_blocks) return;
@@ -113,10 +113,10 @@ __global__ __launch_bounds__(256) void meta_mean_kernel(const uint8_t *__restric
     int n = nblk[u / Hkv];
     n = n < 0 ? 0 : (n > nblk_max ? nblk_max : n);
     if (j >= n) return;
-    const uint32_t *rows = reinterpret_cast<const uint32_t *>(kv_base + unit_off[u] + (int64_t)j * REC);
+    const uint8_t *rec = kv_base + unit_off[u] + (int64_t)j * block_stride;
     uint32_t w[BLK];
 #pragma unroll
-    for (int t = 0; t < BLK; ++t) w[t] = rows[t * (D / 2) + lane];
+    for (int t = 0; t < BLK; ++t) w[t] = reinterpret_cast<const uint32_t *>(rec + t * row_stride)[lane];
     float s0 = 0.0f, s1 = 0.0f;
 #pragma unroll
     for (int t = 0; t < BLK; ++t) {
@@ -128,53 +128,61 @@ __global__ __launch_bounds__(256) void meta_mean_kernel(const uint8_t *__restric
 
 }  // namespace
 
-extern "C" ss_status ss_build_metadata_mean(const void *kv_base, const int64_t *unit_off, const int32_t *nblk,
-                                            int B, int Hkv, int nblk_max, int blk, int d, void *meta, void *stream)
+extern "C" ss_status ss_build_metadata_strided(const void *kv_base, const int64_t *unit_off, const int32_t *nblk,
+                                               int B, int Hkv, int nblk_max, int blk, int d, int64_t block_stride,
+                                               int64_t row_stride, int meta_kind, void *meta, void *stream)
 {
-    SS_CHECK_ARG(B >= 0 && Hkv > 0 && nblk_max >= 0, "ss_build_metadata_mean: bad shape B=%d Hkv=%d nblk_max=%d",
-                 B, Hkv, nblk_max);
-    SS_CHECK_SUPPORTED(d == ss::kHeadDim, "ss_build_metadata_mean: d=%d (only 128)", d);
-    SS_CHECK_SUPPORTED(ss::supported_blk(blk), "ss_build_metadata_mean: blk=%d (8, 16 or 32)", blk);
-    SS_CHECK_SUPPORTED(nblk_max <= ss::kMaxBlocks, "ss_build_metadata_mean: nblk_max=%d > %d", nblk_max,
-                       ss::kMaxBlocks);
+    SS_CHECK_ARG(B >= 0 && Hkv > 0 && nblk_max >= 0, "ss_build_metadata: bad shape B=%d Hkv=%d nblk_max=%d", B,
+                 Hkv, nblk_max);
+    SS_CHECK_ARG(meta_kind == SS_META_CUBOID || meta_kind == SS_META_MEAN, "ss_build_metadata: metadata kind %d",
+                 meta_kind);
+    SS_CHECK_SUPPORTED(d == ss::kHeadDim, "ss_build_metadata: d=%d (only 128)", d);
+    SS_CHECK_SUPPORTED(ss::supported_blk(blk), "ss_build_metadata: blk=%d (8, 16 or 32)", blk);
+    SS_CHECK_SUPPORTED(nblk_max <= ss::kMaxBlocks, "ss_build_metadata: nblk_max=%d > %d", nblk_max, ss::kMaxBlocks);
+    SS_CHECK_ARG(block_stride > 0 && row_stride > 0 && block_stride % 16 == 0 && row_stride % 16 == 0,
+                 "ss_build_metadata: strides %lld, %lld must be positive multiples of 16", (long long)block_stride,
+                 (long long)row_stride);
     const int64_t total = (int64_t)B * Hkv * nblk_max;
     if (total == 0) return SS_OK;
-    SS_CHECK_ARG(kv_base && unit_off && nblk && meta, "ss_build_metadata_mean: null pointer");
-    SS_CHECK_ARG(((uintptr_t)meta & 3) == 0, "ss_build_metadata_mean: meta must be 4-byte aligned");
+    SS_CHECK_ARG(kv_base && unit_off && nblk && meta, "ss_build_metadata: null pointer");
+    SS_CHECK_ARG(((uintptr_t)kv_base & 15) == 0 && ((uintptr_t)meta & 15) == 0,
+                 "ss_build_metadata: kv_base and meta must be 16-byte aligned");
     const int64_t grid = (total + 3) / 4;
-    SS_CHECK_SUPPORTED(grid <= 0x7FFFFFFF, "ss_build_metadata_mean: too many blocks");
+    SS_CHECK_SUPPORTED(grid <= 0x7FFFFFFF, "ss_build_metadata: too many blocks");
     hipStream_t s = ss::as_stream(stream);
     const uint8_t *kv = static_cast<const uint8_t *>(kv_base);
-    uint32_t *m = static_cast<uint32_t *>(meta);
-    switch (blk) {
-    case 8: ss::launch(meta_mean_kernel<8>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
-    case 16: ss::launch(meta_mean_kernel<16>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
-    default: ss::launch(meta_mean_kernel<32>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
+    const dim3 gr((unsigned)grid), bl(256);
+    const int64_t bs = block_stride, rs = row_stride;
+    if (meta_kind == SS_META_CUBOID) {
+        uint16_t *m = static_cast<uint16_t *>(meta);
+        switch (blk) {
+        case 8: ss::launch(meta_kernel<8>, gr, bl, s, kv, unit_off, nblk, Hkv, nblk_max, total, bs, rs, m); break;
+        case 16: ss::launch(meta_kernel<16>, gr, bl, s, kv, unit_off, nblk, Hkv, nblk_max, total, bs, rs, m); break;
+        default: ss::launch(meta_kernel<32>, gr, bl, s, kv, unit_off, nblk, Hkv, nblk_max, total, bs, rs, m); break;
+        }
+    } else {
+        uint32_t *m = static_cast<uint32_t *>(meta);
+        switch (blk) {
+        case 8: ss::launch(meta_mean_kernel<8>, gr, bl, s, kv, unit_off, nblk, Hkv, nblk_max, total, bs, rs, m); break;
+        case 16: ss::launch(meta_mean_kernel<16>, gr, bl, s, kv, unit_off, nblk, Hkv, nblk_max, total, bs, rs, m); break;
+        default: ss::launch(meta_mean_kernel<32>, gr, bl, s, kv, unit_off, nblk, Hkv, nblk_max, total, bs, rs, m); break;
+        }
     }
-    return ss::check_launch("ss_build_metadata_mean");
+    return ss::check_launch("ss_build_metadata");
 }
 
 extern "C" ss_status ss_build_metadata(const void *kv_base, const int64_t *unit_off, const int32_t *nblk, int B,
                                        int Hkv, int nblk_max, int blk, int d, void *meta, void *stream)
 {
-    SS_CHECK_ARG(B >= 0 && Hkv > 0 && nblk_max >= 0, "ss_build_metadata: bad shape B=%d Hkv=%d nblk_max=%d", B,
-                 Hkv, nblk_max);
-    SS_CHECK_SUPPORTED(d == ss::kHeadDim, "ss_build_metadata: d=%d (only 128)", d);
-    SS_CHECK_SUPPORTED(ss::supported_blk(blk), "ss_build_metadata: blk=%d (8, 16 or 32)", blk);
-    SS_CHECK_SUPPORTED(nblk_max <= ss::kMaxBlocks, "ss_build_metadata: nblk_max=%d > %d", nblk_max,
-                       ss::kMaxBlocks);
-    const int64_t total = (int64_t)B * Hkv * nblk_max;
-    if (total == 0) return SS_OK;
-    SS_CHECK_ARG(kv_base && unit_off && nblk && meta, "ss_build_metadata: null pointer");
-    const int64_t grid = (total + 3) / 4;
-    SS_CHECK_SUPPORTED(grid <= 0x7FFFFFFF, "ss_build_metadata: too many blocks");
-    hipStream_t s = ss::as_stream(stream);
-    const uint8_t *kv = static_cast<const uint8_t *>(kv_base);
-    uint16_t *m = static_cast<uint16_t *>(meta);
-    switch (blk) {
-    case 8: ss::launch(meta_kernel<8>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
-    case 16: ss::launch(meta_kernel<16>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
-    default: ss::launch(meta_kernel<32>, dim3((unsigned)grid), dim3(256), s, kv, unit_off, nblk, Hkv, nblk_max, total, m); break;
-    }
-    return ss::check_launch("ss_build_metadata");
+    const int64_t rec = 2LL * blk * d * 2;  // block records: K rows of d bf16 each
+    return ss_build_metadata_strided(kv_base, unit_off, nblk, B, Hkv, nblk_max, blk, d, rec, (int64_t)d * 2,
+                                     SS_META_CUBOID, meta, stream);
+}
+
+extern "C" ss_status ss_build_metadata_mean(const void *kv_base, const int64_t *unit_off, const int32_t *nblk,
+                                            int B, int Hkv, int nblk_max, int blk, int d, void *meta, void *stream)
+{
+    const int64_t rec = 2LL * blk * d * 2;
+    return ss_build_metadata_strided(kv_base, unit_off, nblk, B, Hkv, nblk_max, blk, d, rec, (int64_t)d * 2,
+                                     SS_META_MEAN, meta, stream);
 }

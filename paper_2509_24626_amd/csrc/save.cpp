@@ -18,6 +18,7 @@
 #include <condition_variable>
 #include <cstring>
 #include <deque>
+#include <memory>
 #include <mutex>
 #include <thread>
 #include <vector>
@@ -29,10 +30,18 @@ namespace {
 constexpr int kMaxChunks = 64;            // copies (and events) per save
 constexpr size_t kMinChunkBytes = 1 << 20;
 
+// where a save's tokens go: per unit the byte offset of its block array in
+// the pool, per sequence the blocks that array holds
+struct target {
+    std::vector<int64_t> pool_off;
+    std::vector<int32_t> pool_blocks;
+};
+
 struct job {
     int slot;
     int n_new;
     std::vector<int32_t> len;
+    std::shared_ptr<const target> to;  // fixed when the save is issued
     std::atomic<int> chunks_left{0};
 };
 
@@ -48,8 +57,7 @@ struct ss_kv_saver {
     int B = 0, Hkv = 0, blk = 0, d = 0, max_new = 0;
     size_t record_bytes = 0, row_bytes = 0, slot_bytes = 0;
     uint8_t *pool = nullptr;
-    std::vector<int64_t> pool_off;
-    std::vector<int32_t> pool_blocks;
+    std::shared_ptr<const target> to;
     std::vector<void *> staging;
     std::vector<std::vector<hipEvent_t>> copied;  // [slot][chunk]
     std::vector<bool> busy;
@@ -90,7 +98,7 @@ struct ss_kv_saver {
             const int j = T / blk, p = T - j * blk;
             for (int g = 0; g < Hkv; ++g) {
                 const uint16_t *kv = src + (r * Hkv + g) * 2 * d;
-                uint8_t *rec = pool + pool_off[(size_t)b * Hkv + g] + (int64_t)j * (int64_t)record_bytes;
+                uint8_t *rec = pool + jb.to->pool_off[(size_t)b * Hkv + g] + (int64_t)j * (int64_t)record_bytes;
                 std::memcpy(rec + (size_t)p * d * 2, kv, (size_t)d * 2);
                 uint16_t *vt = reinterpret_cast<uint16_t *>(rec + (size_t)blk * d * 2);
                 for (int c = 0; c < d; ++c) vt[c * blk + p] = kv[d + c];
@@ -162,8 +170,12 @@ ss_status ss_kv_saver_create(int B, int Hkv, int blk, int d, void *pool_host, co
     sv->record_bytes = (size_t)2 * blk * d * 2;
     sv->slot_bytes = (size_t)B * max_new_tokens * Hkv * 2 * d * 2;
     sv->pool = static_cast<uint8_t *>(pool_host);
-    sv->pool_off.assign(pool_off, pool_off + (size_t)B * Hkv);
-    sv->pool_blocks.assign(pool_blocks, pool_blocks + B);
+    {
+        auto t = std::make_shared<target>();
+        t->pool_off.assign(pool_off, pool_off + (size_t)B * Hkv);
+        t->pool_blocks.assign(pool_blocks, pool_blocks + B);
+        sv->to = std::move(t);
+    }
     sv->threads = threads;
     sv->row_bytes = (size_t)Hkv * 2 * d * 2;
     sv->staging.assign(staging_slots, nullptr);
@@ -203,9 +215,9 @@ ss_status ss_kv_save(ss_kv_saver *sv, const void *new_kv, int n_new, const int32
     SS_CHECK_ARG(new_kv, "ss_kv_save: null new_kv");
     for (int b = 0; b < sv->B; ++b) {
         SS_CHECK_ARG(len[b] >= 0, "ss_kv_save: len[%d] < 0", b);
-        SS_CHECK_ARG((int64_t)(len[b] + n_new - 1) / sv->blk < sv->pool_blocks[b],
+        SS_CHECK_ARG((int64_t)(len[b] + n_new - 1) / sv->blk < sv->to->pool_blocks[b],
                      "ss_kv_save: sequence %d: token %d lies past its %d pool blocks", b, len[b] + n_new - 1,
-                     sv->pool_blocks[b]);
+                     sv->to->pool_blocks[b]);
     }
     const hipStream_t s = ss::as_stream(stream);
     std::unique_lock<std::mutex> lk(sv->mu);
@@ -238,6 +250,7 @@ ss_status ss_kv_save(ss_kv_saver *sv, const void *new_kv, int n_new, const int32
     jb->slot = slot;
     jb->n_new = n_new;
     jb->len.assign(len, len + sv->B);
+    jb->to = sv->to;
     jb->chunks_left.store(n_chunks);
     sv->busy[slot] = true;
     ++sv->in_flight;
@@ -248,6 +261,22 @@ ss_status ss_kv_save(ss_kv_saver *sv, const void *new_kv, int n_new, const int32
     sv->next = (slot + 1) % (int)sv->staging.size();
     lk.unlock();
     sv->cv_work.notify_all();
+    return SS_OK;
+}
+
+ss_status ss_kv_saver_retarget(ss_kv_saver *sv, const int64_t *pool_off, const int32_t *pool_blocks)
+{
+    SS_CHECK_ARG(sv && pool_off && pool_blocks, "ss_kv_saver_retarget: null pointer");
+    for (int b = 0; b < sv->B; ++b) SS_CHECK_ARG(pool_blocks[b] >= 0, "ss_kv_saver_retarget: pool_blocks[%d] < 0", b);
+    try {
+        auto t = std::make_shared<target>();
+        t->pool_off.assign(pool_off, pool_off + (size_t)sv->B * sv->Hkv);
+        t->pool_blocks.assign(pool_blocks, pool_blocks + sv->B);
+        std::lock_guard<std::mutex> g(sv->mu);
+        sv->to = std::move(t);  // saves in flight keep the targets they were issued with
+    } catch (const std::bad_alloc &) {
+        return ss::fail(SS_ERR_OOM, "ss_kv_saver_retarget: out of memory");
+    }
     return SS_OK;
 }
 

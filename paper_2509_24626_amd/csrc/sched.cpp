@@ -12,7 +12,9 @@
 //
 // Prefill working sets are exact (closed forms), and the batch control of
 // Algorithm 1 walks the initial batch in order, admitting a request while
-// the admitted working sets fit the available HBM.
+// the admitted working sets fit the available HBM.  The plan of a
+// layer-segmented prefill (Section 3.4) assigns a prompt's layers, or
+// chunks of them, to batches under the maxInjectToken bound.
 #include <algorithm>
 #include <unordered_map>
 #include <vector>
@@ -173,6 +175,32 @@ ss_status ss_schedule_batch(const int64_t *ws_bytes, int n, int64_t m_avl, int32
         if (fits) used += ws_bytes[i];
     }
     *m_used = used;
+    return SS_OK;
+}
+
+ss_status ss_prefill_plan(int64_t T, int layers, int64_t max_inject, int32_t *items, int64_t cap, int64_t *n_items)
+{
+    SS_CHECK_ARG(n_items && (cap == 0 || items), "ss_prefill_plan: null pointer");
+    *n_items = 0;
+    SS_CHECK_ARG(T > 0 && layers > 0 && max_inject > 0, "ss_prefill_plan: T=%lld layers=%d max_inject=%lld",
+                 (long long)T, layers, (long long)max_inject);
+    SS_CHECK_ARG(T <= INT32_MAX, "ss_prefill_plan: T=%lld too large", (long long)T);
+    const bool whole = T <= max_inject;
+    const int64_t per_layer = whole ? 1 : (T + max_inject - 1) / max_inject;
+    const int64_t n = per_layer * layers;
+    if (n > cap) return ss::fail(SS_ERR_OOM, "ss_prefill_plan: %lld items > cap %lld", (long long)n, (long long)cap);
+    const int64_t seg = whole ? max_inject / T : 1;  // whole layers per batch
+    int64_t i = 0;
+    for (int l = 0; l < layers; ++l)
+        for (int64_t c = 0; c < per_layer; ++c, ++i) {
+            const int64_t t0 = whole ? 0 : c * max_inject;
+            const int64_t t1 = whole ? T : std::min(T, t0 + max_inject);
+            items[4 * i + 0] = (int32_t)(whole ? l / seg : l * per_layer + c);
+            items[4 * i + 1] = l;
+            items[4 * i + 2] = (int32_t)t0;
+            items[4 * i + 3] = (int32_t)t1;
+        }
+    *n_items = n;
     return SS_OK;
 }
 

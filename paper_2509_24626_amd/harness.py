@@ -330,3 +330,83 @@ def build_hier_model(cfg, seed, nblk, flags=0, budget=POOL_BUDGET, progress=None
         pool.close()
         raise
     return pool, layers, n
+
+
+class PrefillExecutor:
+    """Layer-segmented prefill of one prompt on the saving side (Section 3.4):
+    the plan (ss_prefill_plan) runs the layers, or chunks of them, in
+    batches.  A layer's new KV over the prompt, token-major [T][Hkv][2][d],
+    lives in the one HBM buffer that every layer reuses (the model's
+    projection would write it; it is drawn here).  Each plan item builds the
+    metadata of the blocks its tokens complete, straight from that buffer,
+    and saves its tokens to the DRAM pool with FlashD2H; when a layer ends,
+    its tail tokens go to the layer's open block.  Every layer's metadata
+    stays in HBM; only one layer's KV is there at a time."""
+
+    def __init__(self, T, layers, Hkv, blk, max_inject, seed=0, meta_kind=0, threads=8, flags=0, same_kv=False):
+        self.T, self.layers, self.Hkv, self.blk, self.max_inject = T, layers, Hkv, blk, max_inject
+        self.seed, self.meta_kind = seed, meta_kind
+        self.rb = 2 * blk * D * 2
+        self.nfull = T // blk
+        self.nmax = self.nfull + 1  # room for the block the tail will fill
+        units = layers * Hkv
+        self.pool = HostPool(units * self.nmax * self.rb, flags)
+        self.pool_off = (np.arange(units, dtype=np.int64) * self.nmax * self.rb).reshape(layers, Hkv)
+        self.items = ss.ss_prefill_plan(T, layers, max_inject)
+        max_chunk = int((self.items[:, 3] - self.items[:, 2]).max())
+        # one saver, pointed at each layer's records in turn
+        self.saver = ss.ss_kv_saver_create(1, Hkv, blk, D, self.pool.host, self.pool_off[0],
+                                           np.array([self.nmax], np.int32), max_chunk, 2, threads)
+        self.same_kv = same_kv  # every layer's KV equal to layer 0's (timing the save side alone)
+        rows = (2,) if meta_kind == ss.SS_META_CUBOID else ()
+        self.meta = torch.zeros(layers, Hkv, self.nmax, *rows, D, dtype=torch.int16, device="cuda")
+        self.buf = torch.empty(T, Hkv, 2, D, dtype=torch.bfloat16, device="cuda")  # one layer's KV
+        self.open = torch.zeros(layers, Hkv, self.rb // 2, dtype=torch.int16, device="cuda")
+        self.len_dev = torch.zeros(layers, dtype=torch.int32, device="cuda")
+        self.nblk_dev = torch.zeros(layers, dtype=torch.int32, device="cuda")
+        self.unit_off = _dev(np.arange(Hkv, dtype=np.int64) * 2 * D * 2, np.int64)
+        self.scales = [gen.channel_scales(Hkv, D, seed, l, "cuda") for l in range(layers)]
+
+    def layer_kv(self, l):
+        sK, sV = self.scales[l]
+        return gen.prefill_kv(self.T, self.Hkv, D, sK, sV, self.seed, l, "cuda")
+
+    def run(self, progress=None):
+        """Runs every batch of the plan; returns the number of batches."""
+        T, blk, Hkv = self.T, self.blk, self.Hkv
+        row = Hkv * 2 * D * 2  # bytes per token
+        cur = -1
+        for batch, l, t0, t1 in self.items.tolist():
+            if l != cur:
+                if cur < 0 or not self.same_kv:
+                    self.buf.copy_(self.layer_kv(l))  # the layer's projection output
+                if cur >= 0:
+                    ss.ss_kv_saver_retarget(self.saver, self.pool_off[l], np.array([self.nmax], np.int32))
+                cur = l
+            j0, j1 = t0 // blk, t1 // blk  # blocks whose last token lies in [t0, t1)
+            if j1 > j0:
+                n = torch.tensor([j1 - j0], dtype=torch.int32, device="cuda")
+                base = self.buf.data_ptr() + j0 * blk * row
+                ss.ss_build_metadata_strided(base, self.unit_off, n, 1, Hkv, self.nmax, blk, D, blk * row, row,
+                                             self.meta_kind, self.meta[l, :, j0:].data_ptr())
+            ss.ss_kv_save(self.saver, self.buf.data_ptr() + t0 * row, t1 - t0, np.array([t0], np.int32))
+            if t1 == T:
+                # the tail of the prompt opens the layer's next block
+                self.len_dev[l] = self.nfull * blk
+                self.nblk_dev[l] = self.nfull
+                for t in range(self.nfull * blk, T):
+                    ss.ss_append_kv(self.buf[t], self.len_dev[l:l + 1], self.nblk_dev[l:l + 1], 1, Hkv, blk, D,
+                                    self.nmax, self.open[l], self.meta[l], None, meta_kind=self.meta_kind)
+                # the next layer's KV overwrites the buffer behind this layer's
+                # copies (same stream); their host scatter continues meanwhile
+            if progress:
+                progress(batch, l, t0, t1)
+        torch.cuda.synchronize()
+        ss.ss_kv_save_wait(self.saver)
+        return int(self.items[-1, 0]) + 1
+
+    def close(self):
+        if self.saver:
+            ss.ss_kv_saver_destroy(self.saver)
+            self.saver = None
+        self.pool.close()

@@ -105,6 +105,16 @@ def new_tokens(B, Hkv, d, sK, sV, seed, layer, step, device="cpu"):
     return torch.stack([K, V], dim=2).to(torch.bfloat16).contiguous()
 
 
+def prefill_kv(T, Hkv, d, sK, sV, seed, layer, device="cpu"):
+    """A prompt's new KV for one layer, token-major bf16 [T][Hkv][2][d] (K
+    then V), drawn like the context: N(0,1) times the layer's channel
+    scales, fp32 rounded to bf16."""
+    g = generator(device, seed, "prefill", layer)
+    K = torch.randn(T, Hkv, d, generator=g, device=device) * sK[None]
+    V = torch.randn(T, Hkv, d, generator=g, device=device) * sV[None]
+    return torch.stack([K, V], dim=2).to(torch.bfloat16).contiguous()
+
+
 def lengths(cfg, seed):
     """Context length in tokens per sequence: fixed, or for a ragged
     workload T_b = blk * round(U[lo, hi] / blk), clamped to [lo, hi]."""

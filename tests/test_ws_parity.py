@@ -137,3 +137,12 @@ def test_prefill_bytes_match_oracle(oracle_impl):
                         assert ss.ss_ws_prefill_bytes(*args) == oracle_impl.ws_prefill(*args), args
     with pytest.raises(ss.SparseServeError):
         ss.ss_ws_prefill_bytes(-1, 0, 0, 32, 8, 16, 8192, True)
+
+
+def test_prefill_plan_matches_oracle(oracle_impl):
+    rng = np.random.default_rng(52)
+    for _ in range(100):
+        T, layers, M = int(rng.integers(1, 200000)), int(rng.integers(1, 40)), int(rng.integers(1, 300000))
+        np.testing.assert_array_equal(ss.ss_prefill_plan(T, layers, M), oracle_impl.prefill_plan(T, layers, M))
+    with pytest.raises(ss.SparseServeError):
+        ss.ss_prefill_plan(0, 2, 10)
