@@ -46,9 +46,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=1, help="untimed steps first (the first fills the cache)")
     ap.add_argument("--config", default="2", help="workload index or name (see synth/configs.py)")
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--parts", default="tent6",
-                    help="sequence groups pipelined within a layer step: N (equal), tentN (small first/last), "
-                         "or comma-separated sizes")
+    ap.add_argument("--parts", default="auto",
+                    help="sequence groups pipelined within a layer step: auto (tent-shaped, about one group per 10 "
+                         "sequences, 2 to 6), N (equal), tentN (small first/last), or comma-separated sizes")
     ap.add_argument("--cpu-seqs", type=int, default=64, help="sequences in the CPU-oracle sample")
     ap.add_argument("--cpu-steps", type=int, default=8, help="timed steps in the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -113,7 +113,11 @@ def main():
     log(f"workload {cfg.name}: {cfg.layers} layer(s), {n_distinct} with DRAM records of their own, "
         f"pool {per_layer * n_distinct / 2**30:.2f} GiB pinned")
     meta_ms = []
-    if args.parts.startswith("tent"):
+    if args.parts == "auto":
+        # per-group costs (a top-k launch, a host resolve, launches) favour few
+        # groups for small batches; tent-shaped groups, about one per 10 sequences
+        parts = H.tent_parts(cfg.B, max(2, min(6, round(cfg.B / 10))))
+    elif args.parts.startswith("tent"):
         parts = H.tent_parts(cfg.B, int(args.parts[4:]))
     elif "," in args.parts:
         parts = [int(x) for x in args.parts.split(",")]
