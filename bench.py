@@ -65,6 +65,7 @@ def parse():
     ap.add_argument("--save-stream", choices=["own", "main"], default="own",
                     help="with --with-save: the FlashD2H copies on a stream of their own or on the main stream")
     ap.add_argument("--no-variants", action="store_true", help="skip the scoring-variant comparison")
+    ap.add_argument("--no-working-set", action="store_true", help="skip the working-set study")
     ap.add_argument("--no-prefill", action="store_true", help="skip the layer-segmented prefill measurement")
     ap.add_argument("--no-save-bandwidth", action="store_true",
                     help="skip the saving-bandwidth comparison (FlashD2H, per-block copies, GPU-direct)")
@@ -254,7 +255,7 @@ def main():
 
     # ------------------------------------------- working sets (Section 3.3)
     ws_study = None
-    if new_kv is None and cfg.layers == 1:
+    if new_kv is None and cfg.layers == 1 and not args.no_working_set:
         ws_study = working_set_study(cfg, layers[0], qstreams[0][-1][0], warmup + steps, args.seed, ss, torch)
 
     # ------------------------------------------- scoring variants
@@ -339,13 +340,14 @@ KERNEL_SOURCES = {
 # hierarchical 128k-context layer, seed 0, 16 timed steps after 1 warm-up, groups 2,9,22,20,9,2
 _KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 16, 1, [2, 9, 22, 20, 9, 2]]
 TRAFFIC = {
-    "gather": {"key": _KEY, "digest": "6bd3251b3905aab8", "bytes": 260451784, "fetch": 131055560,
-               "write": 129396224},
-    "score": {"key": _KEY, "digest": "8d78773623e12ba9", "bytes": 2170171879, "fetch": 2152767879,
-              "write": 17404000},
-    "topk": {"key": _KEY, "digest": "8f6b9786eb7729ab", "bytes": 17254011, "fetch": 16991867, "write": 262144},
-    "attention": {"key": _KEY, "digest": "e242170c7670baf1", "bytes": 539115813, "fetch": 538067237,
-                  "write": 1048576},
+    "gather": {"key": _KEY, "digest": "809c83e6a60754bb", "bytes": 260450312, "fetch": 131054088,
+              "write": 129396224},
+    "score": {"key": _KEY, "digest": "b1d34d18dc71bc7d", "bytes": 2169855320, "fetch": 2152043736,
+              "write": 17811584},
+    "topk": {"key": _KEY, "digest": "2b36a2d12fb03589", "bytes": 17254011, "fetch": 16991867,
+              "write": 262144},
+    "attention": {"key": _KEY, "digest": "f6b1e88a61a963de", "bytes": 539118373, "fetch": 538069797,
+              "write": 1048576},
 }
 
 
