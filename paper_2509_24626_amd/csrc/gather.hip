@@ -7,9 +7,13 @@
 // wave keeps RPI*CH KiB of host-link reads in flight; workgroups stride over
 // the miss list.  The grid is small on purpose: a launch-shape sweep on
 // MI355X (8 GiB pinned pool, 16384 random 8 KiB records) measured 57.1-57.5
-// GB/s with 16-128 workgroups (a contiguous hipMemcpy reaches 57.0) but only
-// 54.5 GB/s with 2048, and a small grid leaves the compute units free for
-// the scoring and attention kernels that run concurrently with the gather.
+// GB/s with 16-128 workgroups alone (a contiguous hipMemcpy reaches 57.0)
+// but only 54.5 GB/s with 2048.  Inside the pipelined decode step, where two
+// gathers overlap beside the scoring and attention kernels, 32 workgroups
+// per launch of 8 KiB records gave the shortest step (2.50 ms on the 128k
+// workload, against 2.58-2.63 with 64, 2.70 with 128, 2.55-2.64 with 16-24
+// and 3.0 with 8); the grid scales inversely with the record size so that
+// each launch keeps the same bytes in flight.
 // The decode step also hands the kernel a small side copy (the group's slot
 // table, from mapped host memory to HBM) so that no copy-engine transfer,
 // and no cross-engine synchronisation, sits between resolve and attention.
@@ -78,7 +82,9 @@ void launch_variant(const int4 *miss, int64_t n_miss, const uint8_t *pool, const
 {
     constexpr int RPI = 2;
     int64_t blocks = (n_miss + RPI - 1) / RPI;
-    const int64_t max_blocks = 64;
+    // about 512 KiB of records in flight per launch: 32 workgroups of two 8 KiB
+    // records, 64 of 4 KiB, 16 of 16 KiB
+    const int64_t max_blocks = 32 * 2 / CH;
     if (blocks > max_blocks) blocks = max_blocks;
     if (blocks < 1) blocks = 1;
     ss::launch(gather_kernel<CH, RPI>, dim3((unsigned)blocks), dim3(256), s, miss, n_miss, pool, pool_off, cache,
