@@ -60,6 +60,8 @@ def parse():
                     help="rocprofv3 --pmc output folders of this script (FETCH_SIZE, WRITE_SIZE) and of "
                          "--calibrate-copy; prints the traffic summary and exits (no GPU)")
     ap.add_argument("--bench-json", help="with --summarize-pmc: the JSON line the profiled run printed")
+    ap.add_argument("--resolve", choices=["host", "device"], default="host",
+                    help="the slot-table resolve on the host (ss_decode_layer) or on the GPU (ss_decode_layer_dev)")
     ap.add_argument("--with-save", action="store_true",
                     help="every step also appends its new tokens (metadata on a fill) and saves them to DRAM "
                          "(FlashD2H); single-layer workloads")
@@ -147,7 +149,8 @@ def main():
                   for s in range(warmup + steps)]
     else:
         pool, layers, _ = H.build_hier_model(cfg, args.seed, nblk, args.pool_flags,
-                                             int(args.pool_budget_gib * 2**30), progress=log, parts=parts)
+                                             int(args.pool_budget_gib * 2**30), progress=log, parts=parts,
+                                             dev_cache=args.resolve == "device")
     qstreams = [H.query_stream(cfg, args.seed, l, warmup + steps - 1) for l in range(cfg.layers)]
 
     def run_step(L, l, s, events=None):
@@ -194,6 +197,7 @@ def main():
                 e.record()
     torch.cuda.synchronize()
     n_miss = np.zeros((steps, len(layers)), np.int64)
+    dev_total0 = [ss.ss_dev_cache_total_misses(L.dev) if L.dev is not None else 0 for L in layers]
     t0 = time.perf_counter()
     for i in range(steps):
         s = warmup + i
@@ -205,6 +209,9 @@ def main():
             ss.ss_kv_save_wait(L.saver)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    for l, L in enumerate(layers):
+        if L.dev is not None:  # the device resolve counts its misses on the GPU: spread the total over the steps
+            n_miss[:, l] = (ss.ss_dev_cache_total_misses(L.dev) - dev_total0[l]) / steps
 
     # ------------------------------------------------------- accounting
     # Gathers of consecutive groups overlap (two transfer streams), so the
@@ -295,7 +302,7 @@ def main():
         "config": {"workload": cfg.name, "batch": cfg.B, "q_heads": cfg.Hq, "kv_heads": cfg.Hkv, "head_dim": D,
                    "context": int(lens.max()), "block": cfg.blk, "topk_blocks": cfg.k, "cache_frac": cfg.cache_frac,
                    "layers": cfg.layers, "layers_with_own_dram_records": n_distinct, "drift": cfg.drift,
-                   "seed": args.seed},
+                   "seed": args.seed, "resolve": args.resolve},
         "roofline": dict(kernel=dominant, **roof[dominant]),
         "pipeline_ms": pipe,
         "rooflines_isolated": iso,

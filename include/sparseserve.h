@@ -231,6 +231,41 @@ ss_status ss_cache_resolve_range(ss_cache *cache, int64_t step, int b_begin, int
  * empty) and its last use.  Arrays hold ss_cache_total_slots entries. */
 ss_status ss_cache_export(const ss_cache *cache, int32_t *slot_block, int64_t *slot_last);
 
+/* ------------------------------------------------ block cache on the GPU
+ * The same per-unit LRU as ss_cache (identical slots and misses for the
+ * same selections), with its state in HBM and its resolve a kernel, so that
+ * a decode step needs no host round trip (ss_decode_layer_dev).  Supported:
+ * capacities up to 8192 slots per unit, k up to 512, steps in [0, 2^31)
+ * and not decreasing.
+ *   table_room: host int32 [B], the most blocks each sequence can reach
+ *       (block indices below it); capacity: host int32 [B*Hkv]
+ * Creation allocates the state in device memory (one hipMalloc) and waits
+ * for its initialisation on `stream`; the resolve allocates nothing. */
+typedef struct ss_dev_cache ss_dev_cache;
+ss_status ss_dev_cache_create(int B, int Hkv, const int32_t *table_room, const int32_t *capacity, void *stream,
+                              ss_dev_cache **out);
+void ss_dev_cache_destroy(ss_dev_cache *cache);
+int64_t ss_dev_cache_total_slots(const ss_dev_cache *cache);
+/* Resolves sequences [b_begin, b_end) on `stream` with the rules of
+ * ss_cache_resolve.  sel: device int32 [b_end-b_begin][Hkv][k] (the rows of
+ * sequence b_begin on); nblk: device int32 [B]; slots: device int32, same
+ * shape as sel; miss: device int32 [B*Hkv][k][4]: unit u's miss rows (b, g,
+ * block, slot), ascending by block, at row u*k, their number kept in the
+ * cache (ss_dev_cache_miss_counts).  A malformed selection or one larger
+ * than the unit's capacity leaves that unit unchanged, writes -1 slots and
+ * no misses, and raises a flag that ss_dev_cache_miss_counts reports (1:
+ * malformed, 2: capacity). */
+ss_status ss_dev_cache_resolve(ss_dev_cache *cache, int64_t step, int b_begin, int b_end, const int32_t *sel, int k,
+                               const int32_t *nblk, int32_t *slots, int32_t *miss, void *stream);
+/* Waits for the device, then copies the last resolve's miss count per unit
+ * (host int32 [B*Hkv]) and, if error_flags is not NULL, the error flags
+ * raised so far. */
+ss_status ss_dev_cache_miss_counts(const ss_dev_cache *cache, int32_t *counts, int32_t *error_flags);
+/* State dump for tests, as ss_cache_export (waits for the device). */
+ss_status ss_dev_cache_export(const ss_dev_cache *cache, int32_t *slot_block, int64_t *slot_last);
+/* Waits for the device; *total = misses over every resolve so far. */
+ss_status ss_dev_cache_total_misses(const ss_dev_cache *cache, int64_t *total);
+
 /* ----------------------------------------------------------------- gather
  * FlashH2D-style loading (Section 3.2.1): one kernel copies every missed
  * block record from the DRAM pool into its HBM cache slot:
@@ -448,6 +483,19 @@ typedef struct ss_layer_buffers {
 
 ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, const void *q, float *out, void *stream,
                           void *const *events, int64_t *n_miss);
+
+/* The decode step with the resolve on the GPU (ss_dev_cache, which takes
+ * the place of L->cache; the host buffers sel_host, slots_host and
+ * miss_host are not used).  Per group, scoring, top-k and the resolve run on
+ * `stream`, the gather on a transfer stream behind the resolve, attention
+ * on `stream` behind the gather.  The host enqueues the step and returns
+ * without waiting; the misses are counted in the cache
+ * (ss_dev_cache_miss_counts).  L->miss_dev holds each unit's miss rows at
+ * row u*k.  events as for ss_decode_layer (events[7p+2] after the resolve).
+ * The block cache's regions must be laid out as ss_cache_region_offsets
+ * gives them for the same capacities. */
+ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache *cache, int64_t step, const void *q,
+                              float *out, void *stream, void *const *events);
 
 #ifdef __cplusplus
 }

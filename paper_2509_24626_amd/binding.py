@@ -85,6 +85,14 @@ _SIGNATURES = {
     "ss_schedule_batch": (_i32, [_vp, _i32, _i64, _vp, _vp]),
     "ss_build_metadata_strided": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i64, _i64, _i32, _vp, _vp]),
     "ss_prefill_plan": (_i32, [_i64, _i32, _i64, _vp, _i64, _vp]),
+    "ss_dev_cache_create": (_i32, [_i32, _i32, _vp, _vp, _vp, _vp]),
+    "ss_dev_cache_destroy": (None, [_vp]),
+    "ss_dev_cache_total_slots": (_i64, [_vp]),
+    "ss_dev_cache_resolve": (_i32, [_vp, _i64, _i32, _i32, _vp, _i32, _vp, _vp, _vp, _vp]),
+    "ss_dev_cache_miss_counts": (_i32, [_vp, _vp, _vp]),
+    "ss_dev_cache_export": (_i32, [_vp, _vp, _vp]),
+    "ss_dev_cache_total_misses": (_i32, [_vp, _vp]),
+    "ss_decode_layer_dev": (_i32, [ctypes.POINTER(ss_layer_buffers), _vp, _i64, _vp, _vp, _vp, _vp]),
 }
 
 
@@ -378,3 +386,52 @@ def ss_kv_saver_retarget(saver, pool_off, pool_blocks):
     pool_off = np.ascontiguousarray(pool_off, dtype=np.int64)
     pool_blocks = np.ascontiguousarray(pool_blocks, dtype=np.int32)
     _check(lib().ss_kv_saver_retarget(saver, pool_off.ctypes.data, pool_blocks.ctypes.data))
+
+
+def ss_dev_cache_create(B, Hkv, table_room, capacity, stream=None):
+    import numpy as np
+    table_room = np.ascontiguousarray(table_room, dtype=np.int32)
+    capacity = np.ascontiguousarray(capacity, dtype=np.int32).reshape(-1)
+    h = ctypes.c_void_p()
+    _check(lib().ss_dev_cache_create(B, Hkv, table_room.ctypes.data, capacity.ctypes.data, _stream(stream),
+                                     ctypes.byref(h)))
+    return h.value
+
+
+def ss_dev_cache_destroy(handle):
+    lib().ss_dev_cache_destroy(handle)
+
+
+def ss_dev_cache_total_slots(handle):
+    return lib().ss_dev_cache_total_slots(handle)
+
+
+def ss_dev_cache_resolve(handle, step, b_begin, b_end, sel, k, nblk, slots, miss, stream=None):
+    _check(lib().ss_dev_cache_resolve(handle, step, b_begin, b_end, _ptr(sel), k, _ptr(nblk), _ptr(slots), _ptr(miss),
+                                      _stream(stream)))
+
+
+def ss_dev_cache_miss_counts(handle, units):
+    """Returns (counts int32 [units], error flags)."""
+    import numpy as np
+    counts = np.empty(units, np.int32)
+    err = ctypes.c_int32(0)
+    _check(lib().ss_dev_cache_miss_counts(handle, counts.ctypes.data, ctypes.byref(err)))
+    return counts, err.value
+
+
+def ss_dev_cache_export(handle, slot_block, slot_last):
+    _check(lib().ss_dev_cache_export(handle, _ptr(slot_block), _ptr(slot_last)))
+
+
+def ss_decode_layer_dev(buffers, handle, step, q, out, stream=None, events=None):
+    ev = None
+    if events is not None:
+        ev = (ctypes.c_void_p * len(events))(*events)
+    _check(lib().ss_decode_layer_dev(ctypes.byref(buffers), handle, step, _ptr(q), _ptr(out), _stream(stream), ev))
+
+
+def ss_dev_cache_total_misses(handle):
+    n = ctypes.c_int64(0)
+    _check(lib().ss_dev_cache_total_misses(handle, ctypes.byref(n)))
+    return n.value

@@ -15,7 +15,7 @@ BUILD = os.path.join(ROOT, "_build", "sparseserve")
 LIBDIR = os.path.join(HERE, "_lib")
 LIB = os.path.join(LIBDIR, "libsparseserve.so")
 SOURCES = ["status.cpp", "cache.cpp", "decode.cpp", "save.cpp", "sched.cpp", "metadata.hip", "score.hip", "topk.hip",
-           "gather.hip", "attention.hip", "append.hip"]
+           "gather.hip", "attention.hip", "append.hip", "devcache.hip"]
 ARCH = "gfx950"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 

@@ -34,6 +34,16 @@ ss_status launch_gather(const int32_t *miss, int64_t n_miss, const void *pool_ba
                         int64_t copy_n, hipStream_t s);
 int cache_batch(const ss_cache *c);
 int cache_kv_heads(const ss_cache *c);
+int dev_cache_batch(const ss_dev_cache *c);
+int dev_cache_kv_heads(const ss_dev_cache *c);
+int32_t *dev_cache_counts(ss_dev_cache *c);
+ss_status dev_cache_check_step(ss_dev_cache *c, int64_t step, int k);
+ss_status dev_cache_launch(ss_dev_cache *c, int64_t step, int b_begin, int b_end, const int32_t *sel, int k,
+                           const int32_t *nblk, int32_t *slots, int32_t *miss, hipStream_t s);
+ss_status launch_gather_units(const int32_t *rows, const int32_t *counts, int u0, int u1, int k,
+                              const void *pool_base, const int64_t *pool_off, void *cache_base,
+                              const int64_t *cache_off, const int32_t *nblk, const int32_t *capacity, int B, int Hkv,
+                              size_t record_bytes, hipStream_t s);
 }  // namespace ss
 
 namespace {
@@ -227,5 +237,97 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
         total += np;
     }
     *n_miss = total;
+    return SS_OK;
+}
+
+// The same step with the slot table resolved on the GPU (ss_dev_cache): per
+// group, scoring, top-k and the resolve run on `stream`; the group's gather
+// runs on a transfer stream behind an event recorded after its resolve, and
+// its attention on `stream` behind the gather.  The host enqueues the whole
+// step and returns without waiting for any of it.
+extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache *dc, int64_t step, const void *q,
+                                         float *out, void *stream, void *const *events)
+{
+    SS_CHECK_ARG(L && dc && q && out, "ss_decode_layer_dev: null argument");
+    SS_CHECK_ARG(L->sel_dev && L->slots_dev && L->miss_dev && L->scores && L->meta && L->nblk_dev,
+                 "ss_decode_layer_dev: null buffer");
+    SS_CHECK_ARG(L->B == ss::dev_cache_batch(dc) && L->Hkv == ss::dev_cache_kv_heads(dc),
+                 "ss_decode_layer_dev: shape differs from the cache's");
+    const int B = L->B, Hkv = L->Hkv, Hq = L->Hq, k = L->k, d = L->d;
+    if (B == 0) return SS_OK;
+    const int64_t rows_per_seq = (int64_t)Hkv * k;
+    SS_CHECK_ARG(L->miss_cap >= (int64_t)B * rows_per_seq, "ss_decode_layer_dev: miss_cap %lld < B*Hkv*k",
+                 (long long)L->miss_cap);
+    SS_CHECK_ARG(L->meta_kind == SS_META_CUBOID || L->meta_kind == SS_META_MEAN,
+                 "ss_decode_layer_dev: metadata kind %d", L->meta_kind);
+    int P = L->parts < 1 ? 1 : (L->parts > B ? B : L->parts);
+    if (L->part_end) {
+        P = L->parts;
+        SS_CHECK_ARG(P >= 1 && L->part_end[P - 1] == B, "ss_decode_layer_dev: part_end must end at B=%d", B);
+        for (int p = 0; p < P; ++p)
+            SS_CHECK_ARG(L->part_end[p] > (p ? L->part_end[p - 1] : 0),
+                         "ss_decode_layer_dev: part_end must be strictly increasing");
+    }
+    ss_status st = ss::dev_cache_check_step(dc, step, k);
+    if (st) return st;
+    std::lock_guard<std::mutex> lock(g_exec_mu);
+    exec_state *ex = nullptr;
+    if ((st = get_exec(P, &ex))) return st;
+    const hipStream_t s = ss::as_stream(stream);
+    const size_t rec = (size_t)2 * L->blk * d * 2;
+    const size_t meta_row = (size_t)(L->meta_kind == SS_META_MEAN ? 1 : 2) * d * 2;
+    const char *q8 = static_cast<const char *>(q);
+    const char *meta8 = static_cast<const char *>(L->meta);
+    const int32_t *pe = L->part_end;
+    auto b_of = [&](int p) { return p == 0 ? 0 : (pe ? pe[p - 1] : (int)((int64_t)B * p / P)); };
+    int32_t *counts = ss::dev_cache_counts(dc);
+
+    if ((st = hip_check(hipEventRecord(ex->start, s), "record")) ||
+        (st = hip_check(hipStreamWaitEvent(ex->xfer[0], ex->start, 0), "order transfer stream")) ||
+        (st = hip_check(hipStreamWaitEvent(ex->xfer[1], ex->start, 0), "order transfer stream")))
+        return st;
+    for (int p = 0; p < P; ++p) {
+        const int b0 = b_of(p), b1 = b_of(p + 1), Bp = b1 - b0;
+        const int64_t row0 = b0 * rows_per_seq;
+        hipStream_t x = ex->xfer[p & 1];
+        if ((st = record(events, 7 * p + 0, s))) return st;
+        st = ss_score_blocks_variant(q8 + (size_t)b0 * Hq * d * 2, meta8 + (size_t)b0 * Hkv * L->nblk_max * meta_row,
+                                     L->meta_kind, L->agg, L->nblk_dev + b0, Bp, Hq, Hkv, L->nblk_max, d,
+                                     L->scores + (size_t)b0 * Hkv * L->nblk_max, stream);
+        if (st) return st;
+        if ((st = record(events, 7 * p + 1, s))) return st;
+        st = ss::launch_topk(L->scores + (size_t)b0 * Hkv * L->nblk_max, L->nblk_dev + b0, Bp, Hkv, L->nblk_max, k,
+                             L->sel_dev + row0, nullptr, s);
+        if (st) return st;
+        st = ss::dev_cache_launch(dc, step, b0, b1, L->sel_dev + row0, k, L->nblk_dev, L->slots_dev + row0,
+                                  L->miss_dev, s);
+        if (st) return st;
+        if ((st = record(events, 7 * p + 2, s))) return st;
+        if ((st = hip_check(hipEventRecord(ex->sel_ready[p], s), "record")) ||
+            (st = hip_check(hipStreamWaitEvent(x, ex->sel_ready[p], 0), "order gather after resolve")))
+            return st;
+        hipEvent_t g0 = events ? reinterpret_cast<hipEvent_t>(events[7 * p + 3]) : nullptr;
+        hipEvent_t g1 = events ? reinterpret_cast<hipEvent_t>(events[7 * p + 4]) : nullptr;
+        ss::set_kernel_timing(g0, g1);
+        st = ss::launch_gather_units(L->miss_dev, counts, b0 * Hkv, b1 * Hkv, k, L->pool, L->pool_off_dev,
+                                     L->cache_base, L->cache_off_dev, L->nblk_dev, L->capacity_dev, B, Hkv, rec, x);
+        const ss::kernel_timing unused = ss::take_kernel_timing();
+        if (st) return st;
+        if ((unused.start && (st = hip_check(hipEventRecord(unused.start, x), "record timing event"))) ||
+            (unused.stop && (st = hip_check(hipEventRecord(unused.stop, x), "record timing event"))))
+            return st;
+        if ((st = hip_check(hipEventRecord(ex->gathered[p], x), "record"))) return st;
+    }
+    for (int p = 0; p < P; ++p) {
+        const int b0 = b_of(p), b1 = b_of(p + 1), Bp = b1 - b0;
+        const int64_t row0 = b0 * rows_per_seq;
+        if ((st = hip_check(hipStreamWaitEvent(s, ex->gathered[p], 0), "order attention after gather"))) return st;
+        if ((st = record(events, 7 * p + 5, s))) return st;
+        st = ss_sparse_attention(q8 + (size_t)b0 * Hq * d * 2, L->cache_base, L->cache_off_dev + b0 * Hkv,
+                                 L->slots_dev + row0, L->slot_limit, Bp, Hq, Hkv, d, L->blk, k, L->scale,
+                                 out + (size_t)b0 * Hq * d, L->attn_ws, L->attn_ws_bytes, stream);
+        if (st) return st;
+        if ((st = record(events, 7 * p + 6, s))) return st;
+    }
     return SS_OK;
 }

@@ -75,6 +75,63 @@ __global__ __launch_bounds__(256) void gather_kernel(const int4 *__restrict__ mi
     }
 }
 
+// The same copy for miss rows kept per unit: unit u's counts[u] rows start at
+// rows + u * k * 4 (the device resolve writes them so).  Workgroups stride
+// over the units [u0, u1) and copy each unit's rows RPI at a time.
+template <int CH, int RPI>
+__global__ __launch_bounds__(256) void gather_units_kernel(const int4 *__restrict__ rows_base,
+                                                           const int32_t *__restrict__ counts, int u0, int u1, int k,
+                                                           const uint8_t *__restrict__ pool,
+                                                           const int64_t *__restrict__ pool_off,
+                                                           uint8_t *__restrict__ cache,
+                                                           const int64_t *__restrict__ cache_off,
+                                                           const int32_t *__restrict__ nblk,
+                                                           const int32_t *__restrict__ capacity, int B, int Hkv)
+{
+    constexpr int64_t REC = 4096LL * CH;
+    const int t = threadIdx.x;
+    for (int uu = u0 + blockIdx.x; uu < u1; uu += gridDim.x) {
+        int cnt = counts[uu];
+        cnt = cnt < 0 ? 0 : (cnt > k ? k : cnt);
+        const int4 *miss = rows_base + (int64_t)uu * k;
+        for (int m0 = 0; m0 < cnt; m0 += RPI) {
+            const u32x4_t *src[RPI];
+            u32x4_t *dst[RPI];
+            bool ok[RPI];
+#pragma unroll
+            for (int r = 0; r < RPI; ++r) {
+                ok[r] = false;
+                src[r] = nullptr;
+                dst[r] = nullptr;
+                if (m0 + r < cnt) {
+                    const int4 e = miss[m0 + r];  // (b, g, block, slot)
+                    if (e.x >= 0 && e.x < B && e.y >= 0 && e.y < Hkv) {
+                        const int64_t u = (int64_t)e.x * Hkv + e.y;
+                        if (e.z >= 0 && e.z < nblk[e.x] && e.w >= 0 && e.w < capacity[u]) {
+                            ok[r] = true;
+                            src[r] = reinterpret_cast<const u32x4_t *>(pool + pool_off[u] + (int64_t)e.z * REC);
+                            dst[r] = reinterpret_cast<u32x4_t *>(cache + cache_off[u] + (int64_t)e.w * REC);
+                        }
+                    }
+                }
+            }
+            u32x4_t v[RPI][CH];
+#pragma unroll
+            for (int r = 0; r < RPI; ++r)
+                if (ok[r]) {
+#pragma unroll
+                    for (int c = 0; c < CH; ++c) v[r][c] = __builtin_nontemporal_load(src[r] + c * 256 + t);
+                }
+#pragma unroll
+            for (int r = 0; r < RPI; ++r)
+                if (ok[r]) {
+#pragma unroll
+                    for (int c = 0; c < CH; ++c) dst[r][c * 256 + t] = v[r][c];
+                }
+        }
+    }
+}
+
 template <int CH>
 void launch_variant(const int4 *miss, int64_t n_miss, const uint8_t *pool, const int64_t *pool_off, uint8_t *cache,
             const int64_t *cache_off, const int32_t *nblk, const int32_t *cap, int B, int Hkv,
@@ -91,9 +148,40 @@ void launch_variant(const int4 *miss, int64_t n_miss, const uint8_t *pool, const
                cache_off, nblk, cap, B, Hkv, copy_src, copy_dst, copy_n);
 }
 
+template <int CH>
+void launch_units_variant(const int4 *rows, const int32_t *counts, int u0, int u1, int k, const uint8_t *pool,
+                          const int64_t *pool_off, uint8_t *cache, const int64_t *cache_off, const int32_t *nblk,
+                          const int32_t *cap, int B, int Hkv, hipStream_t s)
+{
+    constexpr int RPI = 2;
+    int64_t blocks = u1 - u0;
+    const int64_t max_blocks = 32 * 2 / CH;  // as launch_variant: about 512 KiB in flight
+    if (blocks > max_blocks) blocks = max_blocks;
+    ss::launch(gather_units_kernel<CH, RPI>, dim3((unsigned)blocks), dim3(256), s, rows, counts, u0, u1, k, pool,
+               pool_off, cache, cache_off, nblk, cap, B, Hkv);
+}
+
 }  // namespace
 
 namespace ss {
+
+// Gather of the miss rows a device resolve left per unit, for units [u0, u1).
+ss_status launch_gather_units(const int32_t *rows, const int32_t *counts, int u0, int u1, int k,
+                              const void *pool_base, const int64_t *pool_off, void *cache_base,
+                              const int64_t *cache_off, const int32_t *nblk, const int32_t *capacity, int B, int Hkv,
+                              size_t record_bytes, hipStream_t s)
+{
+    if (u1 <= u0) return SS_OK;
+    const int4 *r = reinterpret_cast<const int4 *>(rows);
+    const uint8_t *p = static_cast<const uint8_t *>(pool_base);
+    uint8_t *c = static_cast<uint8_t *>(cache_base);
+    switch (record_bytes) {
+    case 4096: launch_units_variant<1>(r, counts, u0, u1, k, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, s); break;
+    case 8192: launch_units_variant<2>(r, counts, u0, u1, k, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, s); break;
+    default: launch_units_variant<4>(r, counts, u0, u1, k, p, pool_off, c, cache_off, nblk, capacity, B, Hkv, s); break;
+    }
+    return check_launch("ss_decode_layer_dev (gather)");
+}
 
 // Gather plus an optional word copy copy_src[0, copy_n) -> copy_dst (both
 // device-accessible); launches only if there is work.

@@ -103,8 +103,10 @@ class HierLayer:
     """One layer of the hierarchical workload: its DRAM pool slice, HBM
     metadata, HBM block cache and step buffers."""
 
-    def __init__(self, cfg, nblk_host, capacity, pool, pool_off_host, meta, parts=1, reserve=0, meta_kind=0, agg=0):
+    def __init__(self, cfg, nblk_host, capacity, pool, pool_off_host, meta, parts=1, reserve=0, meta_kind=0, agg=0,
+                 dev_cache=False):
         self.cfg = cfg
+        self.dev = None  # the slot table on the GPU (ss_dev_cache) instead of the host handle
         self.meta_kind, self.agg = meta_kind, agg
         # blocks each unit may gain (appended tokens) beyond its initial count:
         # the metadata, the scores and the pool have room for them
@@ -163,10 +165,24 @@ class HierLayer:
             parts=self.parts, part_end=self.part_end.ctypes.data, meta_kind=meta_kind, agg=agg)
         self.last_n_miss = 0
         self.saver = None
+        if dev_cache:
+            self.dev = ss.ss_dev_cache_create(B, Hkv, self.nblk_host + reserve, self.capacity)
+            assert ss.ss_dev_cache_total_slots(self.dev) == self.total_slots
 
     def step(self, t, q, events=None):
-        self.last_n_miss = ss.ss_decode_layer(self.buffers, t, q, self.out, None, events)
+        if self.dev is not None:
+            # nothing is waited for; misses are counted on the GPU (dev_miss_rows)
+            ss.ss_decode_layer_dev(self.buffers, self.dev, t, q, self.out, None, events)
+            self.last_n_miss = None
+        else:
+            self.last_n_miss = ss.ss_decode_layer(self.buffers, t, q, self.out, None, events)
         return self.out
+
+    def dev_miss_rows(self):
+        """Device resolve: (per-unit miss counts, rows [units][k][4], error flags) of the last step."""
+        counts, err = ss.ss_dev_cache_miss_counts(self.dev, self.units)
+        rows = self.miss.view(self.units, self.cfg.k, 4).cpu().numpy()
+        return counts, rows, err
 
     # ---------------------------------------------------------- save path
     def enable_save(self, threads=2, staging_slots=4, save_stream=None):
@@ -211,6 +227,9 @@ class HierLayer:
         return self.out
 
     def close(self):
+        if self.dev is not None:
+            ss.ss_dev_cache_destroy(self.dev)
+            self.dev = None
         if self.saver:
             ss.ss_kv_saver_destroy(self.saver)
             self.saver = None
@@ -249,7 +268,7 @@ def tent_parts(B, n):
 
 
 def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None, parts=1, reserve=0, meta_kind=0,
-                     agg=0):
+                     agg=0, dev_cache=False):
     """Draws one layer's KV per sequence on the GPU, builds its metadata in
     HBM and copies the records into `pool` at pool_base_off.  Returns the
     HierLayer (its pool offsets are relative to the pool base).  With
@@ -277,7 +296,7 @@ def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None,
         if progress and b % 16 == 15:
             progress(f"layer {layer}: {b + 1}/{cfg.B} sequences in the DRAM pool")
     torch.cuda.synchronize()
-    L = HierLayer(cfg, nblk, cache_capacity(cfg, nblk), pool, off, meta, parts, reserve, meta_kind, agg)
+    L = HierLayer(cfg, nblk, cache_capacity(cfg, nblk), pool, off, meta, parts, reserve, meta_kind, agg, dev_cache)
     return L
 
 
@@ -308,7 +327,7 @@ def distinct_layers(cfg, nblk, budget=POOL_BUDGET):
     return max(1, min(cfg.layers, budget // per_layer))
 
 
-def build_hier_model(cfg, seed, nblk, flags=0, budget=POOL_BUDGET, progress=None, parts=1):
+def build_hier_model(cfg, seed, nblk, flags=0, budget=POOL_BUDGET, progress=None, parts=1, dev_cache=False):
     """All cfg.layers layers over one DRAM pool (see distinct_layers).
     Returns (pool, layers, n_distinct)."""
     nblk = np.asarray(nblk, np.int32)
@@ -319,10 +338,11 @@ def build_hier_model(cfg, seed, nblk, flags=0, budget=POOL_BUDGET, progress=None
     try:
         for l in range(cfg.layers):
             if l < n:
-                L = build_hier_layer(cfg, seed, l, pool, l * per_layer, nblk, progress=progress, parts=parts)
+                L = build_hier_layer(cfg, seed, l, pool, l * per_layer, nblk, progress=progress, parts=parts,
+                                     dev_cache=dev_cache)
             else:
                 src = layers[l % n]
-                L = HierLayer(cfg, nblk, src.capacity, pool, src.pool_off_host, src.meta, parts)
+                L = HierLayer(cfg, nblk, src.capacity, pool, src.pool_off_host, src.meta, parts, dev_cache=dev_cache)
             layers.append(L)
     except BaseException:
         for L in layers:

@@ -123,8 +123,14 @@ class Track:
         oslots, omiss = self.lru.step(t, osel)
         o.gather(omiss, self.src, self.src_off, self.image, self.img_off, rb, Hkv)
         oout = o.attention(qh, self.image, self.img_off, oslots, Hkv, cfg.blk)
-        gslots = L.slots_h.numpy()[sb]
-        gmiss = L.miss_h.numpy()[:L.last_n_miss]
+        if L.dev is None:
+            gslots = L.slots_h.numpy()[sb]
+            gmiss = L.miss_h.numpy()[:L.last_n_miss]
+        else:  # device resolve: per-unit regions of miss rows
+            gslots = L.slots.cpu().numpy()[sb]
+            counts, rows, err = L.dev_miss_rows()
+            assert err == 0, err
+            gmiss = np.concatenate([rows[u, :counts[u]] for u in range(L.units)] + [np.zeros((0, 4), np.int32)])
         gout = L.out.cpu().numpy()[sb]
         for i, b in enumerate(sb):
             for g in range(Hkv):
@@ -147,7 +153,7 @@ class Track:
 
 
 def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_diverged_frac=0.25, parts=1, meta_kind=0,
-             agg=0):
+             agg=0, dev_cache=False):
     from paper_2509_24626_amd import harness as H
     lens = synth.gen.lengths(cfg, seed)
     nblk = (lens // cfg.blk).astype(np.int32)
@@ -157,14 +163,14 @@ def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_dive
     pool = H.HostPool(total, flags)
     try:
         L = H.build_hier_layer(cfg, seed, layer, pool, 0, nblk, progress=lambda m: print("[gpu]", m, flush=True),
-                               parts=parts, meta_kind=meta_kind, agg=agg)
+                               parts=parts, meta_kind=meta_kind, agg=agg, dev_cache=dev_cache)
         qs = H.query_stream(cfg, seed, layer, steps)
         tr = Track(oracle_impl, cfg, L, pool, sample_b, cfg.name)
         misses = []
         for t in range(steps + 1):
             L.step(t, qs[t][1])
             torch.cuda.synchronize()
-            misses.append(L.last_n_miss)
+            misses.append(L.last_n_miss if L.dev is None else int(L.dev_miss_rows()[0].sum()))
             tr.check(t, qs[t][1])
         rate = [m / (L.units * cfg.k) for m in misses]
         print(f"[gpu] {cfg.name}: miss rate per step {[round(r, 3) for r in rate]}; "
@@ -291,6 +297,26 @@ def test_hier_128k_full_size_with_save_sampled(ss, oracle_impl):
     every sequence fills one block at step 16."""
     cfg = synth.get(2)
     lockstep_with_save(oracle_impl, cfg, seed=0, sample_b=[0, 63], steps=20, parts=8, save_stream=True)
+
+
+@pytest.mark.parametrize("parts", [1, 3])
+def test_hier_small_device_resolve(ss, oracle_impl, parts):
+    """The decode step with the slot table resolved on the GPU
+    (ss_decode_layer_dev): slots, misses, gathered bytes and attention in
+    lock-step with the oracle."""
+    lockstep(oracle_impl, SMALL, seed=3, sample_b=range(SMALL.B), steps=6, parts=parts, dev_cache=True)
+
+
+def test_hier_gqa7_small_device_resolve(ss, oracle_impl):
+    cfg = dataclasses.replace(synth.get(4), name="qwen-gqa7-small-dev", B=2, ctx=16384, k=64, steps=4)
+    lockstep(oracle_impl, cfg, seed=5, sample_b=range(cfg.B), steps=4, dev_cache=True)
+
+
+def test_hier_128k_full_size_device_resolve_sampled(ss, oracle_impl):
+    """The 128k workload at full size with the device resolve (6 groups)."""
+    cfg = synth.get(2)
+    lockstep(oracle_impl, cfg, seed=0, sample_b=[1, 33, 62], steps=cfg.steps, parts=[2, 9, 22, 20, 9, 2],
+             dev_cache=True)
 
 
 def test_hier_128k_full_size_sampled(ss, oracle_impl):
