@@ -203,7 +203,7 @@ def main():
         s = warmup + i
         for l, L in enumerate(layers):
             run_step(L, l, s, events=[e.cuda_event if used[j] else None for j, e in enumerate(ev[i][l])])
-            n_miss[i, l] = L.last_n_miss
+            n_miss[i, l] = L.last_n_miss or 0
     if new_kv is not None:
         for L in layers:  # the last step's save is part of the work
             ss.ss_kv_save_wait(L.saver)

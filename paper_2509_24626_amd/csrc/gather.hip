@@ -17,6 +17,8 @@
 // The decode step also hands the kernel a small side copy (the group's slot
 // table, from mapped host memory to HBM) so that no copy-engine transfer,
 // and no cross-engine synchronisation, sits between resolve and attention.
+#include <climits>
+
 #include "internal.hpp"
 
 namespace {
@@ -76,8 +78,12 @@ __global__ __launch_bounds__(256) void gather_kernel(const int4 *__restrict__ mi
 }
 
 // The same copy for miss rows kept per unit: unit u's counts[u] rows start at
-// rows + u * k * 4 (the device resolve writes them so).  Workgroups stride
-// over the units [u0, u1) and copy each unit's rows RPI at a time.
+// rows + u * k * 4 (the device resolve writes them so).  The units' counts
+// are summed into a prefix in LDS, UCH units at a time; the workgroups then
+// stride over the flat miss index as gather_kernel does (RPI records each,
+// neighbouring workgroups on neighbouring records, so the load is balanced
+// whatever the spread of misses over units) and find each index's unit with a
+// cursor that only moves forward, 64 prefix entries per wave ballot.
 template <int CH, int RPI>
 __global__ __launch_bounds__(256) void gather_units_kernel(const int4 *__restrict__ rows_base,
                                                            const int32_t *__restrict__ counts, int u0, int u1, int k,
@@ -89,12 +95,41 @@ __global__ __launch_bounds__(256) void gather_units_kernel(const int4 *__restric
                                                            const int32_t *__restrict__ capacity, int B, int Hkv)
 {
     constexpr int64_t REC = 4096LL * CH;
-    const int t = threadIdx.x;
-    for (int uu = u0 + blockIdx.x; uu < u1; uu += gridDim.x) {
-        int cnt = counts[uu];
-        cnt = cnt < 0 ? 0 : (cnt > k ? k : cnt);
-        const int4 *miss = rows_base + (int64_t)uu * k;
-        for (int m0 = 0; m0 < cnt; m0 += RPI) {
+    constexpr int UCH = 1024, PER = UCH / 256;
+    __shared__ int s_pre[UCH + 1];  // s_pre[i]: misses of the chunk's units before unit i
+    __shared__ int s_wave[4];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    for (int c0 = u0; c0 < u1; c0 += UCH) {
+        const int n = min(UCH, u1 - c0);
+        int c[PER], sum = 0;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int i = t * PER + j;
+            int v = i < n ? counts[c0 + i] : 0;
+            v = v < 0 ? 0 : (v > k ? k : v);
+            c[j] = v;
+            sum += v;
+        }
+        int incl = sum;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int y = __shfl_up(incl, o);
+            if (lane >= o) incl += y;
+        }
+        if (lane == 63) s_wave[wave] = incl;
+        __syncthreads();
+        int run = incl - sum;
+        for (int w = 0; w < wave; ++w) run += s_wave[w];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            s_pre[t * PER + j] = run;
+            run += c[j];
+        }
+        if (t == 255) s_pre[UCH] = run;  // the chunk's total: units past n count 0
+        __syncthreads();
+        const int total = s_pre[UCH];
+        int cur = 0;  // s_pre[cur] <= m < s_pre[cur + 1] for the last index m placed
+        for (int m0 = blockIdx.x * RPI; m0 < total; m0 += gridDim.x * RPI) {
             const u32x4_t *src[RPI];
             u32x4_t *dst[RPI];
             bool ok[RPI];
@@ -103,8 +138,19 @@ __global__ __launch_bounds__(256) void gather_units_kernel(const int4 *__restric
                 ok[r] = false;
                 src[r] = nullptr;
                 dst[r] = nullptr;
-                if (m0 + r < cnt) {
-                    const int4 e = miss[m0 + r];  // (b, g, block, slot)
+                const int m = m0 + r;
+                if (m < total) {  // the same m in every lane: the ballots below are uniform
+                    for (;;) {
+                        const int j = cur + 1 + lane;
+                        const int v = j <= UCH ? s_pre[j] : INT_MAX;
+                        const unsigned long long hit = __ballot(v > m);
+                        if (hit) {
+                            cur += __builtin_ctzll(hit);
+                            break;
+                        }
+                        cur += 64;
+                    }
+                    const int4 e = rows_base[(int64_t)(c0 + cur) * k + (m - s_pre[cur])];  // (b, g, block, slot)
                     if (e.x >= 0 && e.x < B && e.y >= 0 && e.y < Hkv) {
                         const int64_t u = (int64_t)e.x * Hkv + e.y;
                         if (e.z >= 0 && e.z < nblk[e.x] && e.w >= 0 && e.w < capacity[u]) {
@@ -120,15 +166,16 @@ __global__ __launch_bounds__(256) void gather_units_kernel(const int4 *__restric
             for (int r = 0; r < RPI; ++r)
                 if (ok[r]) {
 #pragma unroll
-                    for (int c = 0; c < CH; ++c) v[r][c] = __builtin_nontemporal_load(src[r] + c * 256 + t);
+                    for (int c2 = 0; c2 < CH; ++c2) v[r][c2] = __builtin_nontemporal_load(src[r] + c2 * 256 + t);
                 }
 #pragma unroll
             for (int r = 0; r < RPI; ++r)
                 if (ok[r]) {
 #pragma unroll
-                    for (int c = 0; c < CH; ++c) dst[r][c * 256 + t] = v[r][c];
+                    for (int c2 = 0; c2 < CH; ++c2) dst[r][c2 * 256 + t] = v[r][c2];
                 }
         }
+        __syncthreads();  // every wave is done with s_pre before the next chunk overwrites it
     }
 }
 
@@ -154,9 +201,8 @@ void launch_units_variant(const int4 *rows, const int32_t *counts, int u0, int u
                           const int32_t *cap, int B, int Hkv, hipStream_t s)
 {
     constexpr int RPI = 2;
-    int64_t blocks = u1 - u0;
-    const int64_t max_blocks = 32 * 2 / CH;  // as launch_variant: about 512 KiB in flight
-    if (blocks > max_blocks) blocks = max_blocks;
+    // as launch_variant: about 512 KiB in flight (the miss total is known only on the GPU)
+    const int64_t blocks = 32 * 2 / CH;
     ss::launch(gather_units_kernel<CH, RPI>, dim3((unsigned)blocks), dim3(256), s, rows, counts, u0, u1, k, pool,
                pool_off, cache, cache_off, nblk, cap, B, Hkv);
 }
