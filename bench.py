@@ -352,13 +352,13 @@ KERNEL_SOURCES = {
 # hierarchical 128k-context layer, seed 0, 16 timed steps after 1 warm-up, groups 2,9,22,20,9,2
 _KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 16, 1, [2, 9, 22, 20, 9, 2]]
 TRAFFIC = {
-    "gather": {"key": _KEY, "digest": "809c83e6a60754bb", "bytes": 260450312, "fetch": 131054088,
+    "gather": {"key": _KEY, "digest": "cd2e644bbb5402f1", "bytes": 260439881, "fetch": 131043657,
               "write": 129396224},
-    "score": {"key": _KEY, "digest": "b1d34d18dc71bc7d", "bytes": 2169855320, "fetch": 2152043736,
-              "write": 17811584},
+    "score": {"key": _KEY, "digest": "b1d34d18dc71bc7d", "bytes": 2169836376, "fetch": 2152025496,
+              "write": 17810880},
     "topk": {"key": _KEY, "digest": "2b36a2d12fb03589", "bytes": 17254011, "fetch": 16991867,
               "write": 262144},
-    "attention": {"key": _KEY, "digest": "f6b1e88a61a963de", "bytes": 539118373, "fetch": 538069797,
+    "attention": {"key": _KEY, "digest": "f6b1e88a61a963de", "bytes": 539114981, "fetch": 538066405,
               "write": 1048576},
 }
 
