@@ -47,9 +47,9 @@ def parse():
     ap.add_argument("--config", default="2", help="workload index or name (see synth/configs.py)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--parts", default="auto",
-                    help="sequence groups pipelined within a layer step: auto (B >= 40: tent-shaped, about one "
-                         "group per 10 sequences, 2 to 6; smaller B: equal groups of about 5), N (equal), tentN "
-                         "(small first/last), or comma-separated sizes")
+                    help="sequence groups pipelined within a layer step: auto (B >= 40: seven groups that grow "
+                         "then shrink, 2,4,10,20,18,8,2 at B=64; smaller B: equal groups of about 5), N (equal), "
+                         "tentN (small first/last), or comma-separated sizes")
     ap.add_argument("--cpu-seqs", type=int, default=64, help="sequences in the CPU-oracle sample")
     ap.add_argument("--cpu-steps", type=int, default=8, help="timed steps in the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -119,10 +119,10 @@ def main():
     meta_ms = []
     if args.parts == "auto":
         # per-group costs (a top-k launch, a host resolve, launches) favour few
-        # groups for small batches: tent-shaped groups of about 10 sequences
-        # for large batches, equal groups of about 5 for small ones
+        # groups for small batches: equal groups of about 5 sequences; large
+        # batches get seven groups that grow while the pipeline fills
         if cfg.B >= 40:
-            parts = H.tent_parts(cfg.B, max(2, min(6, round(cfg.B / 10))))
+            parts = H.ramp_parts(cfg.B)
         else:
             parts = max(1, min(4, round(cfg.B / 5)))
     elif args.parts.startswith("tent"):

@@ -267,6 +267,22 @@ def tent_parts(B, n):
     return [int(x) for x in sizes]
 
 
+def ramp_parts(B, weights=(1, 2, 5, 10, 9, 4, 1)):
+    """Group sizes that roughly double while the pipeline fills (each gather
+    then lasts about as long as the next group's scoring, top-k and resolve, so
+    the link does not idle between the first gathers), then shrink, so little
+    work is left after the last gather.  For B = 64: 2, 4, 10, 20, 18, 8, 2."""
+    w = np.asarray(weights, np.float64)
+    n = min(len(w), B)
+    if n < len(w):
+        return tent_parts(B, n)
+    sizes = np.maximum(1, np.round(w / w.sum() * B)).astype(int)
+    i = int(np.argmax(w))
+    sizes[i] += B - int(sizes.sum())
+    assert sizes[i] >= 1 and int(sizes.sum()) == B
+    return [int(x) for x in sizes]
+
+
 def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None, parts=1, reserve=0, meta_kind=0,
                      agg=0, dev_cache=False):
     """Draws one layer's KV per sequence on the GPU, builds its metadata in
