@@ -307,6 +307,13 @@ def test_hier_small_device_resolve(ss, oracle_impl, parts):
     lockstep(oracle_impl, SMALL, seed=3, sample_b=range(SMALL.B), steps=6, parts=parts, dev_cache=True)
 
 
+def test_hier_many_units_one_group_device_resolve(ss, oracle_impl):
+    """72 sequences x 16 KV heads in one group: 1152 units, so the gather of
+    per-unit miss rows sums the units' counts in two LDS chunks (1024 + 128)."""
+    cfg = dataclasses.replace(SMALL, name="hier-many-units-b72-h16", B=72, Hq=32, Hkv=16, ctx=1024, k=8, steps=4)
+    lockstep(oracle_impl, cfg, seed=9, sample_b=[0, 35, 64, 71], steps=4, parts=1, dev_cache=True)
+
+
 def test_hier_gqa7_small_device_resolve(ss, oracle_impl):
     cfg = dataclasses.replace(synth.get(4), name="qwen-gqa7-small-dev", B=2, ctx=16384, k=64, steps=4)
     lockstep(oracle_impl, cfg, seed=5, sample_b=range(cfg.B), steps=4, dev_cache=True)
