@@ -71,7 +71,8 @@ def parse():
     ap.add_argument("--no-working-set", action="store_true", help="skip the working-set study")
     ap.add_argument("--no-prefill", action="store_true", help="skip the layer-segmented prefill measurement")
     ap.add_argument("--no-save-bandwidth", action="store_true",
-                    help="skip the saving-bandwidth comparison (FlashD2H, per-block copies, GPU-direct)")
+                    help="skip the transfer comparisons: saving (FlashD2H, per-block copies, GPU-direct) and "
+                         "loading (the gather kernel against per-block copies)")
     ap.add_argument("--pool-budget-gib", type=float, default=56.0,
                     help="pinned DRAM for KV records; layers beyond it reuse earlier layers' records")
     return ap.parse_args()
@@ -275,7 +276,8 @@ def main():
     if new_kv is None and cfg.layers == 1 and not args.no_variants:
         variants = score_variants_study(cfg, layers[0], qstreams[0][-1][1], pool, ss, torch)
 
-    # ------------------------------------------- saving bandwidth
+    # ------------------------------------------- transfer comparisons
+    load_cmp = None if args.no_save_bandwidth else load_comparison(cfg, layers[0], pool, ss, torch)
     save_bw = None if args.no_save_bandwidth else save_bandwidth(ss, torch, H)
 
     # ------------------------------------------- layer-segmented prefill
@@ -324,6 +326,8 @@ def main():
                                        "them with FlashD2H; the last save is waited for inside the timed region"}
     if save_bw is not None:
         result["save_bandwidth"] = save_bw
+    if load_cmp is not None:
+        result["load_comparison"] = load_cmp
     if ws_study is not None:
         result["working_set"] = ws_study
     if variants is not None:
@@ -636,6 +640,60 @@ def prefill_study(ss, torch, H, T=131072, layers=8, Hkv=8, blk=16):
                                            "GBps_saved": round(kv_bytes / wall / 1e9, 2),
                                            "layer_tokens_per_s": round(T * layers / wall, 1)}
     log(f"prefill: {res}")
+    return res
+
+
+def load_comparison(cfg, L, pool, ss, torch, reps=3):
+    """Loading one decode step's missed blocks into their HBM slots two ways
+    (the comparison of Section 3.2.1): the last timed step's miss rows of
+    this layer, each an 8 KiB (blk 16) record from the pinned DRAM pool.
+      memcpy_per_block  one hipMemcpyAsync (host to device) per record, issued
+                        from Python (~1 us of its overhead per call)
+      flashh2d          the gather kernel over the same rows (ss_gather_blocks)
+    Both rewrite the bytes the step already placed, so the cache is
+    unchanged.  GB/s = record bytes / wall time from issue to completion
+    (median of 3)."""
+    import ctypes
+    if L.dev is None:
+        rows = L.miss_h.numpy()[:L.last_n_miss].copy()
+    else:
+        counts, per_unit, err = L.dev_miss_rows()
+        rows = np.concatenate([per_unit[u, :counts[u]] for u in range(L.units)] + [np.zeros((0, 4), np.int32)])
+    n = len(rows)
+    if n == 0:
+        return None
+    rb = cfg.record_bytes
+    u = rows[:, 0].astype(np.int64) * cfg.Hkv + rows[:, 1]
+    src = [int(x) for x in pool.host + L.pool_off_host[u] + rows[:, 2].astype(np.int64) * rb]
+    dst = [int(x) for x in L.cache.data_ptr() + L.cache_off_host[u] + rows[:, 3].astype(np.int64) * rb]
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipMemcpyAsync.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p]
+    hip.hipMemcpyAsync.restype = ctypes.c_int
+    stream = torch.cuda.current_stream().cuda_stream
+    nbytes = n * rb
+    ts = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for d_, s_ in zip(dst, src):
+            if hip.hipMemcpyAsync(d_, s_, rb, 1, stream) != 0:
+                raise RuntimeError("hipMemcpyAsync failed")
+        torch.cuda.synchronize()
+        ts.append(time.perf_counter() - t0)
+    memcpy = nbytes / float(np.median(ts)) / 1e9
+    miss = torch.from_numpy(rows).cuda()
+    ts = []
+    for _ in range(reps):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        ss.ss_gather_blocks(miss, n, pool.dev, L.pool_off, L.cache, L.cache_off, L.nblk, L.cap_dev, cfg.B, cfg.Hkv,
+                            rb)
+        torch.cuda.synchronize()
+        ts.append(time.perf_counter() - t0)
+    flash = nbytes / float(np.median(ts)) / 1e9
+    res = {"records": n, "record_bytes": rb, "memcpy_per_block_GBps": round(memcpy, 2),
+           "flashh2d_GBps": round(flash, 2), "speedup": round(flash / memcpy, 2)}
+    log(f"loading {n} records: {res}")
     return res
 
 
