@@ -279,7 +279,14 @@ def ramp_parts(B, weights=(1, 2, 5, 10, 9, 4, 1)):
     sizes = np.maximum(1, np.round(w / w.sum() * B)).astype(int)
     i = int(np.argmax(w))
     sizes[i] += B - int(sizes.sum())
-    assert sizes[i] >= 1 and int(sizes.sum()) == B
+    if sizes[i] < 1:
+        # small batches, where rounding up to one sequence per group overshoots:
+        # one sequence each, the rest shared by largest remainder
+        share = w / w.sum() * (B - n)
+        sizes = 1 + np.floor(share).astype(int)
+        order = np.argsort(-(share - np.floor(share)), kind="stable")
+        sizes[order[:B - int(sizes.sum())]] += 1
+    assert int(sizes.sum()) == B and sizes.min() >= 1
     return [int(x) for x in sizes]
 
 
