@@ -5,8 +5,9 @@ Default workload: the hierarchical 128k-context layer (B=64, 32 query / 8
 KV heads, head_dim 128, 8192 blocks of 16 tokens per sequence, top-k 128
 blocks, all KV in a pinned DRAM pool, an HBM block cache of 25% of each
 sequence's blocks, queries drifting 0.3 per step).  One step is the whole
-decode path of that layer: block scoring, top-k selection, the host-side
-cache resolve, the gather of missed blocks from DRAM and sparse attention.
+decode path of that layer: block scoring, top-k selection, the cache resolve
+(on the GPU by default; --resolve host runs it on host threads), the gather
+of missed blocks from DRAM and sparse attention.
 Inputs are resident (pool in pinned DRAM, metadata and cache in HBM) when
 timing starts; the warm-up step fills the cold cache.
 
@@ -60,8 +61,9 @@ def parse():
                     help="rocprofv3 --pmc output folders of this script (FETCH_SIZE, WRITE_SIZE) and of "
                          "--calibrate-copy; prints the traffic summary and exits (no GPU)")
     ap.add_argument("--bench-json", help="with --summarize-pmc: the JSON line the profiled run printed")
-    ap.add_argument("--resolve", choices=["host", "device"], default="host",
-                    help="the slot-table resolve on the host (ss_decode_layer) or on the GPU (ss_decode_layer_dev)")
+    ap.add_argument("--resolve", choices=["host", "device"], default="device",
+                    help="the slot-table resolve on the GPU (ss_decode_layer_dev, default) or on host threads "
+                         "(ss_decode_layer)")
     ap.add_argument("--with-save", action="store_true",
                     help="every step also appends its new tokens (metadata on a fill) and saves them to DRAM "
                          "(FlashD2H); single-layer workloads")
@@ -246,7 +248,7 @@ def main():
     gather_bytes = float(n_miss.sum()) / steps * cfg.record_bytes
     busy_ms = pipe["link_busy"] * len(layers)
     ach = gather_bytes / (busy_ms * 1e-3) / 1e9 if busy_ms > 0 else 0.0
-    key = (cfg.name, args.seed, steps, warmup, tuple(layers[0].part_sizes))
+    key = (cfg.name, args.seed, steps, warmup, tuple(layers[0].part_sizes), args.resolve)
     roof = {"gather": {"bound": "host-link", "achieved": round(ach, 2), "peak": round(LINK_PEAK_GBS, 2),
                        "unit": "GB/s", "frac": round(ach / LINK_PEAK_GBS, 4), "bytes_per_step": int(gather_bytes),
                        "link_busy_ms_per_step": round(busy_ms, 4), "launches_per_step": len(layers) * P,
@@ -354,15 +356,15 @@ KERNEL_SOURCES = {
     "attention": ["attention.hip"],
 }
 # hierarchical 128k-context layer, seed 0, 16 timed steps after 1 warm-up, groups 2,9,22,20,9,2
-_KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 16, 1, [2, 4, 10, 20, 18, 8, 2]]
+_KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 16, 1, [2, 4, 10, 20, 18, 8, 2], "device"]
 TRAFFIC = {
-    "gather": {"key": _KEY, "digest": "cd2e644bbb5402f1", "bytes": 260475424, "fetch": 131079200,
-              "write": 129396224},
-    "score": {"key": _KEY, "digest": "b1d34d18dc71bc7d", "bytes": 2169856023, "fetch": 2152061079,
-              "write": 17794944},
+    "gather": {"key": _KEY, "digest": "57cfeae87f2b8a7e", "bytes": 260209184, "fetch": 131075104,
+              "write": 129134080},
+    "score": {"key": _KEY, "digest": "b1d34d18dc71bc7d", "bytes": 2169883160, "fetch": 2152019672,
+              "write": 17863488},
     "topk": {"key": _KEY, "digest": "2b36a2d12fb03589", "bytes": 17254011, "fetch": 16991867,
               "write": 262144},
-    "attention": {"key": _KEY, "digest": "f6b1e88a61a963de", "bytes": 539116517, "fetch": 538067941,
+    "attention": {"key": _KEY, "digest": "f6b1e88a61a963de", "bytes": 539113957, "fetch": 538065381,
               "write": 1048576},
 }
 
@@ -379,7 +381,7 @@ def source_digest(kernel):
 
 def traffic(kernel, key):
     rec = TRAFFIC.get(kernel)
-    norm = lambda k: (k[0], int(k[1]), int(k[2]), int(k[3]), tuple(int(x) for x in k[4]))
+    norm = lambda k: (k[0], int(k[1]), int(k[2]), int(k[3]), tuple(int(x) for x in k[4]), k[5] if len(k) > 5 else "host")
     if not rec or norm(rec["key"]) != norm(key):
         return None
     if rec["digest"] != source_digest(kernel):
@@ -439,7 +441,7 @@ def summarize_pmc(args):
     lines = []
     for c, folder in (("FETCH_SIZE", fetch_dir), ("WRITE_SIZE", write_dir)):
         rows = _pmc_rows(folder, c)
-        g = [v for n, _, v in rows if "gather_kernel" in n]
+        g = [v for n, _, v in rows if "gather_kernel" in n or "gather_units_kernel" in n]
         assert len(g) == (warmup + steps) * P, (len(g), warmup, steps, P)
         timed = g[warmup * P:]
         per_step = sum(timed) / steps * 1024 * scale[c]
@@ -448,7 +450,8 @@ def summarize_pmc(args):
             # the isolated full-batch launches are each kernel's last 10 dispatches
             vals = [v for n, _, v in rows if tag in n][-10:]
             out.setdefault(name, {})[c] = float(np.median(vals)) * 1024 * scale[c]
-    key = [bench["config"]["workload"], bench["config"]["seed"], steps, warmup, bench["parts"]]
+    key = [bench["config"]["workload"], bench["config"]["seed"], steps, warmup, bench["parts"],
+           bench["config"].get("resolve", "host")]
     algo = {"gather": bench["roofline"]["bytes_per_step"]}
     for name in ("score", "topk", "attention"):
         algo[name] = bench["rooflines_isolated"][name]["bytes_per_launch"]

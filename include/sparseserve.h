@@ -193,7 +193,7 @@ void ss_cache_destroy(ss_cache *cache);
 int64_t ss_cache_total_slots(const ss_cache *cache);
 /* off: host int64 [B*Hkv], byte offset of each unit's region */
 ss_status ss_cache_region_offsets(const ss_cache *cache, int64_t *off);
-/* Host threads used by ss_cache_resolve (default: hardware concurrency, at most 16). */
+/* Host threads used by ss_cache_resolve (default: half the CPUs the process may run on, at most 8). */
 ss_status ss_cache_set_threads(ss_cache *cache, int n_threads);
 /* New block counts after sequences grew (a block fills when its last token
  * is appended, Section 3.1): nblk host int32 [B], each >= the current

@@ -15,6 +15,8 @@
 // Units are independent; ss_cache_resolve validates every unit, sizes the
 // miss list with a prefix sum, then updates the units in parallel on a
 // small persistent thread pool.  Output order does not depend on threading.
+#include <sched.h>
+
 #include <algorithm>
 #include <atomic>
 #include <condition_variable>
@@ -119,11 +121,17 @@ struct unit_state {
 // host block-table entries a unit reserves beyond its blocks (sequences grow)
 int32_t block_slack(int32_t n) { return std::max<int32_t>(16, n / 8); }
 
+// Half the CPUs this process may run on, at most 8: idle workers spin
+// (yielding) between the groups of a step, and a pool as wide as the
+// process's CPU share, with the caller also polling, can exhaust a CPU quota
+// and get the whole process throttled for a scheduling period.
 int default_threads()
 {
-    unsigned n = std::thread::hardware_concurrency();
-    if (n == 0) n = 1;
-    return (int)std::min(16u, n);
+    int n = 0;
+    cpu_set_t set;
+    if (sched_getaffinity(0, sizeof(set), &set) == 0) n = CPU_COUNT(&set);
+    if (n <= 0) n = (int)std::thread::hardware_concurrency();
+    return std::max(1, std::min(8, n / 2));
 }
 
 // One pool for the process: resolves on different handles take turns.

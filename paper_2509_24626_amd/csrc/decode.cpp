@@ -55,6 +55,7 @@ namespace {
 // caller's stream would serialise the pipeline.
 struct exec_state {
     hipStream_t xfer[2] = {nullptr, nullptr};  // groups alternate between them
+    hipStream_t comp = nullptr;                // device resolve: scoring chain of groups after the first
     hipEvent_t start = nullptr;
     std::vector<hipEvent_t> sel_ready, gathered;
 };
@@ -240,11 +241,14 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
     return SS_OK;
 }
 
-// The same step with the slot table resolved on the GPU (ss_dev_cache): per
-// group, scoring, top-k and the resolve run on `stream`; the group's gather
-// runs on a transfer stream behind an event recorded after its resolve, and
-// its attention on `stream` behind the gather.  The host enqueues the whole
-// step and returns without waiting for any of it.
+// The same step with the slot table resolved on the GPU (ss_dev_cache).  The
+// first group's scoring, top-k, resolve, gather and attention run in order
+// on `stream`, so the link starts with no cross-queue hand-off (each costs
+// ~20 us).  The later groups' scoring, top-k and resolve run on a compute
+// stream of the library's, in parallel with the first group's; each such
+// group's gather runs on a transfer stream behind an event recorded after
+// its resolve, and its attention on `stream` behind the gather.  The host
+// enqueues the whole step and returns without waiting for any of it.
 extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache *dc, int64_t step, const void *q,
                                          float *out, void *stream, void *const *events)
 {
@@ -282,29 +286,36 @@ extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache
     auto b_of = [&](int p) { return p == 0 ? 0 : (pe ? pe[p - 1] : (int)((int64_t)B * p / P)); };
     int32_t *counts = ss::dev_cache_counts(dc);
 
+    if (P > 1 && !ex->comp &&
+        (st = hip_check(hipStreamCreateWithFlags(&ex->comp, hipStreamNonBlocking), "create compute stream")))
+        return st;
     if ((st = hip_check(hipEventRecord(ex->start, s), "record")) ||
         (st = hip_check(hipStreamWaitEvent(ex->xfer[0], ex->start, 0), "order transfer stream")) ||
-        (st = hip_check(hipStreamWaitEvent(ex->xfer[1], ex->start, 0), "order transfer stream")))
+        (st = hip_check(hipStreamWaitEvent(ex->xfer[1], ex->start, 0), "order transfer stream")) ||
+        (P > 1 && (st = hip_check(hipStreamWaitEvent(ex->comp, ex->start, 0), "order compute stream"))))
         return st;
     for (int p = 0; p < P; ++p) {
         const int b0 = b_of(p), b1 = b_of(p + 1), Bp = b1 - b0;
         const int64_t row0 = b0 * rows_per_seq;
-        hipStream_t x = ex->xfer[p & 1];
-        if ((st = record(events, 7 * p + 0, s))) return st;
+        // the first group's chain and gather on `stream`; later groups' chains on
+        // the compute stream, their gathers on alternate transfer streams
+        const hipStream_t c = p == 0 ? s : ex->comp;
+        const hipStream_t x = p == 0 ? s : ex->xfer[p & 1];
+        if ((st = record(events, 7 * p + 0, c))) return st;
         st = ss_score_blocks_variant(q8 + (size_t)b0 * Hq * d * 2, meta8 + (size_t)b0 * Hkv * L->nblk_max * meta_row,
                                      L->meta_kind, L->agg, L->nblk_dev + b0, Bp, Hq, Hkv, L->nblk_max, d,
-                                     L->scores + (size_t)b0 * Hkv * L->nblk_max, stream);
+                                     L->scores + (size_t)b0 * Hkv * L->nblk_max, c);
         if (st) return st;
-        if ((st = record(events, 7 * p + 1, s))) return st;
+        if ((st = record(events, 7 * p + 1, c))) return st;
         st = ss::launch_topk(L->scores + (size_t)b0 * Hkv * L->nblk_max, L->nblk_dev + b0, Bp, Hkv, L->nblk_max, k,
-                             L->sel_dev + row0, nullptr, s);
+                             L->sel_dev + row0, nullptr, c);
         if (st) return st;
         st = ss::dev_cache_launch(dc, step, b0, b1, L->sel_dev + row0, k, L->nblk_dev, L->slots_dev + row0,
-                                  L->miss_dev, s);
+                                  L->miss_dev, c);
         if (st) return st;
-        if ((st = record(events, 7 * p + 2, s))) return st;
-        if ((st = hip_check(hipEventRecord(ex->sel_ready[p], s), "record")) ||
-            (st = hip_check(hipStreamWaitEvent(x, ex->sel_ready[p], 0), "order gather after resolve")))
+        if ((st = record(events, 7 * p + 2, c))) return st;
+        if (p > 0 && ((st = hip_check(hipEventRecord(ex->sel_ready[p], c), "record")) ||
+                      (st = hip_check(hipStreamWaitEvent(x, ex->sel_ready[p], 0), "order gather after resolve"))))
             return st;
         hipEvent_t g0 = events ? reinterpret_cast<hipEvent_t>(events[7 * p + 3]) : nullptr;
         hipEvent_t g1 = events ? reinterpret_cast<hipEvent_t>(events[7 * p + 4]) : nullptr;
@@ -316,12 +327,13 @@ extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache
         if ((unused.start && (st = hip_check(hipEventRecord(unused.start, x), "record timing event"))) ||
             (unused.stop && (st = hip_check(hipEventRecord(unused.stop, x), "record timing event"))))
             return st;
-        if ((st = hip_check(hipEventRecord(ex->gathered[p], x), "record"))) return st;
+        if (p > 0 && (st = hip_check(hipEventRecord(ex->gathered[p], x), "record"))) return st;
     }
     for (int p = 0; p < P; ++p) {
         const int b0 = b_of(p), b1 = b_of(p + 1), Bp = b1 - b0;
         const int64_t row0 = b0 * rows_per_seq;
-        if ((st = hip_check(hipStreamWaitEvent(s, ex->gathered[p], 0), "order attention after gather"))) return st;
+        if (p > 0 && (st = hip_check(hipStreamWaitEvent(s, ex->gathered[p], 0), "order attention after gather")))
+            return st;
         if ((st = record(events, 7 * p + 5, s))) return st;
         st = ss_sparse_attention(q8 + (size_t)b0 * Hq * d * 2, L->cache_base, L->cache_off_dev + b0 * Hkv,
                                  L->slots_dev + row0, L->slot_limit, Bp, Hq, Hkv, d, L->blk, k, L->scale,
