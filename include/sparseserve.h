@@ -486,14 +486,19 @@ ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, const void *q
 
 /* The decode step with the resolve on the GPU (ss_dev_cache, which takes
  * the place of L->cache; the host buffers sel_host, slots_host and
- * miss_host are not used).  Per group, scoring, top-k and the resolve run on
- * `stream`, the gather on a transfer stream behind the resolve, attention
- * on `stream` behind the gather.  The host enqueues the step and returns
- * without waiting; the misses are counted in the cache
- * (ss_dev_cache_miss_counts).  L->miss_dev holds each unit's miss rows at
- * row u*k.  events as for ss_decode_layer (events[7p+2] after the resolve).
- * The block cache's regions must be laid out as ss_cache_region_offsets
- * gives them for the same capacities. */
+ * miss_host are not used).  The first group's scoring, top-k, resolve,
+ * gather and attention run in order on `stream`.  Each later group's
+ * scoring, top-k and resolve run on a compute stream the library creates
+ * once per device (default priority), its gather on a transfer stream
+ * behind the resolve, and its attention on `stream` behind the gather; all
+ * of it is ordered after the work already on `stream`, and `stream` holds
+ * every attention, so work enqueued on `stream` afterwards sees the whole
+ * step.  The host enqueues the step and returns without waiting; the misses
+ * are counted in the cache (ss_dev_cache_miss_counts).  L->miss_dev holds
+ * each unit's miss rows at row u*k.  events as for ss_decode_layer
+ * (events[7p+0..2] on the stream that runs group p's scoring;
+ * events[7p+2] after the resolve).  The block cache's regions must be laid
+ * out as ss_cache_region_offsets gives them for the same capacities. */
 ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache *cache, int64_t step, const void *q,
                               float *out, void *stream, void *const *events);
 
