@@ -183,7 +183,8 @@ def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_dive
         pool.close()
 
 
-def lockstep_with_save(oracle_impl, cfg, seed, sample_b, steps, parts=1, save_stream=False, meta_kind=0, agg=0):
+def lockstep_with_save(oracle_impl, cfg, seed, sample_b, steps, parts=1, save_stream=False, meta_kind=0, agg=0,
+                       dev_cache=False):
     """Decode steps that also append and save each step's new tokens
     (ss_append_kv, FlashD2H), so blocks fill during the run and become
     selectable; the oracle follows the sampled sequences on its own copy of
@@ -197,7 +198,8 @@ def lockstep_with_save(oracle_impl, cfg, seed, sample_b, steps, parts=1, save_st
           f"sampled {sample_b}, {parts} group(s), save stream {save_stream}", flush=True)
     pool = H.HostPool(total)
     try:
-        L = H.build_hier_layer(cfg, seed, 0, pool, 0, nblk, parts=parts, reserve=reserve, meta_kind=meta_kind, agg=agg)
+        L = H.build_hier_layer(cfg, seed, 0, pool, 0, nblk, parts=parts, reserve=reserve, meta_kind=meta_kind, agg=agg,
+                               dev_cache=dev_cache)
         L.enable_save(threads=2, save_stream=torch.cuda.Stream() if save_stream else None)
         sK, sV = synth.gen.channel_scales(cfg.Hkv, 128, seed, 0, "cuda")
         qs = H.query_stream(cfg, seed, 0, steps)
@@ -270,6 +272,21 @@ def test_hier_small_score_variants(ss, oracle_impl, kind, agg):
     """Whole decode steps with the mean-key metadata and the sum over the
     GQA group: selections, slots, misses, gathered bytes and attention."""
     lockstep(oracle_impl, SMALL, seed=14, sample_b=range(SMALL.B), steps=6, parts=2, meta_kind=kind, agg=agg)
+
+
+@pytest.mark.parametrize("save_stream", [False, True])
+def test_hier_small_with_append_and_save_device_resolve(ss, oracle_impl, save_stream):
+    """The save side with the cache resolved on the GPU: blocks filled by
+    appends enter the device block table (its room covers the reserve) and
+    are selected and gathered back."""
+    n = lockstep_with_save(oracle_impl, SAVE_SMALL, seed=16, sample_b=range(SAVE_SMALL.B), steps=40, parts=2,
+                           save_stream=save_stream, dev_cache=True)
+    assert n > 0
+
+
+def test_hier_ragged_with_append_and_save_device_resolve(ss, oracle_impl):
+    cfg = dataclasses.replace(synth.get(3), name="ragged-save-small-dev", B=4, ctx_range=(1024, 4096), k=16, layers=1)
+    lockstep_with_save(oracle_impl, cfg, seed=17, sample_b=range(cfg.B), steps=36, dev_cache=True)
 
 
 def test_hier_small_mean_metadata_with_save(ss, oracle_impl):
