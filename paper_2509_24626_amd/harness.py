@@ -243,9 +243,12 @@ class HierLayer:
 
 
 def cache_capacity(cfg, nblk):
-    """Slots per unit: floor(cache_frac * blocks of the sequence)."""
-    per_seq = np.floor(cfg.cache_frac * np.asarray(nblk, np.float64)).astype(np.int32)
-    return np.repeat(per_seq, cfg.Hkv)
+    """Slots per unit: floor(cache_frac * blocks of the sequence), and never
+    fewer than one step's selection, min(k, blocks), which attention needs in
+    HBM at once (short sequences only; every benchmark sequence has more)."""
+    n = np.asarray(nblk, np.int64)
+    per_seq = np.maximum(np.floor(cfg.cache_frac * n.astype(np.float64)).astype(np.int64), np.minimum(cfg.k, n))
+    return np.repeat(per_seq.astype(np.int32), cfg.Hkv)
 
 
 def pool_layout(cfg, nblk, reserve=0):

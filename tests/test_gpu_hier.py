@@ -153,10 +153,11 @@ class Track:
 
 
 def lockstep(oracle_impl, cfg, seed, sample_b, steps, layer=0, flags=0, max_diverged_frac=0.25, parts=1, meta_kind=0,
-             agg=0, dev_cache=False):
+             agg=0, dev_cache=False, nblk=None):
     from paper_2509_24626_amd import harness as H
-    lens = synth.gen.lengths(cfg, seed)
-    nblk = (lens // cfg.blk).astype(np.int32)
+    if nblk is None:
+        nblk = (synth.gen.lengths(cfg, seed) // cfg.blk).astype(np.int32)
+    nblk = np.asarray(nblk, np.int32)
     off, total = H.pool_layout(cfg, nblk)
     print(f"[gpu] {cfg.name}: pool {total / 2**30:.2f} GiB, sampled sequences {sample_b}, {parts} group(s)",
           flush=True)
@@ -329,6 +330,15 @@ def test_hier_many_units_one_group_device_resolve(ss, oracle_impl):
     per-unit miss rows sums the units' counts in two LDS chunks (1024 + 128)."""
     cfg = dataclasses.replace(SMALL, name="hier-many-units-b72-h16", B=72, Hq=32, Hkv=16, ctx=1024, k=8, steps=4)
     lockstep(oracle_impl, cfg, seed=9, sample_b=[0, 35, 64, 71], steps=4, parts=1, dev_cache=True)
+
+
+@pytest.mark.parametrize("dev_cache", [False, True])
+def test_hier_empty_and_short_sequences(ss, oracle_impl, dev_cache):
+    """A sequence with no blocks, ones with fewer blocks than k (padded
+    selections, every block selected) and a longer one, in two groups."""
+    cfg = dataclasses.replace(SMALL, name="hier-empty-short", B=5, k=8)
+    lockstep(oracle_impl, cfg, seed=21, sample_b=range(cfg.B), steps=5, parts=2, dev_cache=dev_cache,
+             nblk=[0, 3, 40, 1, 90])
 
 
 def test_hier_gqa7_small_device_resolve(ss, oracle_impl):
