@@ -114,6 +114,15 @@ def test_gqa7_shape_k512(ss, oracle_impl):
     run_stream(ss, oracle_impl, nblk, 4, 512, cap, 10, 0.5, seed=14)
 
 
+def test_largest_capacity_and_k(ss, oracle_impl):
+    """8192 slots (the largest supported region, every LDS array full) and
+    k = 512 with full churn: the cache fills after 16 steps, then every step
+    evicts 512 of 8192 candidates."""
+    nblk = np.array([16384, 12000], np.int32)
+    cap = np.full(2 * 2, 8192, np.int32)
+    run_stream(ss, oracle_impl, nblk, 2, 512, cap, 24, 1.0, seed=15)
+
+
 def test_error_flags_leave_units_unchanged(ss, oracle_impl):
     B, Hkv, k = 2, 1, 4
     nblk = np.array([20, 20], np.int32)
