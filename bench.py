@@ -242,6 +242,12 @@ def main():
             pipe["link_gaps"].append(last - first - busy)
             pipe["tail"].append(e[0].elapsed_time(e[7 * (P - 1) + 6]) - last)
     pipe = {k: round(float(np.mean(v)), 4) for k, v in pipe.items()}
+    # each step on its own: from the first layer's first event to the last
+    # layer's last (GPU time; the wall-clock mean above includes host time
+    # between steps)
+    step_ms = np.array([ev[i][0][0].elapsed_time(ev[i][-1][7 * (P - 1) + 6]) for i in range(steps)])
+    step_stats = {"median": round(float(np.median(step_ms)), 4), "min": round(float(step_ms.min()), 4),
+                  "max": round(float(step_ms.max()), 4), "p90": round(float(np.percentile(step_ms, 90)), 4)}
     units = cfg.B * cfg.Hkv
     # the gather's algorithmic bytes per step: the missed block records (mean
     # over the timed steps) over the host link, against the link's busy time
@@ -309,6 +315,7 @@ def main():
                    "seed": args.seed, "resolve": args.resolve},
         "roofline": dict(kernel=dominant, **roof[dominant]),
         "pipeline_ms": pipe,
+        "step_ms_events": step_stats,
         "rooflines_isolated": iso,
         "parts": layers[0].part_sizes,
         "miss_rate": round(miss_rate, 4),
