@@ -436,6 +436,19 @@ ss_status ss_cache_resolve_range(ss_cache *c, int64_t step, int b_begin, int b_e
         }
     }
     const int nt = std::min(c->threads, workers.size());
+    // the workers' scratch (touched slots, slot bitmap) at full size up front:
+    // nothing may allocate, and so throw, inside a worker thread
+    try {
+        int32_t cap_max = 0;
+        for (int u = u0; u < u0 + units; ++u) cap_max = std::max(cap_max, c->units[u].cap);
+        const size_t words = ((size_t)cap_max + 63) / 64;
+        for (int w = 0; w < nt; ++w) {
+            c->touched[w].reserve((size_t)k + (size_t)cap_max);
+            if (c->mark[w].size() < words) c->mark[w].resize(words);
+        }
+    } catch (const std::bad_alloc &) {
+        return ss::fail(SS_ERR_OOM, "ss_cache_resolve: out of memory");
+    }
     // pass 1 (parallel, read-only): validate and count misses per unit
     std::atomic<int> bad_unit{-1}, bad_kind{0};
     workers.run([&](int w) {

@@ -19,6 +19,7 @@
 // a kernel on a compute queue: no copy-engine transfer, whose cross-engine
 // synchronisation costs tens of microseconds per hand-off, is on the path.
 #include <mutex>
+#include <new>
 #include <thread>
 #include <unordered_map>
 #include <vector>
@@ -77,7 +78,8 @@ ss_status get_exec(int parts, exec_state **out)
     if ((st = hip_check(hipGetDevice(&dev), "hipGetDevice"))) return st;
     exec_state *&e = g_exec[dev];
     if (!e) {
-        exec_state *n = new exec_state;
+        exec_state *n = new (std::nothrow) exec_state;
+        if (!n) return ss::fail(SS_ERR_OOM, "ss_decode_layer: out of memory");
         if ((st = hip_check(hipStreamCreateWithFlags(&n->xfer[0], hipStreamNonBlocking), "create transfer stream")) ||
             (st = hip_check(hipStreamCreateWithFlags(&n->xfer[1], hipStreamNonBlocking), "create transfer stream")) ||
             (st = hip_check(hipEventCreateWithFlags(&n->start, hipEventDisableTiming), "create event"))) {
@@ -95,6 +97,14 @@ ss_status get_exec(int parts, exec_state **out)
         if ((st = hip_check(hipEventCreateWithFlags(&b, hipEventDisableTiming), "create event"))) {
             (void)hipEventDestroy(a);
             return st;
+        }
+        try {
+            e->sel_ready.reserve(e->sel_ready.size() + 1);
+            e->gathered.reserve(e->gathered.size() + 1);
+        } catch (const std::bad_alloc &) {
+            (void)hipEventDestroy(a);
+            (void)hipEventDestroy(b);
+            return ss::fail(SS_ERR_OOM, "ss_decode_layer: out of memory");
         }
         e->sel_ready.push_back(a);
         e->gathered.push_back(b);

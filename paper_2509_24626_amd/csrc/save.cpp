@@ -20,6 +20,7 @@
 #include <deque>
 #include <memory>
 #include <mutex>
+#include <new>
 #include <thread>
 #include <vector>
 
@@ -161,7 +162,9 @@ ss_status ss_kv_saver_create(int B, int Hkv, int blk, int d, void *pool_host, co
                  staging_slots);
     SS_CHECK_ARG(threads >= 1 && threads <= 64, "ss_kv_saver_create: threads=%d (1..64)", threads);
     for (int b = 0; b < B; ++b) SS_CHECK_ARG(pool_blocks[b] >= 0, "ss_kv_saver_create: pool_blocks[%d] < 0", b);
-    auto *sv = new ss_kv_saver;
+    auto *sv = new (std::nothrow) ss_kv_saver;
+    if (!sv) return ss::fail(SS_ERR_OOM, "ss_kv_saver_create: out of memory");
+    try {
     sv->B = B;
     sv->Hkv = Hkv;
     sv->blk = blk;
@@ -181,6 +184,10 @@ ss_status ss_kv_saver_create(int B, int Hkv, int blk, int d, void *pool_host, co
     sv->staging.assign(staging_slots, nullptr);
     sv->copied.assign(staging_slots, std::vector<hipEvent_t>(kMaxChunks, nullptr));
     sv->busy.assign(staging_slots, false);
+    } catch (const std::bad_alloc &) {
+        delete sv;
+        return ss::fail(SS_ERR_OOM, "ss_kv_saver_create: out of memory");
+    }
     for (int i = 0; i < staging_slots; ++i) {
         hipError_t e = hipHostMalloc(&sv->staging[i], sv->slot_bytes, hipHostMallocDefault);
         for (int c = 0; c < kMaxChunks && e == hipSuccess; ++c)
@@ -191,7 +198,12 @@ ss_status ss_kv_saver_create(int B, int Hkv, int blk, int d, void *pool_host, co
             return ss::fail(SS_ERR_OOM, "ss_kv_saver_create: staging buffer or event: %s", hipGetErrorString(e));
         }
     }
-    for (int i = 0; i < threads; ++i) sv->workers.emplace_back([sv] { sv->worker(); });
+    try {
+        for (int i = 0; i < threads; ++i) sv->workers.emplace_back([sv] { sv->worker(); });
+    } catch (const std::exception &) {
+        delete sv;  // joins the workers already started
+        return ss::fail(SS_ERR_OOM, "ss_kv_saver_create: could not start %d threads", threads);
+    }
     *out = sv;
     ss::clear_error();
     return SS_OK;
@@ -213,14 +225,15 @@ ss_status ss_kv_save(ss_kv_saver *sv, const void *new_kv, int n_new, const int32
     SS_CHECK_ARG(n_new >= 0 && n_new <= sv->max_new, "ss_kv_save: n_new=%d (0..%d)", n_new, sv->max_new);
     if (n_new == 0) return SS_OK;
     SS_CHECK_ARG(new_kv, "ss_kv_save: null new_kv");
-    for (int b = 0; b < sv->B; ++b) {
-        SS_CHECK_ARG(len[b] >= 0, "ss_kv_save: len[%d] < 0", b);
-        SS_CHECK_ARG((int64_t)(len[b] + n_new - 1) / sv->blk < sv->to->pool_blocks[b],
-                     "ss_kv_save: sequence %d: token %d lies past its %d pool blocks", b, len[b] + n_new - 1,
-                     sv->to->pool_blocks[b]);
-    }
     const hipStream_t s = ss::as_stream(stream);
     std::unique_lock<std::mutex> lk(sv->mu);
+    const std::shared_ptr<const target> to = sv->to;  // ss_kv_saver_retarget swaps it under the lock
+    for (int b = 0; b < sv->B; ++b) {
+        SS_CHECK_ARG(len[b] >= 0, "ss_kv_save: len[%d] < 0", b);
+        SS_CHECK_ARG((int64_t)(len[b] + n_new - 1) / sv->blk < to->pool_blocks[b],
+                     "ss_kv_save: sequence %d: token %d lies past its %d pool blocks", b, len[b] + n_new - 1,
+                     to->pool_blocks[b]);
+    }
     if (sv->error != SS_OK) return ss::fail(sv->error, "%s", sv->error_msg.c_str());
     const int slot = sv->next;
     sv->wait_locked(lk, slot);  // its previous scatter must be finished
@@ -246,11 +259,17 @@ ss_status ss_kv_save(ss_kv_saver *sv, const void *new_kv, int n_new, const int32
             return ss::fail(SS_ERR_HIP, "ss_kv_save: copy to staging: %s", hipGetErrorString(e));
         }
     }
-    job *jb = new job;
+    job *jb = new (std::nothrow) job;
+    if (!jb) return ss::fail(SS_ERR_OOM, "ss_kv_save: out of memory");
+    try {
+        jb->len.assign(len, len + sv->B);
+    } catch (const std::bad_alloc &) {
+        delete jb;
+        return ss::fail(SS_ERR_OOM, "ss_kv_save: out of memory");
+    }
     jb->slot = slot;
     jb->n_new = n_new;
-    jb->len.assign(len, len + sv->B);
-    jb->to = sv->to;
+    jb->to = to;
     jb->chunks_left.store(n_chunks);
     sv->busy[slot] = true;
     ++sv->in_flight;
