@@ -100,11 +100,28 @@ ss_status ss_ws_observe(ss_ws *t, int layer, int64_t step, const int64_t *req_id
         }
         t->k = k;
         const int w = t->w, Hkv = t->Hkv;
+        // every allocation on this thread (a worker thread must not throw):
+        // the workers find each unit's largest block index, then the rings and
+        // counts that need room get it here
+        std::vector<int32_t> hi((size_t)B * Hkv);
+        ss::parallel_for((int64_t)B * Hkv, 16, [&](int64_t u0, int64_t u1) {
+            for (int64_t u = u0; u < u1; ++u) {
+                int32_t m = -1;
+                for (int i = 0; i < k; ++i) m = std::max(m, sel[u * k + i]);
+                hi[u] = m;
+            }
+        });
+        for (int64_t u = 0; u < (int64_t)B * Hkv; ++u) {
+            const int b = (int)(u / Hkv), g = (int)(u - (int64_t)b * Hkv);
+            unit_ws &st = rq[b]->units[(size_t)layer * Hkv + g];
+            if (st.ring.empty()) st.ring.assign((size_t)w * k, -1);
+            if (hi[u] >= 0 && (size_t)hi[u] >= st.count.size())
+                st.count.resize(std::max<size_t>((size_t)hi[u] + 1, st.count.size() * 2), 0);
+        }
         ss::parallel_for((int64_t)B * Hkv, 16, [&](int64_t u0, int64_t u1) {
             for (int64_t u = u0; u < u1; ++u) {
                 const int b = (int)(u / Hkv), g = (int)(u - (int64_t)b * Hkv);
                 unit_ws &st = rq[b]->units[(size_t)layer * Hkv + g];
-                if (st.ring.empty()) st.ring.assign((size_t)w * k, -1);
                 int32_t *row = st.ring.data() + (size_t)st.head * k;
                 if (st.held == w)  // the oldest observation leaves the window
                     for (int i = 0; i < k; ++i)
@@ -114,8 +131,6 @@ ss_status ss_ws_observe(ss_ws *t, int layer, int64_t step, const int64_t *req_id
                     const int32_t j = s[i];
                     row[i] = j;
                     if (j < 0) continue;
-                    if ((size_t)j >= st.count.size())
-                        st.count.resize(std::max<size_t>((size_t)j + 1, st.count.size() * 2), 0);
                     if (st.count[j]++ == 0) ++st.size;
                 }
                 st.head = (st.head + 1) % w;
