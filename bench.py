@@ -70,7 +70,8 @@ def parse():
     ap.add_argument("--save-stream", choices=["own", "main"], default="own",
                     help="with --with-save: the FlashD2H copies on a stream of their own or on the main stream")
     ap.add_argument("--no-variants", action="store_true", help="skip the scoring-variant comparison")
-    ap.add_argument("--no-working-set", action="store_true", help="skip the working-set study")
+    ap.add_argument("--no-working-set", action="store_true",
+                    help="skip the working-set study and the batch-control comparison (Algorithm 1)")
     ap.add_argument("--no-prefill", action="store_true", help="skip the layer-segmented prefill measurement")
     ap.add_argument("--no-save-bandwidth", action="store_true",
                     help="skip the transfer comparisons: saving (FlashD2H, per-block copies, GPU-direct) and "
@@ -279,6 +280,11 @@ def main():
     if new_kv is None and cfg.layers == 1 and not args.no_working_set:
         ws_study = working_set_study(cfg, layers[0], qstreams[0][-1][0], warmup + steps, args.seed, ss, torch)
 
+    # ------------------------------------------- batch control (Algorithm 1)
+    batch_ctl = None
+    if new_kv is None and cfg.layers == 1 and not args.no_working_set:
+        batch_ctl = batch_control_study(cfg, layers[0], pool, ss, torch, H, args.seed)
+
     # ------------------------------------------- scoring variants
     variants = None
     if new_kv is None and cfg.layers == 1 and not args.no_variants:
@@ -339,6 +345,8 @@ def main():
         result["load_comparison"] = load_cmp
     if ws_study is not None:
         result["working_set"] = ws_study
+    if batch_ctl is not None:
+        result["batch_control"] = batch_ctl
     if variants is not None:
         result["score_variants"] = variants
     if prefill is not None:
@@ -589,7 +597,7 @@ def working_set_study(cfg, L, q32, first_step, seed, ss, torch, steps=28, window
             q32, q = gen.drift(q32, cfg.drift, seed, 0, first_step + i)
             L.step(first_step + i, q)
             torch.cuda.synchronize()
-            sel = L.sel_h.numpy().copy()
+            sel = L.sel.cpu().numpy()  # the device copy: both resolve paths write it
             hist.append(sel)
             t0 = time.perf_counter()
             ss.ss_ws_observe(tr, 0, first_step + i, ids, sel)
@@ -625,6 +633,73 @@ def working_set_study(cfg, L, q32, first_step, seed, ss, torch, steps=28, window
            "overlap_with_preceding_window": overlap, "steps": steps}
     log(f"working sets: {res}")
     return res
+
+
+def batch_control_study(cfg, L, pool, ss, torch, H, seed, window=12, fill=16, timed=8, budget_frac=0.5):
+    """Working-set-aware batch control (Section 3.3, Algorithm 1) with the
+    decode step itself.  The batch's decoding working sets (window 12) are
+    estimated from `window` steps of the whole batch on this layer; the HBM
+    budget for the block caches is then set to `budget_frac` of their sum.
+    Two runs share that budget, split evenly over the running requests'
+    (sequence, KV head) units:
+      no_control  every request runs; each unit gets budget / (B * Hkv)
+                  slots, fewer than its working set
+      alg1        the requests Algorithm 1 admits run; each unit gets
+                  budget / (admitted * Hkv) slots
+    Each run starts from an empty cache, fills it over `fill` steps and
+    times `timed` more (the same drifting queries for both); misses come
+    from the GPU resolve's own count.  The layer's DRAM records and
+    metadata are shared, so the study allocates only the caches."""
+    import dataclasses
+    B, Hkv, k, rb = cfg.B, cfg.Hkv, cfg.k, cfg.record_bytes
+    qs = H.query_stream(cfg, seed + 7, 0, window + fill + timed)
+    ids = np.arange(B, dtype=np.int64)
+    first = 1 << 20  # step numbers after any the layer's cache has seen
+    tr = ss.ss_ws_create(1, Hkv, window, rb)
+    try:
+        for t in range(window):
+            L.step(first + t, qs[t][1])
+            torch.cuda.synchronize()
+            ss.ss_ws_observe(tr, 0, t, ids, L.sel.cpu().numpy())
+        ws = ss.ss_ws_decode_bytes(tr, ids)
+    finally:
+        ss.ss_ws_destroy(tr)
+    budget = int(budget_frac * ws.sum())
+    admit, used = ss.ss_schedule_batch(ws, budget)
+    out = {"window": window, "ws_bytes_total": int(ws.sum()), "budget_bytes": budget,
+           "admitted": int(admit.sum()), "fill_steps": fill, "timed_steps": timed}
+    for name, idx in (("no_control", np.arange(B)), ("alg1", np.nonzero(admit)[0])):
+        n = len(idx)
+        if n == 0:
+            out[name] = None
+            continue
+        nb = L.nblk_host[idx]
+        slots = np.minimum(np.maximum(budget // (n * Hkv * rb), np.minimum(k, nb)), nb)
+        units = (idx[:, None] * Hkv + np.arange(Hkv)).reshape(-1)
+        meta = L.meta if n == B else L.meta[torch.from_numpy(idx).cuda()].contiguous()
+        parts = H.ramp_parts(n) if n >= 40 else max(1, min(4, round(n / 5)))
+        Ln = H.HierLayer(dataclasses.replace(cfg, B=n), nb, np.repeat(slots, Hkv).astype(np.int32), pool,
+                         L.pool_off_host[units], meta, parts, dev_cache=True)
+        qi = torch.from_numpy(idx).cuda()
+        try:
+            for t in range(fill):
+                Ln.step(t, qs[window + t][1].index_select(0, qi))
+            torch.cuda.synchronize()
+            m0 = ss.ss_dev_cache_total_misses(Ln.dev)
+            t0 = time.perf_counter()
+            for t in range(fill, fill + timed):
+                Ln.step(t, qs[window + t][1].index_select(0, qi))
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - t0
+            m = ss.ss_dev_cache_total_misses(Ln.dev) - m0
+        finally:
+            Ln.close()
+        out[name] = {"requests": n, "slots_per_head": int(slots.min()), "cache_bytes": int(slots.sum()) * Hkv * rb,
+                     "miss_rate": round(m / (timed * n * Hkv * k), 4),
+                     "block_loads_per_step": round(m / timed, 1),
+                     "ms_per_step": round(wall / timed * 1e3, 4), "tokens_per_s": round(n * timed / wall, 1)}
+    log(f"batch control: {out}")
+    return out
 
 
 def prefill_study(ss, torch, H, T=131072, layers=8, Hkv=8, blk=16):
