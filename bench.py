@@ -373,13 +373,13 @@ KERNEL_SOURCES = {
 # hierarchical 128k-context layer, seed 0, 16 timed steps after 1 warm-up, groups 2,9,22,20,9,2
 _KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 16, 1, [2, 4, 10, 20, 18, 8, 2], "device"]
 TRAFFIC = {
-    "gather": {"key": _KEY, "digest": "57cfeae87f2b8a7e", "bytes": 260209184, "fetch": 131075104,
+    "gather": {"key": _KEY, "digest": "b6afd93dae4c85a6", "bytes": 260092459, "fetch": 130958379,
               "write": 129134080},
-    "score": {"key": _KEY, "digest": "b1d34d18dc71bc7d", "bytes": 2169883160, "fetch": 2152019672,
-              "write": 17863488},
+    "score": {"key": _KEY, "digest": "b1d34d18dc71bc7d", "bytes": 2169869272, "fetch": 2152047768,
+              "write": 17821504},
     "topk": {"key": _KEY, "digest": "2b36a2d12fb03589", "bytes": 17254011, "fetch": 16991867,
               "write": 262144},
-    "attention": {"key": _KEY, "digest": "f6b1e88a61a963de", "bytes": 539113957, "fetch": 538065381,
+    "attention": {"key": _KEY, "digest": "f6b1e88a61a963de", "bytes": 539111333, "fetch": 538062757,
               "write": 1048576},
 }
 
