@@ -122,13 +122,7 @@ def main():
         f"pool {per_layer * n_distinct / 2**30:.2f} GiB pinned")
     meta_ms = []
     if args.parts == "auto":
-        # per-group costs (a top-k launch, a host resolve, launches) favour few
-        # groups for small batches: equal groups of about 5 sequences; large
-        # batches get seven groups that grow while the pipeline fills
-        if cfg.B >= 40:
-            parts = H.ramp_parts(cfg.B)
-        else:
-            parts = max(1, min(4, round(cfg.B / 5)))
+        parts = H.default_parts(cfg.B)
     elif args.parts.startswith("tent"):
         parts = H.tent_parts(cfg.B, int(args.parts[4:]))
     elif "," in args.parts:

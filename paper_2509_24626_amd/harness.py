@@ -293,6 +293,15 @@ def ramp_parts(B, weights=(1, 2, 5, 10, 9, 4, 1)):
     return [int(x) for x in sizes]
 
 
+def default_parts(B):
+    """The decode step's automatic sequence groups: seven ramp-shaped groups
+    for batches of 40 or more, otherwise equal groups of about 5 sequences
+    (per-group costs, a top-k launch and a resolve, favour few groups)."""
+    if B >= 40:
+        return ramp_parts(B)
+    return max(1, min(4, round(B / 5)))
+
+
 def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None, parts=1, reserve=0, meta_kind=0,
                      agg=0, dev_cache=False):
     """Draws one layer's KV per sequence on the GPU, builds its metadata in

@@ -347,9 +347,11 @@ def test_hier_gqa7_small_device_resolve(ss, oracle_impl):
 
 
 def test_hier_128k_full_size_device_resolve_sampled(ss, oracle_impl):
-    """The 128k workload at full size with the device resolve (6 groups)."""
+    """The 128k workload at full size in the launch configuration bench.py
+    times: the resolve on the GPU and the automatic groups."""
+    from paper_2509_24626_amd import harness as H
     cfg = synth.get(2)
-    lockstep(oracle_impl, cfg, seed=0, sample_b=[1, 33, 62], steps=cfg.steps, parts=[2, 9, 22, 20, 9, 2],
+    lockstep(oracle_impl, cfg, seed=0, sample_b=[1, 33, 62], steps=cfg.steps, parts=H.default_parts(cfg.B),
              dev_cache=True)
 
 
@@ -369,17 +371,29 @@ def test_hier_gqa7_full_size_sampled(ss, oracle_impl):
     lockstep(oracle_impl, cfg, seed=0, sample_b=[0, 47], steps=cfg.steps, parts=6)
 
 
+def test_hier_gqa7_full_size_device_resolve_sampled(ss, oracle_impl):
+    """The GQA-7 workload at full size in the launch configuration bench.py
+    times (the resolve on the GPU, the automatic groups)."""
+    from paper_2509_24626_amd import harness as H
+    cfg = synth.get(4)
+    lockstep(oracle_impl, cfg, seed=0, sample_b=[3, 30], steps=cfg.steps, parts=H.default_parts(cfg.B),
+             dev_cache=True)
+
+
 def test_layers32_ragged_full_size_sampled(ss, oracle_impl):
     """The 32-layer ragged workload at full size (B=16, lengths U[8k, 64k],
     k=128, 30% cache per layer, 8 drifting steps): every step runs all 32
     layers in order; the oracle follows 2 sequences in each of 4 layers,
-    two of which read DRAM records shared with an earlier layer."""
+    two of which read DRAM records shared with an earlier layer.  The launch
+    configuration is the one bench.py times: the resolve on the GPU and the
+    automatic groups."""
     from paper_2509_24626_amd import harness as H
     cfg = synth.get(3)
     seed = 0
     nblk = (synth.gen.lengths(cfg, seed) // cfg.blk).astype(np.int32)
     log = lambda m: print("[gpu]", m, flush=True)
-    pool, layers, n = H.build_hier_model(cfg, seed, nblk, progress=log, parts=H.tent_parts(cfg.B, 4))
+    pool, layers, n = H.build_hier_model(cfg, seed, nblk, progress=log, parts=H.default_parts(cfg.B),
+                                         dev_cache=True)
     try:
         print(f"[gpu] {cfg.name}: {n} of {cfg.layers} layers with their own DRAM records", flush=True)
         assert n < cfg.layers  # the 32 layers do not fit the pinned budget
@@ -393,10 +407,11 @@ def test_layers32_ragged_full_size_sampled(ss, oracle_impl):
             torch.cuda.synchronize()
             for l, tr in tracks.items():
                 tr.check(t, qs[l][t][1])
-            rates = [L.last_n_miss / (L.units * cfg.k) for L in layers]
+            misses = [int(L.dev_miss_rows()[0].sum()) for L in layers]
+            rates = [m / (L.units * cfg.k) for m, L in zip(misses, layers)]
             print(f"[gpu] step {t}: miss rate over layers {min(rates):.3f}..{max(rates):.3f}", flush=True)
             if t == 0:
-                assert all(L.last_n_miss == sum(min(cfg.k, int(x)) for x in nblk) * cfg.Hkv for L in layers)
+                assert all(m == sum(min(cfg.k, int(x)) for x in nblk) * cfg.Hkv for m in misses)
         units = sum(len(tr.units) for tr in tracks.values())
         div = sum(len(tr.diverged) for tr in tracks.values())
         print(f"[gpu] diverged units {div}/{units}", flush=True)

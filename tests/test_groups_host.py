@@ -25,3 +25,9 @@ def test_ramp_parts_at_batch_64():
 def test_tent_parts_cover_the_batch(B, n):
     sizes = H.tent_parts(B, n)
     assert sum(sizes) == B and min(sizes) >= 1 and len(sizes) == min(n, B)
+
+
+def test_default_parts():
+    assert H.default_parts(64) == H.ramp_parts(64)
+    assert H.default_parts(48) == H.ramp_parts(48)
+    assert H.default_parts(16) == 3 and H.default_parts(2) == 1 and H.default_parts(39) == 4
