@@ -97,3 +97,27 @@ def test_attention_workspace_sizes():
 def test_host_alloc_rejects_bad_flags():
     expect(ss.SS_ERR_INVALID_ARG, ss.ss_host_alloc_mapped, 4096, 7)
     assert ss.ss_host_alloc_mapped(0) == (0, 0)
+
+
+def test_header_and_host_calls_from_plain_c(tmp_path):
+    """tests/c_abi_check.c, built as strict C99 against the in-tree library,
+    calls the host-only entry points; the header also parses as C++."""
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    inc = os.path.join(root, "include")
+    libdir = os.path.dirname(ss.LIB_PATH)
+    exe = str(tmp_path / "c_abi_check")
+    subprocess.run([cc, "-std=c99", "-Wall", "-Wextra", "-Werror", "-pedantic", "-I", inc,
+                    os.path.join(root, "tests", "c_abi_check.c"), "-o", exe, "-L", libdir, "-lsparseserve",
+                    "-Wl,-rpath," + libdir], check=True)
+    out = subprocess.run([exe], check=True, capture_output=True, text=True).stdout
+    assert "c abi ok" in out
+    cxx = shutil.which("g++")
+    if cxx:
+        src = tmp_path / "h.cpp"
+        src.write_text('#include "sparseserve.h"\nint main() { return ss_abi_version() == SS_ABI_VERSION ? 0 : 1; }\n')
+        subprocess.run([cxx, "-std=c++11", "-Wall", "-Werror", "-fsyntax-only", "-I", inc, str(src)], check=True)
