@@ -347,8 +347,8 @@ def test_hier_gqa7_small_device_resolve(ss, oracle_impl):
 
 
 def test_hier_128k_full_size_device_resolve_sampled(ss, oracle_impl):
-    """The 128k workload at full size in the launch configuration bench.py
-    times: the resolve on the GPU and the automatic groups."""
+    """The 128k workload at full size with the resolve on the GPU and the
+    automatic groups (bench.py --resolve device)."""
     from paper_2509_24626_amd import harness as H
     cfg = synth.get(2)
     lockstep(oracle_impl, cfg, seed=0, sample_b=[1, 33, 62], steps=cfg.steps, parts=H.default_parts(cfg.B),
@@ -358,42 +358,48 @@ def test_hier_128k_full_size_device_resolve_sampled(ss, oracle_impl):
 def test_hier_128k_full_size_sampled(ss, oracle_impl):
     """The hierarchical 128k-context workload at full size (B=64, 32/8
     heads, 8192 blocks of 16 tokens, k=128, 25% cache, 16 drifting steps
-    after the warm-up); the oracle follows 3 of the 64 sequences."""
+    after the warm-up) in the launch configuration bench.py times (the
+    host-side resolve, the automatic groups); the oracle follows 3 of the
+    64 sequences."""
+    from paper_2509_24626_amd import harness as H
     cfg = synth.get(2)
-    rate = lockstep(oracle_impl, cfg, seed=0, sample_b=[0, 31, 63], steps=cfg.steps, parts=8)
+    rate = lockstep(oracle_impl, cfg, seed=0, sample_b=[0, 31, 63], steps=cfg.steps, parts=H.default_parts(cfg.B))
     assert 0.05 < np.mean(rate[1:]) < 0.5
 
 
 def test_hier_gqa7_full_size_sampled(ss, oracle_impl):
     """The Qwen-like GQA-7 fragmentation workload at full size (B=48, 28/4
-    heads, 16384 blocks of 8 tokens, k=512, 15% cache, 8 steps)."""
+    heads, 16384 blocks of 8 tokens, k=512, 15% cache, 8 steps) in the
+    launch configuration bench.py times."""
+    from paper_2509_24626_amd import harness as H
     cfg = synth.get(4)
-    lockstep(oracle_impl, cfg, seed=0, sample_b=[0, 47], steps=cfg.steps, parts=6)
+    lockstep(oracle_impl, cfg, seed=0, sample_b=[0, 47], steps=cfg.steps, parts=H.default_parts(cfg.B))
 
 
 def test_hier_gqa7_full_size_device_resolve_sampled(ss, oracle_impl):
-    """The GQA-7 workload at full size in the launch configuration bench.py
-    times (the resolve on the GPU, the automatic groups)."""
+    """The GQA-7 workload at full size with the resolve on the GPU and the
+    automatic groups (bench.py --resolve device)."""
     from paper_2509_24626_amd import harness as H
     cfg = synth.get(4)
     lockstep(oracle_impl, cfg, seed=0, sample_b=[3, 30], steps=cfg.steps, parts=H.default_parts(cfg.B),
              dev_cache=True)
 
 
-def test_layers32_ragged_full_size_sampled(ss, oracle_impl):
+@pytest.mark.parametrize("dev_cache", [False, True])
+def test_layers32_ragged_full_size_sampled(ss, oracle_impl, dev_cache):
     """The 32-layer ragged workload at full size (B=16, lengths U[8k, 64k],
     k=128, 30% cache per layer, 8 drifting steps): every step runs all 32
     layers in order; the oracle follows 2 sequences in each of 4 layers,
-    two of which read DRAM records shared with an earlier layer.  The launch
-    configuration is the one bench.py times: the resolve on the GPU and the
-    automatic groups."""
+    two of which read DRAM records shared with an earlier layer.  The
+    automatic groups, with the resolve on host threads (bench.py's default)
+    and on the GPU."""
     from paper_2509_24626_amd import harness as H
     cfg = synth.get(3)
     seed = 0
     nblk = (synth.gen.lengths(cfg, seed) // cfg.blk).astype(np.int32)
     log = lambda m: print("[gpu]", m, flush=True)
     pool, layers, n = H.build_hier_model(cfg, seed, nblk, progress=log, parts=H.default_parts(cfg.B),
-                                         dev_cache=True)
+                                         dev_cache=dev_cache)
     try:
         print(f"[gpu] {cfg.name}: {n} of {cfg.layers} layers with their own DRAM records", flush=True)
         assert n < cfg.layers  # the 32 layers do not fit the pinned budget
@@ -407,7 +413,7 @@ def test_layers32_ragged_full_size_sampled(ss, oracle_impl):
             torch.cuda.synchronize()
             for l, tr in tracks.items():
                 tr.check(t, qs[l][t][1])
-            misses = [int(L.dev_miss_rows()[0].sum()) for L in layers]
+            misses = [L.last_n_miss if L.dev is None else int(L.dev_miss_rows()[0].sum()) for L in layers]
             rates = [m / (L.units * cfg.k) for m, L in zip(misses, layers)]
             print(f"[gpu] step {t}: miss rate over layers {min(rates):.3f}..{max(rates):.3f}", flush=True)
             if t == 0:
