@@ -370,13 +370,13 @@ KERNEL_SOURCES = {
 # hierarchical 128k-context layer, seed 0, 16 timed steps after 1 warm-up, groups 2,9,22,20,9,2
 _KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 16, 1, [2, 4, 10, 20, 18, 8, 2], "host"]
 TRAFFIC = {
-    "gather": {"key": _KEY, "digest": "b6afd93dae4c85a6", "bytes": 260484736, "fetch": 131088512,
+    "gather": {"key": _KEY, "digest": "b6afd93dae4c85a6", "bytes": 260479456, "fetch": 131083232,
               "write": 129396224},
-    "score": {"key": _KEY, "digest": "b1d34d18dc71bc7d", "bytes": 2169937783, "fetch": 2152085719,
-              "write": 17852064},
+    "score": {"key": _KEY, "digest": "b1d34d18dc71bc7d", "bytes": 2169861496, "fetch": 2152047576,
+              "write": 17813920},
     "topk": {"key": _KEY, "digest": "2b36a2d12fb03589", "bytes": 17254011, "fetch": 16991867,
               "write": 262144},
-    "attention": {"key": _KEY, "digest": "f6b1e88a61a963de", "bytes": 539117029, "fetch": 538068453,
+    "attention": {"key": _KEY, "digest": "275b5374d3e47ca9", "bytes": 545207897, "fetch": 544159321,
               "write": 1048576},
 }
 
