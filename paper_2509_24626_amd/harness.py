@@ -295,11 +295,14 @@ def ramp_parts(B, weights=(1, 2, 5, 10, 9, 4, 1)):
 
 def default_parts(B):
     """The decode step's automatic sequence groups: seven ramp-shaped groups
-    for batches of 40 or more, otherwise equal groups of about 5 sequences
-    (per-group costs, a top-k launch and a resolve, favour few groups)."""
+    for batches of 40 or more, four (weights 2, 3, 5, 6) for 8 to 39, and
+    otherwise one or two equal groups (per-group costs, a top-k launch and a
+    resolve, favour few groups)."""
     if B >= 40:
         return ramp_parts(B)
-    return max(1, min(4, round(B / 5)))
+    if B >= 8:
+        return ramp_parts(B, weights=(2, 3, 5, 6))
+    return max(1, min(2, round(B / 4)))
 
 
 def build_hier_layer(cfg, seed, layer, pool, pool_base_off, nblk, progress=None, parts=1, reserve=0, meta_kind=0,

@@ -30,4 +30,8 @@ def test_tent_parts_cover_the_batch(B, n):
 def test_default_parts():
     assert H.default_parts(64) == H.ramp_parts(64)
     assert H.default_parts(48) == H.ramp_parts(48)
-    assert H.default_parts(16) == 3 and H.default_parts(2) == 1 and H.default_parts(39) == 4
+    assert H.default_parts(16) == [2, 3, 5, 6] and H.default_parts(8) == [1, 2, 2, 3]
+    for B in range(8, 40):
+        sizes = H.default_parts(B)
+        assert len(sizes) == 4 and sum(sizes) == B and min(sizes) >= 1
+    assert H.default_parts(2) == 1 and H.default_parts(7) == 2 and H.default_parts(1) == 1
