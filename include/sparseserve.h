@@ -176,6 +176,9 @@ ss_status ss_select_topk(const float *scores, const int32_t *nblk, int B, int Hk
  * fp32 [B][Hkv][nblk_max] buffer and holds the scores afterwards. */
 ss_status ss_score_topk(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv,
                         int nblk_max, int d, int k, float *scores, int32_t *sel, void *stream);
+/* Bytes of the `scores` buffer ss_score_topk needs (B*Hkv*nblk_max fp32);
+ * 0 for invalid shapes.  Host-only. */
+size_t ss_score_topk_workspace(int B, int Hq, int Hkv, int nblk_max, int d, int k);
 
 /* ------------------------------------------------------------ block cache
  * The HBM tier of the KV cache manager (Section 3.1): per unit, a region of

@@ -64,6 +64,7 @@ _SIGNATURES = {
     "ss_cache_export": (_i32, [_vp, _vp, _vp]),
     "ss_gather_blocks": (_i32, [_vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _sz, _vp]),
     "ss_sparse_attention_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32]),
+    "ss_score_topk_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32]),
     "ss_sparse_attention": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
                                    _sz, _vp]),
     "ss_decode_layer": (_i32, [ctypes.POINTER(ss_layer_buffers), _i64, _vp, _vp, _vp, _vp, _vp]),
@@ -240,6 +241,10 @@ def ss_gather_blocks(miss, n_miss, pool_base, pool_off, cache_base, cache_off, n
 
 def ss_sparse_attention_workspace(B, Hq, Hkv, d, blk, k):
     return lib().ss_sparse_attention_workspace(B, Hq, Hkv, d, blk, k)
+
+
+def ss_score_topk_workspace(B, Hq, Hkv, nblk_max, d, k):
+    return int(lib().ss_score_topk_workspace(B, Hq, Hkv, nblk_max, d, k))
 
 
 def ss_sparse_attention(q, kv_base, region_off, slots, slot_limit, B, Hq, Hkv, d, blk, k, scale, out, workspace,

@@ -229,6 +229,12 @@ extern "C" ss_status ss_select_topk(const float *scores, const int32_t *nblk, in
     return ss::launch_topk(scores, nblk, B, Hkv, nblk_max, k, sel, nullptr, ss::as_stream(stream));
 }
 
+extern "C" size_t ss_score_topk_workspace(int B, int Hq, int Hkv, int nblk_max, int d, int k)
+{
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv || d != ss::kHeadDim || nblk_max < 0 || k <= 0) return 0;
+    return (size_t)B * Hkv * nblk_max * sizeof(float);
+}
+
 extern "C" ss_status ss_score_topk(const void *q, const void *meta, const int32_t *nblk, int B, int Hq, int Hkv,
                                    int nblk_max, int d, int k, float *scores, int32_t *sel, void *stream)
 {

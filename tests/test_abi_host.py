@@ -84,6 +84,13 @@ def test_empty_work_is_a_no_op():
     ss.ss_sparse_attention(None, None, None, None, 8, 0, 8, 2, 128, 16, 4, 0.1, None, None, 0, 0)
 
 
+def test_score_topk_workspace_sizes():
+    assert ss.ss_score_topk_workspace(64, 32, 8, 8192, 128, 128) == 64 * 8 * 8192 * 4
+    assert ss.ss_score_topk_workspace(0, 32, 8, 8192, 128, 128) == 0
+    assert ss.ss_score_topk_workspace(2, 30, 8, 100, 128, 8) == 0  # Hq not a multiple of Hkv
+    assert ss.ss_score_topk_workspace(2, 32, 8, 100, 64, 8) == 0   # d other than 128
+
+
 def test_attention_workspace_sizes():
     # split plan: several splits for few units, none for a single small unit
     assert ss.ss_sparse_attention_workspace(2, 8, 2, 128, 16, 16) == 0
