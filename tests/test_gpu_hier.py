@@ -464,3 +464,30 @@ def test_gather_bytes_and_range_checks(ss):
                 assert np.all(c[~written] == 0), (src_name, rb)
         finally:
             pool.close()
+
+
+def random_shapes(n, seed):
+    """Seeded small hierarchical configurations: batch, heads and group
+    size, block size, k, ragged lengths, cache fraction, group count and
+    the resolve path all vary."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for i in range(n):
+        Hkv = int(rng.choice([1, 2, 4, 8]))
+        G = int(rng.choice([1, 2, 4, 7, 16]))
+        blk = int(rng.choice([8, 16, 32]))
+        k = int(rng.choice([4, 16, 33, 64, 128]))
+        lo = int(rng.integers(1, 80)) * blk
+        hi = lo + int(rng.integers(0, 300)) * blk
+        B = int(rng.integers(1, 12))
+        cfg = Config(f"random-shape-{seed}-{i}", B=B, Hq=Hkv * G, Hkv=Hkv, d=128, blk=blk, k=k,
+                     ctx_range=(lo, hi), placement="host", cache_frac=float(rng.choice([0.1, 0.25, 0.6])),
+                     steps=3, drift=float(rng.choice([0.3, 0.8])))
+        parts = int(rng.integers(1, min(B, 4) + 1))
+        out.append((cfg, parts, bool(rng.integers(0, 2))))
+    return out
+
+
+@pytest.mark.parametrize("cfg,parts,dev_cache", random_shapes(20, 31), ids=lambda x: getattr(x, "name", str(x)))
+def test_hier_random_shapes(ss, oracle_impl, cfg, parts, dev_cache):
+    lockstep(oracle_impl, cfg, seed=7, sample_b=range(cfg.B), steps=cfg.steps, parts=parts, dev_cache=dev_cache)
