@@ -39,6 +39,28 @@ CASES = {
     "k-above-blocks": (2, 8, 2, 16, 20, 32, 0, [20, 13]),
 }
 
+
+
+def _random_cases(n, seed):
+    """Seeded extra shapes: heads and group size (1 to 16), block size,
+    nblk_max, k (1 to 200, often above some sequences' block counts) and
+    ragged block counts, empty sequences included."""
+    rng = np.random.default_rng(seed)
+    out = {}
+    for i in range(n):
+        Hkv = int(rng.choice([1, 2, 4, 8]))
+        G = int(rng.choice([1, 2, 4, 7, 16]))
+        blk = int(rng.choice([8, 16, 32]))
+        nmax = int(rng.integers(1, 700))
+        k = int(rng.choice([1, 5, 16, 64, 200]))
+        B = int(rng.integers(1, 6))
+        nblk = [int(x) for x in rng.integers(0, nmax + 1, size=B)]
+        out[f"random-{seed}-{i}"] = (B, Hkv * G, Hkv, blk, nmax, k, 0, nblk)
+    return out
+
+
+CASES.update(_random_cases(8, 17))
+
 _cache = {}
 
 
