@@ -368,16 +368,16 @@ KERNEL_SOURCES = {
     "topk": ["topk.hip"],
     "attention": ["attention.hip"],
 }
-# hierarchical 128k-context layer, seed 0, 16 timed steps after 1 warm-up, groups 2,9,22,20,9,2
+# hierarchical 128k-context layer, seed 0, 16 timed steps after 1 warm-up, groups 2,4,10,20,18,8,2, host resolve
 _KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 16, 1, [2, 4, 10, 20, 18, 8, 2], "host"]
 TRAFFIC = {
-    "gather": {"key": _KEY, "digest": "b6afd93dae4c85a6", "bytes": 260479456, "fetch": 131083232,
+    "gather": {"key": _KEY, "digest": "b6afd93dae4c85a6", "bytes": 260478744, "fetch": 131082520,
               "write": 129396224},
-    "score": {"key": _KEY, "digest": "b1d34d18dc71bc7d", "bytes": 2169861496, "fetch": 2152047576,
-              "write": 17813920},
-    "topk": {"key": _KEY, "digest": "2b36a2d12fb03589", "bytes": 17254011, "fetch": 16991867,
+    "score": {"key": _KEY, "digest": "b1d34d18dc71bc7d", "bytes": 2169859159, "fetch": 2152070231,
+              "write": 17788928},
+    "topk": {"key": _KEY, "digest": "1a1ad0e4eb4df940", "bytes": 17254011, "fetch": 16991867,
               "write": 262144},
-    "attention": {"key": _KEY, "digest": "275b5374d3e47ca9", "bytes": 545207897, "fetch": 544159321,
+    "attention": {"key": _KEY, "digest": "275b5374d3e47ca9", "bytes": 545243736, "fetch": 544195160,
               "write": 1048576},
 }
 
