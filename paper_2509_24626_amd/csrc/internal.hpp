@@ -50,14 +50,22 @@ void set_kernel_timing(hipEvent_t start, hipEvent_t stop);
 // Launches `k`, attaching this thread's pending timing events, if any, to
 // the dispatch itself, so they bracket the kernel's execution and not the
 // queue's dispatch latency.
+// `lds` bytes of dynamic LDS are allocated per workgroup on top of the
+// kernel's static LDS.
 template <typename... P, typename... A>
-inline void launch(void (*k)(P...), dim3 grid, dim3 block, hipStream_t s, A... args)
+inline void launch_lds(void (*k)(P...), dim3 grid, dim3 block, size_t lds, hipStream_t s, A... args)
 {
     const kernel_timing t = take_kernel_timing();
     if (t.start || t.stop)
-        hipExtLaunchKernelGGL(k, grid, block, 0, s, t.start, t.stop, 0, static_cast<P>(args)...);
+        hipExtLaunchKernelGGL(k, grid, block, lds, s, t.start, t.stop, 0, static_cast<P>(args)...);
     else
-        k<<<grid, block, 0, s>>>(static_cast<P>(args)...);
+        k<<<grid, block, lds, s>>>(static_cast<P>(args)...);
+}
+
+template <typename... P, typename... A>
+inline void launch(void (*k)(P...), dim3 grid, dim3 block, hipStream_t s, A... args)
+{
+    launch_lds(k, grid, block, 0, s, args...);
 }
 
 }  // namespace ss

@@ -15,6 +15,12 @@
 // Every MFMA B fragment is a direct 16-byte load of one metadata row, so the
 // 512-byte rows stream from HBM with no LDS staging and no cross-lane
 // reduction; the head maximum is taken over accumulator registers.
+//
+// The launch reserves LDS that the kernel never touches (kResidencyLds), so
+// that at most two workgroups (8 waves) share a CU: on MI355X the 128k-token
+// batch streams at 0.765 of the 8 TB/s peak that way, against 0.73 with the
+// eight workgroups per CU the registers allow, 0.75 with three and 0.69 with
+// one.
 #include "internal.hpp"
 
 namespace {
@@ -24,6 +30,10 @@ constexpr int TILE = 16;              // blocks per MFMA tile
 constexpr int WAVES = 4;
 constexpr int TILES_PER_WAVE = 4;
 constexpr int BLOCKS_PER_WG = TILE * WAVES * TILES_PER_WAVE;  // 256
+// 2 x 60 KiB fit in a CU's 160 KiB of LDS and 3 do not; the 40 KiB left over
+// still take one attention workgroup (34 KiB) beside two scoring workgroups
+constexpr size_t kResidencyLds = 60 * 1024;
+constexpr int kBufferFlags = 0x00020000;  // raw buffer descriptor word 3 for gfx9 (32-bit data)
 
 union frag_t {
     bf16x8_t v;
@@ -31,14 +41,15 @@ union frag_t {
     uint16_t h[8];
 };
 
-// Lane (L = lane/16, col = lane%16) takes 16-byte chunks c = L*NCH + m of a
-// metadata row for the NCH MFMAs m of a tile: each lane streams NCH*16
-// contiguous bytes of its row.  (A mapping where each load instruction
-// covers a contiguous 64-byte piece of every row instead measured 6% slower
-// on MI355X.)  The A fragments hold the matching weights of head `col`.
+// Lane (L = lane/16, col = lane%16) takes 16-byte chunk c = 4*m + L of a
+// metadata row for MFMA m of a tile, so each load instruction covers one
+// contiguous 64-byte piece of each of the tile's 16 rows.  (Each lane
+// streaming NCH*16 contiguous bytes of its row instead measured 1.5% slower
+// through buffer loads.)  The A fragments hold the matching weights of head
+// `col`.
 //
 // KIND 0, cuboid rows [lo, hi] (512 B, NCH = 8): chunks 0..15 are lo and
-// multiply min(q, 0), chunks 16..31 are hi and multiply max(q, 0).
+// multiply min(q, 0), chunks 16..31 (m >= 4) are hi and multiply max(q, 0).
 // KIND 1, mean-key rows (256 B, NCH = 4): each chunk multiplies q itself.
 // AGG 0 takes the maximum over the group's heads, AGG 1 their sum.
 template <int KIND, int AGG>
@@ -69,10 +80,10 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__
         const bool live = col < G;
         const uint16_t *qh = q + ((int64_t)b * Hq + g * G + (live ? col : 0)) * D;
         const uint32_t live_mask = live ? 0xFFFFFFFFu : 0u;
-        const bool hi_half = KIND == 0 && L >= 2;  // cuboid chunks 16..31 (L >= 2) multiply hi
 #pragma unroll
         for (int m = 0; m < NCH; ++m) {
-            const int c = (L * NCH + m) & 15;  // q channels c*8 .. c*8+7
+            const bool hi_half = KIND == 0 && m >= 4;  // cuboid chunks 16..31 multiply hi
+            const int c = (4 * m + L) & 15;            // q channels c*8 .. c*8+7
             const uint4 x = *reinterpret_cast<const uint4 *>(qh + c * 8);
             uint32_t v[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
@@ -90,16 +101,18 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__
 
     const uint8_t *mu = meta + (int64_t)u * nblk_max * ROW;
     float *su = scores + (int64_t)u * nblk_max;
-    const int lane_off = L * NCH * 16;
+    // n * ROW <= kMaxBlocks * 512 bytes < 2^31
+    const __amdgpu_buffer_rsrc_t mrs = __builtin_amdgcn_make_buffer_rsrc((void *)mu, (short)0, n * ROW, kBufferFlags);
 
     // interleave waves over tiles so the WG walks memory front to back
     frag_t cur[NCH], nxt[NCH];
     auto load_tile = [&](int t, frag_t *f) {
         int j = j0 + (t * WAVES + wave) * TILE + col;
         j = j < n ? j : n - 1;  // rows past the end are loaded in range and not stored
-        const uint8_t *row = mu + (int64_t)j * ROW + lane_off;
+        const uint32_t off = (uint32_t)j * ROW + L * 16;
 #pragma unroll
-        for (int m = 0; m < NCH; ++m) f[m].u = *reinterpret_cast<const uint4 *>(row + m * 16);
+        for (int m = 0; m < NCH; ++m)
+            f[m].v = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(mrs, off + m * 64, 0, 0));
     };
 
     int ntiles = 0;
@@ -152,13 +165,13 @@ ss_status launch_score(const void *q, const void *meta, int meta_kind, int agg, 
     const dim3 gr((unsigned)grid), bl(256);
     const int G = Hq / Hkv;
     if (meta_kind == SS_META_CUBOID && agg == SS_AGG_MAX)
-        ss::launch(score_kernel<0, 0>, gr, bl, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
+        ss::launch_lds(score_kernel<0, 0>, gr, bl, kResidencyLds, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
     else if (meta_kind == SS_META_CUBOID)
-        ss::launch(score_kernel<0, 1>, gr, bl, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
+        ss::launch_lds(score_kernel<0, 1>, gr, bl, kResidencyLds, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
     else if (agg == SS_AGG_MAX)
-        ss::launch(score_kernel<1, 0>, gr, bl, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
+        ss::launch_lds(score_kernel<1, 0>, gr, bl, kResidencyLds, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
     else
-        ss::launch(score_kernel<1, 1>, gr, bl, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
+        ss::launch_lds(score_kernel<1, 1>, gr, bl, kResidencyLds, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
     return check_launch("ss_score_blocks");
 }
 
