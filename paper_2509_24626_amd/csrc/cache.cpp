@@ -3,9 +3,12 @@
 // least-recently-used replacement.  The selected blocks of a step are
 // resolved to slots here; the misses go to the GPU gather.
 //
-// Per unit: block -> slot map (O(1) hit test), slot -> block, last use, and
-// an intrusive doubly linked list of the cached slots in (last_use, slot)
-// order, so the eviction victim is always the list head.  Hits and misses of
+// Per unit: block -> slot map (O(1) hit test) and one 32-byte record per
+// slot (block held, last use, links of an intrusive doubly linked list of the
+// cached slots in (last_use, slot) order), so the eviction victim is always
+// the list head and a hit touches one cache line of slot state.  A unit's
+// state is cold at every step (all units together hold tens of MB), so the
+// block lookups of a unit are all issued before any update.  Hits and misses of
 // a call are unlinked while they are processed (a block selected in this
 // call can never be the victim) and re-appended at the tail in slot order,
 // merged with any tail entries already stamped with the same step.  Empty
@@ -14,7 +17,8 @@
 //
 // Units are independent; ss_cache_resolve validates every unit, sizes the
 // miss list with a prefix sum, then updates the units in parallel on a
-// small persistent thread pool.  Output order does not depend on threading.
+// small persistent thread pool (both passes in one dispatch, with a barrier
+// between them).  Output order does not depend on threading.
 #include <sched.h>
 
 #include <algorithm>
@@ -163,6 +167,13 @@ void parallel_for(int64_t n, int max_threads, const std::function<void(int64_t, 
 }
 }  // namespace ss
 
+// one slot's state; 32 bytes, so a record never straddles a cache line
+struct alignas(32) slot_rec {
+    int64_t last = 0;              // step of the last use
+    int32_t block = -1;            // block held, -1 empty
+    int32_t prev = -1, next = -1;  // LRU list links (slots local to the unit), -1 none
+};
+
 struct ss_cache {
     int B = 0, Hkv = 0;
     size_t record_bytes = 0;
@@ -170,13 +181,13 @@ struct ss_cache {
     int64_t last_step = INT64_MIN;
     std::vector<unit_state> units;
     std::vector<int32_t> block_slot;  // [sum block_cap] slot holding the block, -1
-    std::vector<int32_t> slot_block;  // [total] block held, -1 empty
-    std::vector<int64_t> slot_last;   // [total]
-    std::vector<int32_t> prev, next;  // [total] LRU links, slot indices local to the unit
+    std::vector<slot_rec> rec;        // [total]
     std::vector<int64_t> miss_count;  // [units] scratch
     int threads = 1;                          // workers used by resolve
     std::vector<std::vector<uint64_t>> mark;  // per worker: slot bitmap for ordering
     std::vector<std::vector<int32_t>> touched;  // per worker
+    std::vector<std::vector<int32_t>> found;    // per worker: slot of each selected block, -1
+    std::vector<int64_t> part_misses;           // per worker: misses of its units
 };
 
 namespace ss {
@@ -207,13 +218,12 @@ int check_unit(const unit_state &st, const int32_t *sel, int k)
     return count;
 }
 
-inline void unlink(ss_cache *c, unit_state &st, int32_t s)
+inline void unlink(slot_rec *r, unit_state &st, int32_t s)
 {
-    int32_t *pv = c->prev.data() + st.slot_base, *nx = c->next.data() + st.slot_base;
-    const int32_t p = pv[s], n = nx[s];
-    if (p >= 0) nx[p] = n; else st.head = n;
-    if (n >= 0) pv[n] = p; else st.tail = p;
-    pv[s] = nx[s] = -1;
+    const int32_t p = r[s].prev, n = r[s].next;
+    if (p >= 0) r[p].next = n; else st.head = n;
+    if (n >= 0) r[n].prev = p; else st.tail = p;
+    r[s].prev = r[s].next = -1;
 }
 
 void resolve_unit(ss_cache *c, int worker, int u, int64_t step, const int32_t *sel, int k, int32_t *slots,
@@ -221,41 +231,43 @@ void resolve_unit(ss_cache *c, int worker, int u, int64_t step, const int32_t *s
 {
     unit_state &st = c->units[u];
     int32_t *bs = c->block_slot.data() + st.block_base;
-    int32_t *sb = c->slot_block.data() + st.slot_base;
-    int64_t *last = c->slot_last.data() + st.slot_base;
-    int32_t *pv = c->prev.data() + st.slot_base, *nx = c->next.data() + st.slot_base;
+    slot_rec *r = c->rec.data() + st.slot_base;
     std::vector<int32_t> &touched = c->touched[worker];
+    int32_t *found = c->found[worker].data();
     touched.clear();
 
-    // 1. hits
+    // 1. hits: every lookup first (independent loads, prefetching the hit
+    //    slots' records), then the updates
     for (int i = 0; i < k; ++i) {
         const int32_t j = sel[i];
-        slots[i] = -1;
-        if (j < 0) continue;
-        const int32_t s = bs[j];
-        if (s >= 0) {
-            last[s] = step;
-            unlink(c, st, s);
-            touched.push_back(s);
-            slots[i] = s;
-        }
+        const int32_t s = j >= 0 ? bs[j] : -1;
+        found[i] = s;
+        if (s >= 0) __builtin_prefetch(r + s, 1);
+    }
+    for (int i = 0; i < k; ++i) {
+        const int32_t s = found[i];
+        slots[i] = s;
+        if (s < 0) continue;
+        r[s].last = step;
+        unlink(r, st, s);
+        touched.push_back(s);
     }
     // 2. misses, ascending block order
     int64_t nm = 0;
     for (int i = 0; i < k; ++i) {
         const int32_t j = sel[i];
-        if (j < 0 || slots[i] >= 0) continue;
+        if (j < 0 || found[i] >= 0) continue;
         int32_t s;
         if (st.used < st.cap) {
             s = st.used++;
         } else {
             s = st.head;  // least recently used, lowest slot among equals
-            unlink(c, st, s);
-            bs[sb[s]] = -1;
+            unlink(r, st, s);
+            bs[r[s].block] = -1;
         }
-        sb[s] = j;
+        r[s].block = j;
         bs[j] = s;
-        last[s] = step;
+        r[s].last = step;
         touched.push_back(s);
         slots[i] = s;
         int32_t *row = miss_rows + 4 * nm++;
@@ -267,9 +279,9 @@ void resolve_unit(ss_cache *c, int worker, int u, int64_t step, const int32_t *s
     if (touched.empty()) return;
     // 3. re-append the touched slots in slot order, merged with the tail run
     //    already stamped with this step
-    while (st.tail >= 0 && last[st.tail] == step) {
+    while (st.tail >= 0 && r[st.tail].last == step) {
         const int32_t s = st.tail;
-        unlink(c, st, s);
+        unlink(r, st, s);
         touched.push_back(s);
     }
     std::vector<uint64_t> &bits = c->mark[worker];
@@ -282,9 +294,9 @@ void resolve_unit(ss_cache *c, int worker, int u, int64_t step, const int32_t *s
         while (x) {
             const int32_t s = (int32_t)(w * 64 + __builtin_ctzll(x));
             x &= x - 1;
-            pv[s] = st.tail;
-            nx[s] = -1;
-            if (st.tail >= 0) nx[st.tail] = s; else st.head = s;
+            r[s].prev = st.tail;
+            r[s].next = -1;
+            if (st.tail >= 0) r[st.tail].next = s; else st.head = s;
             st.tail = s;
         }
     }
@@ -328,14 +340,13 @@ ss_status ss_cache_create(int B, int Hkv, const int32_t *nblk, const int32_t *ca
         }
         c->total_slots = slots;
         c->block_slot.assign(blocks, -1);
-        c->slot_block.assign(slots, -1);
-        c->slot_last.assign(slots, 0);
-        c->prev.assign(slots, -1);
-        c->next.assign(slots, -1);
+        c->rec.assign(slots, slot_rec{});
         c->miss_count.assign(units, 0);
         c->threads = default_threads();
         c->mark.resize(64);
         c->touched.resize(64);
+        c->found.resize(64);
+        c->part_misses.assign(64, 0);
     } catch (const std::bad_alloc &) {
         delete c;
         return ss::fail(SS_ERR_OOM, "ss_cache_create: out of memory");
@@ -445,15 +456,21 @@ ss_status ss_cache_resolve_range(ss_cache *c, int64_t step, int b_begin, int b_e
         for (int w = 0; w < nt; ++w) {
             c->touched[w].reserve((size_t)k + (size_t)cap_max);
             if (c->mark[w].size() < words) c->mark[w].resize(words);
+            if (c->found[w].size() < (size_t)k) c->found[w].resize(k);
         }
     } catch (const std::bad_alloc &) {
         return ss::fail(SS_ERR_OOM, "ss_cache_resolve: out of memory");
     }
-    // pass 1 (parallel, read-only): validate and count misses per unit
-    std::atomic<int> bad_unit{-1}, bad_kind{0};
+    // one dispatch: pass 1 (read-only) validates the units and counts their
+    // misses; after a barrier every worker sees all counts and either stops
+    // (an invalid unit, too many misses: no state changed) or, in pass 2,
+    // updates its units, writing their miss rows at their prefix offsets
+    std::atomic<int> bad_unit{-1}, bad_kind{0}, arrived{0};
+    int64_t *part = c->part_misses.data();
     workers.run([&](int w) {
         if (w >= nt) return;
         const int lo = (int)((int64_t)units * w / nt), hi = (int)((int64_t)units * (w + 1) / nt);
+        int64_t mine = 0;
         for (int i = lo; i < hi; ++i) {
             const int u = u0 + i;
             const unit_state &st = c->units[u];
@@ -470,6 +487,24 @@ ss_status ss_cache_resolve_range(ss_cache *c, int64_t step, int b_begin, int b_e
             for (int e = 0; e < k; ++e)
                 if (su[e] >= 0 && bs[su[e]] < 0) ++m;
             c->miss_count[u] = m;
+            mine += m;
+        }
+        part[w] = mine;
+        arrived.fetch_add(1, std::memory_order_acq_rel);
+        while (arrived.load(std::memory_order_acquire) < nt) std::this_thread::yield();
+        if (bad_unit.load() >= 0) return;
+        int64_t before = 0, all = 0;
+        for (int v = 0; v < nt; ++v) {
+            if (v < w) before += part[v];
+            all += part[v];
+        }
+        if (all > miss_cap) return;
+        for (int i = lo; i < hi; ++i) {
+            const int u = u0 + i;
+            int32_t *rows = miss + 4 * before;
+            before += c->miss_count[u];
+            resolve_unit(c, w, u, step, sel + (int64_t)i * k, k, slots + (int64_t)i * k, rows, u / c->Hkv,
+                         u % c->Hkv);
         }
     });
     if (bad_unit.load() >= 0) {
@@ -481,25 +516,10 @@ ss_status ss_cache_resolve_range(ss_cache *c, int64_t step, int b_begin, int b_e
                         "ss_cache_resolve: unit %d selection is not strictly ascending in [0, nblk) then -1", u);
     }
     int64_t total = 0;
-    for (int u = u0; u < u0 + units; ++u) {
-        const int64_t m = c->miss_count[u];
-        c->miss_count[u] = total;  // becomes the unit's first output row
-        total += m;
-    }
+    for (int w = 0; w < nt; ++w) total += part[w];
     if (total > miss_cap)
         return ss::fail(SS_ERR_OOM, "ss_cache_resolve: %lld misses > miss_cap %lld", (long long)total,
                         (long long)miss_cap);
-
-    // pass 2 (parallel): update the units
-    workers.run([&](int w) {
-        if (w >= nt) return;
-        const int lo = (int)((int64_t)units * w / nt), hi = (int)((int64_t)units * (w + 1) / nt);
-        for (int i = lo; i < hi; ++i) {
-            const int u = u0 + i;
-            resolve_unit(c, w, u, step, sel + (int64_t)i * k, k, slots + (int64_t)i * k, miss + 4 * c->miss_count[u],
-                         u / c->Hkv, u % c->Hkv);
-        }
-    });
     c->last_step = step;
     *n_miss = total;
     return SS_OK;
@@ -508,8 +528,10 @@ ss_status ss_cache_resolve_range(ss_cache *c, int64_t step, int b_begin, int b_e
 ss_status ss_cache_export(const ss_cache *c, int32_t *slot_block, int64_t *slot_last)
 {
     SS_CHECK_ARG(c && slot_block && slot_last, "ss_cache_export: null pointer");
-    std::memcpy(slot_block, c->slot_block.data(), sizeof(int32_t) * c->total_slots);
-    std::memcpy(slot_last, c->slot_last.data(), sizeof(int64_t) * c->total_slots);
+    for (int64_t s = 0; s < c->total_slots; ++s) {
+        slot_block[s] = c->rec[s].block;
+        slot_last[s] = c->rec[s].last;
+    }
     return SS_OK;
 }
 
