@@ -16,11 +16,14 @@
 // 512-byte rows stream from HBM with no LDS staging and no cross-lane
 // reduction; the head maximum is taken over accumulator registers.
 //
-// The launch reserves LDS that the kernel never touches (kResidencyLds), so
-// that at most two workgroups (8 waves) share a CU: on MI355X the 128k-token
-// batch streams at 0.765 of the 8 TB/s peak that way, against 0.73 with the
-// eight workgroups per CU the registers allow, 0.75 with three and 0.69 with
-// one.
+// For cuboid rows the launch reserves LDS that the kernel never touches
+// (kResidencyLds), so that at most two workgroups (8 waves) share a CU: on
+// MI355X the 128k-token batch streams at 0.765 of the 8 TB/s peak that way,
+// against 0.73 with the eight workgroups per CU the registers allow, 0.75
+// with three and 0.69 with one.  Mean-key rows are half as long, so each
+// workgroup streams half the bytes; they run fastest with no reservation
+// (0.186 ms for the batch, against 0.183-0.205 with four, three or two
+// workgroups per CU).
 #include "internal.hpp"
 
 namespace {
@@ -169,9 +172,9 @@ ss_status launch_score(const void *q, const void *meta, int meta_kind, int agg, 
     else if (meta_kind == SS_META_CUBOID)
         ss::launch_lds(score_kernel<0, 1>, gr, bl, kResidencyLds, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
     else if (agg == SS_AGG_MAX)
-        ss::launch_lds(score_kernel<1, 0>, gr, bl, kResidencyLds, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
+        ss::launch_lds(score_kernel<1, 0>, gr, bl, 0, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
     else
-        ss::launch_lds(score_kernel<1, 1>, gr, bl, kResidencyLds, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
+        ss::launch_lds(score_kernel<1, 1>, gr, bl, 0, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
     return check_launch("ss_score_blocks");
 }
 
