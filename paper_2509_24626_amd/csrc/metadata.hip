@@ -2,11 +2,13 @@
 // bounding cuboid (channel-wise min and max) of the keys of each KV block,
 // or, as the mean-key variant, the mean of the block's keys.
 //
-// One wave per block record.  A K tile is blk rows of 128 bf16 channels
-// (256 B per row); each lane loads 16 B (8 channels) of one row per step, so
-// one wave-wide load covers 4 rows.  Min and max run on 16-bit totalOrder
-// keys, two channels per 32-bit word, then across the four row groups of
-// the wave.  Lanes 0..15 write lo and hi.
+// Cuboids: one wave per 64/blk consecutive block records.  A K tile is blk
+// rows of 128 bf16 channels (256 B per row); each lane loads 16 B (8
+// channels) of one row per step, so one wave-wide load covers 4 rows, and
+// all 16 loads of the wave's records are issued before any is reduced (a
+// wave per single record kept too few bytes in flight).  Min and max run on
+// 16-bit totalOrder keys, two channels per 32-bit word, then across the four
+// row groups of the wave.  Lanes 0..15 write lo and hi.
 #include "internal.hpp"
 
 namespace {
@@ -47,49 +49,72 @@ __global__ __launch_bounds__(256) void meta_kernel(const uint8_t *__restrict__ k
                                                    uint16_t *__restrict__ meta)
 {
     constexpr int D = ss::kHeadDim;
+    constexpr int BPW = 64 / BLK;  // block records per wave: 16 loads of 16 B per lane in flight
+    constexpr int LPB = BLK / 4;   // wave-wide loads per K tile (4 rows each)
     const int lane = threadIdx.x & 63;
-    const int64_t id = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (id >= total_blocks) return;
-    const int64_t u = id / nblk_max;
-    const int j = (int)(id - u * nblk_max);
-    int n = nblk[u / Hkv];
-    n = n < 0 ? 0 : (n > nblk_max ? nblk_max : n);
-    if (j >= n) return;
-
-    const uint8_t *rec = kv_base + unit_off[u] + (int64_t)j * block_stride;
-    const int row0 = lane >> 4;         // 0..3
+    const int64_t id0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * BPW;
+    const int row0 = lane >> 4;          // 0..3
     const int cbyte = (lane & 15) * 16;  // 8 channels
-    uint32_t lo[4], hi[4];
-    {
-        uint4 v = *reinterpret_cast<const uint4 *>(rec + row0 * row_stride + cbyte);
-        lo[0] = hi[0] = to_key2(v.x);
-        lo[1] = hi[1] = to_key2(v.y);
-        lo[2] = hi[2] = to_key2(v.z);
-        lo[3] = hi[3] = to_key2(v.w);
-    }
+
+    // issue every load of the wave's records before reducing any of them
+    uint4 v[BPW][LPB];
+    bool live[BPW];
+    int64_t u_of[BPW];
+    int j_of[BPW];
 #pragma unroll
-    for (int r = 4; r < BLK; r += 4) {
-        uint4 v = *reinterpret_cast<const uint4 *>(rec + (r + row0) * row_stride + cbyte);
-        uint32_t k0 = to_key2(v.x), k1 = to_key2(v.y), k2 = to_key2(v.z), k3 = to_key2(v.w);
-        lo[0] = min2(lo[0], k0); hi[0] = max2(hi[0], k0);
-        lo[1] = min2(lo[1], k1); hi[1] = max2(hi[1], k1);
-        lo[2] = min2(lo[2], k2); hi[2] = max2(hi[2], k2);
-        lo[3] = min2(lo[3], k3); hi[3] = max2(hi[3], k3);
-    }
+    for (int b = 0; b < BPW; ++b) {
+        const int64_t id = id0 + b;  // wave-uniform
+        live[b] = id < total_blocks;
+        u_of[b] = 0;
+        j_of[b] = 0;
+        if (live[b]) {
+            const int64_t u = id / nblk_max;
+            const int j = (int)(id - u * nblk_max);
+            int n = nblk[u / Hkv];
+            n = n < 0 ? 0 : (n > nblk_max ? nblk_max : n);
+            live[b] = j < n;
+            u_of[b] = u;
+            j_of[b] = j;
+        }
+        if (live[b]) {
+            const uint8_t *rec = kv_base + unit_off[u_of[b]] + (int64_t)j_of[b] * block_stride;
 #pragma unroll
-    for (int x = 16; x <= 32; x <<= 1) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            lo[i] = min2(lo[i], (uint32_t)__shfl_xor((int)lo[i], x));
-            hi[i] = max2(hi[i], (uint32_t)__shfl_xor((int)hi[i], x));
+            for (int r = 0; r < LPB; ++r)
+                v[b][r] = *reinterpret_cast<const uint4 *>(rec + (4 * r + row0) * row_stride + cbyte);
         }
     }
-    if (lane < 16) {
-        uint16_t *m = meta + ((int64_t)u * nblk_max + j) * (2 * D);
-        uint4 l4 = make_uint4(from_key2(lo[0]), from_key2(lo[1]), from_key2(lo[2]), from_key2(lo[3]));
-        uint4 h4 = make_uint4(from_key2(hi[0]), from_key2(hi[1]), from_key2(hi[2]), from_key2(hi[3]));
-        *reinterpret_cast<uint4 *>(m + lane * 8) = l4;
-        *reinterpret_cast<uint4 *>(m + D + lane * 8) = h4;
+#pragma unroll
+    for (int b = 0; b < BPW; ++b) {
+        if (!live[b]) continue;
+        uint32_t lo[4], hi[4];
+        lo[0] = hi[0] = to_key2(v[b][0].x);
+        lo[1] = hi[1] = to_key2(v[b][0].y);
+        lo[2] = hi[2] = to_key2(v[b][0].z);
+        lo[3] = hi[3] = to_key2(v[b][0].w);
+#pragma unroll
+        for (int r = 1; r < LPB; ++r) {
+            const uint32_t k0 = to_key2(v[b][r].x), k1 = to_key2(v[b][r].y), k2 = to_key2(v[b][r].z),
+                           k3 = to_key2(v[b][r].w);
+            lo[0] = min2(lo[0], k0); hi[0] = max2(hi[0], k0);
+            lo[1] = min2(lo[1], k1); hi[1] = max2(hi[1], k1);
+            lo[2] = min2(lo[2], k2); hi[2] = max2(hi[2], k2);
+            lo[3] = min2(lo[3], k3); hi[3] = max2(hi[3], k3);
+        }
+#pragma unroll
+        for (int x = 16; x <= 32; x <<= 1) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                lo[i] = min2(lo[i], (uint32_t)__shfl_xor((int)lo[i], x));
+                hi[i] = max2(hi[i], (uint32_t)__shfl_xor((int)hi[i], x));
+            }
+        }
+        if (lane < 16) {
+            uint16_t *m = meta + ((int64_t)u_of[b] * nblk_max + j_of[b]) * (2 * D);
+            const uint4 l4 = make_uint4(from_key2(lo[0]), from_key2(lo[1]), from_key2(lo[2]), from_key2(lo[3]));
+            const uint4 h4 = make_uint4(from_key2(hi[0]), from_key2(hi[1]), from_key2(hi[2]), from_key2(hi[3]));
+            *reinterpret_cast<uint4 *>(m + lane * 8) = l4;
+            *reinterpret_cast<uint4 *>(m + D + lane * 8) = h4;
+        }
     }
 }
 
@@ -147,7 +172,9 @@ extern "C" ss_status ss_build_metadata_strided(const void *kv_base, const int64_
     SS_CHECK_ARG(kv_base && unit_off && nblk && meta, "ss_build_metadata: null pointer");
     SS_CHECK_ARG(((uintptr_t)kv_base & 15) == 0 && ((uintptr_t)meta & 15) == 0,
                  "ss_build_metadata: kv_base and meta must be 16-byte aligned");
-    const int64_t grid = (total + 3) / 4;
+    // cuboids: 4 waves of 64/blk records per workgroup; mean keys: 4 records
+    const int64_t per_wg = meta_kind == SS_META_CUBOID ? 4 * (64 / blk) : 4;
+    const int64_t grid = (total + per_wg - 1) / per_wg;
     SS_CHECK_SUPPORTED(grid <= 0x7FFFFFFF, "ss_build_metadata: too many blocks");
     hipStream_t s = ss::as_stream(stream);
     const uint8_t *kv = static_cast<const uint8_t *>(kv_base);
