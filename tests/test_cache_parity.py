@@ -80,6 +80,32 @@ def test_thread_count_does_not_change_results(oracle_impl, threads):
     run_stream(oracle_impl, nblk, Hkv, k, cap, steps=10, churn=0.3, seed=13, threads=threads)
 
 
+def test_caches_resolved_from_several_threads(oracle_impl):
+    """The resolve workers are one pool per process, shared by every cache,
+    and one call validates and updates in a single dispatch with a barrier
+    between the passes.  Four caches (different shapes and thread counts)
+    resolved at the same time from four Python threads (the C call releases
+    the interpreter lock) must each match the oracle step for step."""
+    import threading
+    shapes = [([120] * 9, 3, 10, 30, 2), ([64, 7, 200], 4, 12, 25, 5), ([300] * 4, 2, 16, 48, 16), ([90] * 6, 1, 8, 8, 1)]
+    errors = []
+
+    def run(i, nblk, Hkv, k, capv, threads):
+        try:
+            cap = np.full((len(nblk), Hkv), capv, np.int32)
+            run_stream(oracle_impl, nblk, Hkv, k, cap, steps=25, churn=0.4, seed=100 + i, threads=threads)
+        except BaseException as e:  # reported on the main thread
+            errors.append((i, e))
+
+    workers = [threading.Thread(target=run, args=(i, *sh)) for i, sh in enumerate(shapes)]
+    for w in workers:
+        w.start()
+    for w in workers:
+        w.join(timeout=120)
+    assert not any(w.is_alive() for w in workers), "a resolve did not return"
+    assert not errors, errors
+
+
 def test_repeated_step_numbers(oracle_impl):
     nblk = [50, 50]
     cap = np.full((2, 2), 10, np.int32)
