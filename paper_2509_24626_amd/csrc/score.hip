@@ -12,18 +12,21 @@
 // fp32 and accumulate in fp32.  The GQA heads fill the MFMA rows (padded to
 // 16 with zero weights); each column is one block.
 //
-// Every MFMA B fragment is a direct 16-byte load of one metadata row, so the
-// 512-byte rows stream from HBM with no LDS staging and no cross-lane
-// reduction; the head maximum is taken over accumulator registers.
+// Each wave reads a tile of 16 consecutive metadata rows as whole contiguous
+// 1 KiB pieces with the non-temporal cache policy, stages it in LDS and reads
+// its MFMA B fragments from there; there is no cross-lane reduction, the head
+// maximum is taken over accumulator registers.  On MI355X the 128k-token
+// batch streams at 0.82 of the 8 TB/s peak this way.  Fragments loaded
+// straight from HBM (each instruction covering 64-byte pieces of 16 rows)
+// reached 0.765 and got slower with the non-temporal policy, since a
+// 128-byte line was then requested by two instructions; staged through LDS
+// with the default policy they reached 0.765 too.
 //
-// For cuboid rows the launch reserves LDS that the kernel never touches
-// (kResidencyLds), so that at most two workgroups (8 waves) share a CU: on
-// MI355X the 128k-token batch streams at 0.765 of the 8 TB/s peak that way,
-// against 0.73 with the eight workgroups per CU the registers allow, 0.75
-// with three and 0.69 with one.  Mean-key rows are half as long, so each
-// workgroup streams half the bytes; they run fastest with no reservation
-// (0.186 ms for the batch, against 0.183-0.205 with four, three or two
-// workgroups per CU).
+// For cuboid rows the launch reserves LDS up to kResidencyLds per workgroup,
+// so that at most two workgroups (8 waves) share a CU: 0.82 that way against
+// 0.81 with four.  (With direct fragment loads, before the staging: 0.765
+// with two, 0.73 with the eight the registers allow, 0.75 with three, 0.69
+// with one.)  Mean-key rows are half as long and launch with no reservation.
 #include "internal.hpp"
 
 namespace {
@@ -36,7 +39,11 @@ constexpr int BLOCKS_PER_WG = TILE * WAVES * TILES_PER_WAVE;  // 256
 // 2 x 60 KiB fit in a CU's 160 KiB of LDS and 3 do not; the 40 KiB left over
 // still take one attention workgroup (34 KiB) beside two scoring workgroups
 constexpr size_t kResidencyLds = 60 * 1024;
+// static LDS of the staging buffers for `row` bytes per metadata row
+constexpr size_t stage_bytes(int row) { return (size_t)WAVES * TILE * (row / 16 + 1) * 16; }
+static_assert(stage_bytes(512) <= kResidencyLds, "staging exceeds the residency budget");
 constexpr int kBufferFlags = 0x00020000;  // raw buffer descriptor word 3 for gfx9 (32-bit data)
+constexpr int kStream = 2;                // cache policy of the metadata loads: non-temporal
 
 union frag_t {
     bf16x8_t v;
@@ -44,12 +51,9 @@ union frag_t {
     uint16_t h[8];
 };
 
-// Lane (L = lane/16, col = lane%16) takes 16-byte chunk c = 4*m + L of a
-// metadata row for MFMA m of a tile, so each load instruction covers one
-// contiguous 64-byte piece of each of the tile's 16 rows.  (Each lane
-// streaming NCH*16 contiguous bytes of its row instead measured 1.5% slower
-// through buffer loads.)  The A fragments hold the matching weights of head
-// `col`.
+// Lane (L = lane/16, col = lane%16) reads 16-byte chunk c = 4*m + L of
+// metadata row `col` of the staged tile for MFMA m.  The A fragments hold
+// the matching weights of head `col`.
 //
 // KIND 0, cuboid rows [lo, hi] (512 B, NCH = 8): chunks 0..15 are lo and
 // multiply min(q, 0), chunks 16..31 (m >= 4) are hi and multiply max(q, 0).
@@ -107,15 +111,23 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__
     // n * ROW <= kMaxBlocks * 512 bytes < 2^31
     const __amdgpu_buffer_rsrc_t mrs = __builtin_amdgcn_make_buffer_rsrc((void *)mu, (short)0, n * ROW, kBufferFlags);
 
-    // interleave waves over tiles so the WG walks memory front to back
-    frag_t cur[NCH], nxt[NCH];
-    auto load_tile = [&](int t, frag_t *f) {
-        int j = j0 + (t * WAVES + wave) * TILE + col;
-        j = j < n ? j : n - 1;  // rows past the end are loaded in range and not stored
-        const uint32_t off = (uint32_t)j * ROW + L * 16;
+    // each wave stages its 16-row tile through its own LDS region: eight (cuboid)
+    // or four (mean key) contiguous 1 KiB non-temporal loads, then the MFMA
+    // fragments are read back (row pitch padded by 16 B, so each 16-lane group
+    // of a fragment read touches 64 distinct banks); the waves interleave over
+    // tiles, so the workgroup walks its rows front to back
+    constexpr int NLD = TILE * ROW / 1024;
+    constexpr int RU = ROW / 16;  // 16-byte units per row
+    constexpr int LR = RU + 1;    // LDS row pitch in 16-byte units
+    __shared__ uint4 stage[WAVES][TILE * LR];
+    uint4 *my = stage[wave];
+    const int lane_id = threadIdx.x & 63;
+    uint4 buf[2][NLD];
+    auto load_tile = [&](int t, uint4 *r) {
+        const uint32_t base = (uint32_t)(j0 + (t * WAVES + wave) * TILE) * ROW + lane_id * 16;
 #pragma unroll
-        for (int m = 0; m < NCH; ++m)
-            f[m].v = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(mrs, off + m * 64, 0, 0));
+        for (int i = 0; i < NLD; ++i)  // rows at or past n read as zero (buffer bounds) and are not stored
+            r[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(mrs, base + i * 1024, 0, kStream));
     };
 
     int ntiles = 0;
@@ -123,13 +135,23 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__
         if (j0 + (t * WAVES + wave) * TILE < n) ntiles = t + 1;
     if (ntiles == 0) return;
 
-    load_tile(0, cur);
-    for (int t = 0; t < ntiles; ++t) {
-        if (t + 1 < ntiles) load_tile(t + 1, nxt);
+    load_tile(0, buf[0]);
+#pragma unroll
+    for (int t = 0; t < TILES_PER_WAVE; ++t) {
+        if (t >= ntiles) break;
+        if (t + 1 < ntiles) load_tile(t + 1, buf[(t + 1) & 1]);
+#pragma unroll
+        for (int i = 0; i < NLD; ++i) {
+            const int e = i * 64 + lane_id;
+            my[(e / RU) * LR + e % RU] = buf[t & 1][i];
+        }
         f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int m = 0; m < NCH; ++m) acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[m].v, cur[m].v, acc, 0, 0, 0);
-        // lane holds heads L*4 .. L*4+3 of block column `col`
+        for (int m = 0; m < NCH; ++m) {
+            frag_t f;
+            f.u = my[col * LR + 4 * m + L];
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(w[m].v, f.v, acc, 0, 0, 0);
+        }
         float s;
         if (AGG == 0) {
             s = -INFINITY;
@@ -145,10 +167,6 @@ __global__ __launch_bounds__(256) void score_kernel(const uint16_t *__restrict__
         }
         const int j = j0 + (t * WAVES + wave) * TILE + col;
         if (L == 0 && j < n) su[j] = s;
-        if (t + 1 < ntiles) {
-#pragma unroll
-            for (int m = 0; m < NCH; ++m) cur[m] = nxt[m];
-        }
     }
 }
 
@@ -168,9 +186,9 @@ ss_status launch_score(const void *q, const void *meta, int meta_kind, int agg, 
     const dim3 gr((unsigned)grid), bl(256);
     const int G = Hq / Hkv;
     if (meta_kind == SS_META_CUBOID && agg == SS_AGG_MAX)
-        ss::launch_lds(score_kernel<0, 0>, gr, bl, kResidencyLds, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
+        ss::launch_lds(score_kernel<0, 0>, gr, bl, kResidencyLds - stage_bytes(512), s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
     else if (meta_kind == SS_META_CUBOID)
-        ss::launch_lds(score_kernel<0, 1>, gr, bl, kResidencyLds, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
+        ss::launch_lds(score_kernel<0, 1>, gr, bl, kResidencyLds - stage_bytes(512), s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
     else if (agg == SS_AGG_MAX)
         ss::launch_lds(score_kernel<1, 0>, gr, bl, 0, s, qq, mm, nblk, Hq, Hkv, G, nblk_max, chunks, scores);
     else
