@@ -10,10 +10,14 @@
 //   O^T[128 ch x 16 heads] += V^T[128 x 16 tok] * P^T   8 x v_mfma_f32_16x16x16_bf16 (x2, hi/lo)
 // The S^T accumulator leaves lane (L = lane/16, col = lane%16) holding head
 // `col` for tokens 4L .. 4L+3, which is exactly the lane's B fragment of the
-// 16x16x16 PV product, so P never moves between lanes.  K fragments are one
-// 16-byte load per lane (channels m*32 + 8L .. +7, so each load instruction
-// reads a contiguous 64-byte piece of 16 token rows); the V tile of a block
-// record is stored channel-major, so each V^T fragment is one 8-byte load.
+// 16x16x16 PV product, so P never moves between lanes.  The step's K rows
+// are read as four contiguous 1 KiB loads and staged in the wave's LDS tile,
+// from which the A fragments (channels m*32 + 8L .. +7 of row `col`) are
+// read; loading the fragments directly (each instruction a 64-byte piece of
+// 16 rows) measured 0.805 of the HBM peak on the 128k batch against 0.825.
+// The V tile of a block record is stored channel-major, so each V^T
+// fragment is one 8-byte load and each V load instruction reads 512
+// contiguous bytes.
 // Each wave keeps two steps in flight (the next step's loads are issued
 // before the current step is computed).  K and V are read with raw buffer
 // loads over the unit's cache region: a skipped entry gets an offset past
@@ -38,6 +42,7 @@ namespace {
 constexpr int D = ss::kHeadDim;
 constexpr int WAVES = 4;
 constexpr int TOK = 16;  // tokens per wave step
+constexpr int KPITCH = D * 2 / 16 + 1;  // LDS row pitch of a staged K tile, in 16-byte units
 
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 constexpr int kBufferFlags = 0x00020000;  // raw buffer descriptor word 3 for gfx9 (32-bit data)
@@ -80,6 +85,7 @@ __global__ __launch_bounds__(256, 3) void attn_kernel(const uint16_t *__restrict
     constexpr int64_t REC = 2LL * BLK * D * 2;
     __shared__ float sm_m[WAVES][16], sm_l[WAVES][16];
     __shared__ float sm_o[WAVES][16][D + 4];
+    __shared__ uint4 kst[WAVES][TOK * KPITCH];  // each wave's K tile of the current step
 
     const int u = blockIdx.x, split = blockIdx.y, splits = gridDim.y;
     const int b = u / Hkv, g = u - b * Hkv;
@@ -117,28 +123,31 @@ __global__ __launch_bounds__(256, 3) void attn_kernel(const uint16_t *__restrict
     for (int t = 0; t < 8; ++t) o[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
     struct step_t {
-        frag8_t kf[4];
+        uint4 kr[4];  // K rows 4i + L, channels 8col .. 8col+7
         frag4_t vf[8];
         bool vz;  // the lane's accumulator tokens 4L .. 4L+3 are selected
     };
     // token t of the unit's selected-token sequence -> (entry t / BLK, position t % BLK)
     auto load_step = [&](int st, step_t &x) {
-        const int tk = st * TOK + col;     // this lane's K row
-        const int tv = st * TOK + L * 4;   // this lane's V^T / accumulator tokens
+        const int tv = st * TOK + L * 4;  // this lane's V^T / accumulator tokens
         // entries of the step (uniform): one, or two when BLK = 8
         const int e0 = (st * TOK) / BLK;
         const int s0 = e0 < k ? us[e0] : -1;
         const int s1 = (BLK == 8 && e0 + 1 < k) ? us[e0 + 1] : -1;
-        const int sk = (BLK == 8 && col >= 8) ? s1 : s0;
         const int sv = (BLK == 8 && L >= 2) ? s1 : s0;
         const bool live = st < s_end;  // steps past the range load zeros
-        const bool vk = live && sk >= 0 && sk < slot_limit;
         const bool vv = live && sv >= 0 && sv < slot_limit;
-        // skipped entries read at `lim`, past the region: the loads return zeros
-        const uint32_t ko = vk ? (uint32_t)sk * (uint32_t)REC + (tk % BLK) * (D * 2) + L * 16 : lim;
+        // skipped entries read at `lim`, past the region: the loads return zeros.
+        // K: load i reads token rows 4i .. 4i+3 of the step, 1 KiB contiguous
+        // (whole 128-byte lines, so the non-temporal policy pays)
 #pragma unroll
-        for (int m = 0; m < 4; ++m)
-            x.kf[m].v = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rsrc, ko + m * 64, 0, kStream));
+        for (int i = 0; i < 4; ++i) {
+            const int r = 4 * i + L;
+            const int sr = (BLK == 8 && r >= 8) ? s1 : s0;
+            const bool vr = live && sr >= 0 && sr < slot_limit;
+            const uint32_t ko = vr ? (uint32_t)sr * (uint32_t)REC + ((st * TOK + r) % BLK) * (D * 2) + col * 16 : lim;
+            x.kr[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, ko, 0, kStream));
+        }
         const uint32_t vo = vv ? (uint32_t)sv * (uint32_t)REC + BLK * D * 2 + (col * BLK + tv % BLK) * 2 : lim;
 #pragma unroll
         for (int t = 0; t < 8; ++t)
@@ -146,9 +155,17 @@ __global__ __launch_bounds__(256, 3) void attn_kernel(const uint16_t *__restrict
         x.vz = vv;
     };
     auto compute_step = [&](const step_t &x) {
+        // K rows through the wave's LDS tile into A fragments: row `col`,
+        // channels m*32 + 8L .. +7 (the padded pitch keeps each 16-lane group
+        // of a fragment read on 64 distinct banks)
+        uint4 *kt = kst[wave];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) kt[(4 * i + L) * KPITCH + col] = x.kr[i];
         f32x4_t sacc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int m = 0; m < 4; ++m) sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(x.kf[m].v, qf[m].v, sacc, 0, 0, 0);
+        for (int m = 0; m < 4; ++m)
+            sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kt[col * KPITCH + 4 * m + L]),
+                                                           qf[m].v, sacc, 0, 0, 0);
         float z[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) z[i] = x.vz ? sacc[i] * scale_log2 : -INFINITY;

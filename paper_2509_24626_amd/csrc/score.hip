@@ -36,9 +36,9 @@ constexpr int TILE = 16;              // blocks per MFMA tile
 constexpr int WAVES = 4;
 constexpr int TILES_PER_WAVE = 4;
 constexpr int BLOCKS_PER_WG = TILE * WAVES * TILES_PER_WAVE;  // 256
-// 2 x 60 KiB fit in a CU's 160 KiB of LDS and 3 do not; the 40 KiB left over
-// still take one attention workgroup (34 KiB) beside two scoring workgroups
-constexpr size_t kResidencyLds = 60 * 1024;
+// 2 x 54 KiB fit in a CU's 160 KiB of LDS and 3 do not; the 52 KiB left over
+// still take one attention workgroup (50.5 KiB) beside two scoring workgroups
+constexpr size_t kResidencyLds = 54 * 1024;
 // static LDS of the staging buffers for `row` bytes per metadata row
 constexpr size_t stage_bytes(int row) { return (size_t)WAVES * TILE * (row / 16 + 1) * 16; }
 static_assert(stage_bytes(512) <= kResidencyLds, "staging exceeds the residency budget");
