@@ -371,13 +371,13 @@ KERNEL_SOURCES = {
 # hierarchical 128k-context layer, seed 0, 16 timed steps after 1 warm-up, groups 2,4,10,20,18,8,2, host resolve
 _KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 16, 1, [2, 4, 10, 20, 18, 8, 2], "host"]
 TRAFFIC = {
-    "gather": {"key": _KEY, "digest": "b6afd93dae4c85a6", "bytes": 260492095, "fetch": 131094847,
+    "gather": {"key": _KEY, "digest": "b6afd93dae4c85a6", "bytes": 260492263, "fetch": 131095015,
               "write": 129397248},
-    "score": {"key": _KEY, "digest": "2c912802edb4f092", "bytes": 2168573248, "fetch": 2151667040,
-              "write": 16906208},
+    "score": {"key": _KEY, "digest": "c9510f2bf97a7ac5", "bytes": 2168518559, "fetch": 2151712415,
+              "write": 16806144},
     "topk": {"key": _KEY, "digest": "42708fbdeead668e", "bytes": 17173117, "fetch": 16910973,
               "write": 262144},
-    "attention": {"key": _KEY, "digest": "275b5374d3e47ca9", "bytes": 545197337, "fetch": 544148761,
+    "attention": {"key": _KEY, "digest": "5cedad6fe6654272", "bytes": 539117669, "fetch": 538069093,
               "write": 1048576},
 }
 
