@@ -205,6 +205,32 @@ def test_planted_blocks_are_selected(ss):
             assert set(planted.tolist()) <= set(gsel[b, g].tolist())
 
 
+def test_scores_at_the_largest_block_count(ss, oracle_impl):
+    """Scoring and selection at 65536 blocks per unit (the largest supported)
+    with a ragged second sequence: each wave's staged tiles past a
+    sequence's end read zeros through the buffer bounds and nothing is
+    written past the end; scores and selection match the oracle."""
+    rng = np.random.default_rng(21)
+    B, Hq, Hkv, nmax, k = 2, 8, 2, 65536, 128
+    nblk = np.array([65536, 40001], np.int32)
+    a = torch.from_numpy(rng.standard_normal((B, Hkv, nmax, 128)).astype(np.float32))
+    c = torch.from_numpy(rng.standard_normal((B, Hkv, nmax, 128)).astype(np.float32))
+    meta = torch.stack([torch.minimum(a, c), torch.maximum(a, c)], 3).bfloat16().cuda().contiguous()
+    del a, c
+    q = torch.from_numpy(rng.standard_normal((B, Hq, 128)).astype(np.float32)).bfloat16().cuda()
+    scores = torch.full((B, Hkv, nmax), 7.0, dtype=torch.float32, device="cuda")
+    sel = torch.empty(B, Hkv, k, dtype=torch.int32, device="cuda")
+    ss.ss_score_topk(q, meta, torch.from_numpy(nblk).cuda(), B, Hq, Hkv, nmax, 128, k, scores, sel)
+    torch.cuda.synchronize()
+    q_host = gu.u16(q)
+    meta_host = gu.u16(meta)
+    S = oracle_impl.score(q_host, meta_host, nblk, Hq, Hkv, nmax, 128)
+    got = scores.cpu().numpy()
+    assert np.all(got[1, :, 40001:] == 7.0), "scores written past the sequence's end"
+    gu.check_scores(got, S, q_host, meta_host, nblk, Hq // Hkv)
+    gu.check_selection(sel.cpu().numpy(), oracle_impl.select(S, nblk, k), S, nblk, k)
+
+
 def test_topk_exact_ties(ss, oracle_impl):
     """Scores drawn from a handful of values (massive exact ties, +0 and -0,
     negatives): the GPU selection must equal the oracle's bit for bit."""
