@@ -874,7 +874,7 @@ def isolated_rates(cfg, L, q, ss, torch, reps=10):
                   blocks * (2 * D * 2 + 4) + B * Hq * D * 2),
         "topk": (lambda: ss.ss_select_topk(L.scores, L.nblk, B, Hkv, L.nblk_max, k, L.sel),
                  blocks * 4 + B * Hkv * k * 4),
-        "attention": (lambda: ss.ss_sparse_attention(q, L.cache, L.cache_off, L.slots, int(L.capacity.max()), B, Hq,
+        "attention": (lambda: ss.ss_sparse_attention(q, L.cache, L.cache_off, L.slots, L.cap_dev, int(L.capacity.max()), B, Hq,
                                                      Hkv, D, cfg.blk, k, 1.0 / math.sqrt(D), out, ws, ws_bytes),
                       valid * cfg.record_bytes + B * Hq * D * (2 + 4)),
     }

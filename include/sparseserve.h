@@ -66,7 +66,7 @@ typedef int ss_status;
 #define SS_ERR_OOM 4         /* host allocation failed, or a caller buffer is too small */
 #define SS_ERR_HIP 5         /* a HIP runtime call or kernel launch failed */
 
-#define SS_ABI_VERSION 2
+#define SS_ABI_VERSION 3
 
 int ss_abi_version(void);
 const char *ss_status_string(ss_status status);
@@ -290,20 +290,26 @@ ss_status ss_gather_blocks(const int32_t *miss, int64_t n_miss, const void *pool
  * restricted as in Section 2.2):
  *     z_t = scale * q[b,h] . K_t,  p = softmax(z),  out[b,h] = sum_t p_t V_t
  * over the tokens t of the records at kv_base + region_off[u] +
- * slots[u][i]*record_bytes, i < k; entries < 0 or >= slot_limit are
- * skipped.  With no token the output is 0.  fp32 accumulation; the
- * probabilities enter the PV product as a bf16 hi/lo pair, so they are
- * carried to about 16 significant bits.
+ * slots[u][i]*record_bytes, i < k.  An entry is skipped (never read) if it
+ * is < 0, >= slot_limit, or >= capacity[u] when `capacity` is given, so a
+ * unit reads only its own region even when the units' slot counts differ.
+ * With no token the output is 0.  fp32 accumulation; the probabilities
+ * enter the PV product as a bf16 hi/lo pair, so they are carried to about
+ * 16 significant bits.
  *   q: device bf16 [B][Hq][d]; region_off: device int64 [B*Hkv];
  *   slots: device int32 [B][Hkv][k]; out: device fp32 [B][Hq][d]
+ *   capacity: device int32 [B*Hkv], the slots of each unit's region (the
+ *   block cache's capacities), or NULL to bound every unit by slot_limit
+ *   slot_limit: the largest slot count of any unit (slot_limit records
+ *   must span less than 2 GiB; SS_ERR_UNSUPPORTED otherwise)
  *   workspace: device, at least ss_sparse_attention_workspace(...) bytes
  *   (the call fails with SS_ERR_OOM if ws_bytes is smaller).
- * All-HBM layouts pass slots = the selection and region_off = the units'
- * block arrays. */
+ * All-HBM layouts pass slots = the selection, region_off = the units'
+ * block arrays, capacity = NULL and slot_limit = nblk_max. */
 size_t ss_sparse_attention_workspace(int B, int Hq, int Hkv, int d, int blk, int k);
 ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t *region_off, const int32_t *slots,
-                              int32_t slot_limit, int B, int Hq, int Hkv, int d, int blk, int k, float scale,
-                              float *out, void *workspace, size_t ws_bytes, void *stream);
+                              const int32_t *capacity, int32_t slot_limit, int B, int Hq, int Hkv, int d, int blk,
+                              int k, float scale, float *out, void *workspace, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------ appending tokens
  * The decode step's new KV (Section 3.2.2: each layer's new KV tensor, one
@@ -448,8 +454,8 @@ ss_status ss_prefill_plan(int64_t T, int layers, int64_t max_inject, int32_t *it
  * (pinned, mapped, coherent: ss_host_alloc_mapped with flags 0): sel_host,
  * slots_host int32 [B][Hkv][k]; miss_host int32 [miss_cap][4];
  * miss_cap >= B*Hkv*k; SS_ERR_INVALID_ARG if they are not mapped.
- * slot_limit: the largest per-unit capacity (slots at or above it are never
- * read).  cache_off_dev = ss_cache_region_offsets, copied to the device.
+ * slot_limit: the largest per-unit capacity; attention reads no slot at or
+ * above a unit's own capacity_dev entry.  cache_off_dev = ss_cache_region_offsets, copied to the device.
  * After the call, miss_host rows [0, *n_miss) hold the step's misses in
  * unit order (as one ss_cache_resolve would list them).
  * events: NULL, or 7*parts hipEvent_t (any entry may be NULL); for group p,

@@ -65,8 +65,8 @@ _SIGNATURES = {
     "ss_gather_blocks": (_i32, [_vp, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _i32, _i32, _sz, _vp]),
     "ss_sparse_attention_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32]),
     "ss_score_topk_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32]),
-    "ss_sparse_attention": (_i32, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp, _vp,
-                                   _sz, _vp]),
+    "ss_sparse_attention": (_i32, [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32, _vp,
+                                   _vp, _sz, _vp]),
     "ss_decode_layer": (_i32, [ctypes.POINTER(ss_layer_buffers), _i64, _vp, _vp, _vp, _vp, _vp]),
     "ss_cache_set_blocks": (_i32, [_vp, _vp]),
     "ss_append_kv": (_i32, [_vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _i32, _vp, _vp]),
@@ -247,10 +247,11 @@ def ss_score_topk_workspace(B, Hq, Hkv, nblk_max, d, k):
     return int(lib().ss_score_topk_workspace(B, Hq, Hkv, nblk_max, d, k))
 
 
-def ss_sparse_attention(q, kv_base, region_off, slots, slot_limit, B, Hq, Hkv, d, blk, k, scale, out, workspace,
-                        ws_bytes, stream=None):
-    _check(lib().ss_sparse_attention(_ptr(q), _ptr(kv_base), _ptr(region_off), _ptr(slots), slot_limit, B, Hq, Hkv,
-                                     d, blk, k, float(scale), _ptr(out), _ptr(workspace), ws_bytes, _stream(stream)))
+def ss_sparse_attention(q, kv_base, region_off, slots, capacity, slot_limit, B, Hq, Hkv, d, blk, k, scale, out,
+                        workspace, ws_bytes, stream=None):
+    _check(lib().ss_sparse_attention(_ptr(q), _ptr(kv_base), _ptr(region_off), _ptr(slots), _ptr(capacity),
+                                     slot_limit, B, Hq, Hkv, d, blk, k, float(scale), _ptr(out), _ptr(workspace),
+                                     ws_bytes, _stream(stream)))
 
 
 def ss_decode_layer(buffers, step, q, out, stream=None, events=None):

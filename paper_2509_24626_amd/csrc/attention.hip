@@ -78,7 +78,8 @@ struct split_plan {
 template <int BLK>
 __global__ __launch_bounds__(256, 3) void attn_kernel(const uint16_t *__restrict__ q, const uint8_t *__restrict__ kv,
                                                       const int64_t *__restrict__ region_off,
-                                                      const int32_t *__restrict__ slots, int slot_limit, int Hq,
+                                                      const int32_t *__restrict__ slots,
+                                                      const int32_t *__restrict__ capacity, int slot_limit, int Hq,
                                                       int Hkv, int G, int k, float scale_log2, int steps_per_split,
                                                       float *__restrict__ out, float *__restrict__ ws)
 {
@@ -113,7 +114,14 @@ __global__ __launch_bounds__(256, 3) void attn_kernel(const uint16_t *__restrict
 
     const uint8_t *ubase = kv + region_off[u];
     const int32_t *us = slots + (int64_t)u * k;
-    const uint32_t lim = (uint32_t)slot_limit * (uint32_t)REC;  // bytes of the region (< 2^31, host-checked)
+    // the unit's own slot count bounds its entries, so a slot past it can
+    // never reach into the next unit's region (or past the cache)
+    int nslot = slot_limit;
+    if (capacity) {
+        const int c = capacity[u];
+        nslot = c < 0 ? 0 : (c < slot_limit ? c : slot_limit);
+    }
+    const uint32_t lim = (uint32_t)nslot * (uint32_t)REC;  // bytes of the region (< 2^31, host-checked)
     const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc((void *)ubase, (short)0, (int)lim,
                                                                           kBufferFlags);
 
@@ -136,7 +144,7 @@ __global__ __launch_bounds__(256, 3) void attn_kernel(const uint16_t *__restrict
         const int s1 = (BLK == 8 && e0 + 1 < k) ? us[e0 + 1] : -1;
         const int sv = (BLK == 8 && L >= 2) ? s1 : s0;
         const bool live = st < s_end;  // steps past the range load zeros
-        const bool vv = live && sv >= 0 && sv < slot_limit;
+        const bool vv = live && sv >= 0 && sv < nslot;
         // skipped entries read at `lim`, past the region: the loads return zeros.
         // K: load i reads token rows 4i .. 4i+3 of the step, 1 KiB contiguous
         // (whole 128-byte lines, so the non-temporal policy pays)
@@ -144,7 +152,7 @@ __global__ __launch_bounds__(256, 3) void attn_kernel(const uint16_t *__restrict
         for (int i = 0; i < 4; ++i) {
             const int r = 4 * i + L;
             const int sr = (BLK == 8 && r >= 8) ? s1 : s0;
-            const bool vr = live && sr >= 0 && sr < slot_limit;
+            const bool vr = live && sr >= 0 && sr < nslot;
             const uint32_t ko = vr ? (uint32_t)sr * (uint32_t)REC + ((st * TOK + r) % BLK) * (D * 2) + col * 16 : lim;
             x.kr[i] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, ko, 0, kStream));
         }
@@ -304,7 +312,8 @@ extern "C" size_t ss_sparse_attention_workspace(int B, int Hq, int Hkv, int d, i
 }
 
 extern "C" ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t *region_off,
-                                         const int32_t *slots, int32_t slot_limit, int B, int Hq, int Hkv, int d,
+                                         const int32_t *slots, const int32_t *capacity, int32_t slot_limit, int B,
+                                         int Hq, int Hkv, int d,
                                          int blk, int k, float scale, float *out, void *workspace, size_t ws_bytes,
                                          void *stream)
 {
@@ -332,9 +341,9 @@ extern "C" ss_status ss_sparse_attention(const void *q, const void *kv_base, con
     const uint8_t *kv = static_cast<const uint8_t *>(kv_base);
     float *ws = static_cast<float *>(workspace);
     switch (blk) {
-    case 8: ss::launch(attn_kernel<8>, grid, dim3(256), s, qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
-    case 16: ss::launch(attn_kernel<16>, grid, dim3(256), s, qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
-    default: ss::launch(attn_kernel<32>, grid, dim3(256), s, qq, kv, region_off, slots, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
+    case 8: ss::launch(attn_kernel<8>, grid, dim3(256), s, qq, kv, region_off, slots, capacity, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
+    case 16: ss::launch(attn_kernel<16>, grid, dim3(256), s, qq, kv, region_off, slots, capacity, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
+    default: ss::launch(attn_kernel<32>, grid, dim3(256), s, qq, kv, region_off, slots, capacity, slot_limit, Hq, Hkv, G, k, scale_log2, sp.steps_per_split, out, ws); break;
     }
     ss_status st = ss::check_launch("ss_sparse_attention");
     if (st != SS_OK || sp.splits == 1) return st;

@@ -241,7 +241,8 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
             return st;
         if ((st = record(events, 7 * p + 5, s))) return st;
         st = ss_sparse_attention(q8 + (size_t)b0 * Hq * d * 2, L->cache_base, L->cache_off_dev + b0 * Hkv,
-                                 L->slots_dev + row0, L->slot_limit, Bp, Hq, Hkv, d, L->blk, k, L->scale,
+                                 L->slots_dev + row0, L->capacity_dev ? L->capacity_dev + b0 * Hkv : nullptr,
+                                 L->slot_limit, Bp, Hq, Hkv, d, L->blk, k, L->scale,
                                  out + (size_t)b0 * Hq * d, L->attn_ws, L->attn_ws_bytes, stream);
         if (st) return st;
         if ((st = record(events, 7 * p + 6, s))) return st;
@@ -346,7 +347,8 @@ extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache
             return st;
         if ((st = record(events, 7 * p + 5, s))) return st;
         st = ss_sparse_attention(q8 + (size_t)b0 * Hq * d * 2, L->cache_base, L->cache_off_dev + b0 * Hkv,
-                                 L->slots_dev + row0, L->slot_limit, Bp, Hq, Hkv, d, L->blk, k, L->scale,
+                                 L->slots_dev + row0, L->capacity_dev ? L->capacity_dev + b0 * Hkv : nullptr,
+                                 L->slot_limit, Bp, Hq, Hkv, d, L->blk, k, L->scale,
                                  out + (size_t)b0 * Hq * d, L->attn_ws, L->attn_ws_bytes, stream);
         if (st) return st;
         if ((st = record(events, 7 * p + 6, s))) return st;

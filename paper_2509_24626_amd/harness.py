@@ -76,8 +76,8 @@ class HbmLayer:
 
     def attend(self, q, slots=None):
         c = self.cfg
-        ss.ss_sparse_attention(q, self.kv, self.unit_off, self.sel if slots is None else slots, c.nblk_max, c.B,
-                               c.Hq, c.Hkv, D, c.blk, c.k, 1.0 / math.sqrt(D), self.out, self.ws, self.ws_bytes)
+        ss.ss_sparse_attention(q, self.kv, self.unit_off, self.sel if slots is None else slots, None, c.nblk_max,
+                               c.B, c.Hq, c.Hkv, D, c.blk, c.k, 1.0 / math.sqrt(D), self.out, self.ws, self.ws_bytes)
 
     def step(self, q):
         self.select(q)

@@ -117,12 +117,12 @@ def run_metadata(ss, w, stream=None):
     return meta
 
 
-def run_attention(ss, w, slots_dev, slot_limit=None):
+def run_attention(ss, w, slots_dev, slot_limit=None, capacity=None):
     out = torch.empty(w.B, w.Hq, w.d, dtype=torch.float32, device="cuda")
     wsb = ss.ss_sparse_attention_workspace(w.B, w.Hq, w.Hkv, w.d, w.blk, slots_dev.shape[-1])
     ws = torch.empty(max(wsb, 4), dtype=torch.uint8, device="cuda")
-    ss.ss_sparse_attention(w.q, w.kv, w.unit_off, slots_dev, w.nblk_max if slot_limit is None else slot_limit, w.B,
-                           w.Hq, w.Hkv, w.d, w.blk, slots_dev.shape[-1], 1.0 / math.sqrt(w.d), out, ws, wsb)
+    ss.ss_sparse_attention(w.q, w.kv, w.unit_off, slots_dev, capacity, w.nblk_max if slot_limit is None else slot_limit,
+                           w.B, w.Hq, w.Hkv, w.d, w.blk, slots_dev.shape[-1], 1.0 / math.sqrt(w.d), out, ws, wsb)
     return out
 
 

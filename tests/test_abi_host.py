@@ -25,7 +25,7 @@ def declared_functions():
 def test_library_builds_and_loads():
     assert os.path.exists(ss.LIB_PATH)
     header = open(os.path.join(ROOT, "include", "sparseserve.h")).read()
-    assert ss.ss_abi_version() == int(re.search(r"#define SS_ABI_VERSION (\d+)", header).group(1)) == 2
+    assert ss.ss_abi_version() == int(re.search(r"#define SS_ABI_VERSION (\d+)", header).group(1)) == 3
 
 
 def test_every_declared_symbol_is_exported():
@@ -63,9 +63,9 @@ def test_unsupported_shapes_rejected():
     expect(ss.SS_ERR_INVALID_ARG, ss.ss_select_topk, FAKE, FAKE, 1, 1, 16, 0, FAKE, 0)  # k = 0
     expect(ss.SS_ERR_UNSUPPORTED, ss.ss_gather_blocks, FAKE, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 1000, 0)
     expect(ss.SS_ERR_INVALID_ARG, ss.ss_gather_blocks, FAKE + 4, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8192, 0)
-    expect(ss.SS_ERR_UNSUPPORTED, ss.ss_sparse_attention, FAKE, FAKE, FAKE, FAKE, 8, 1, 8, 2, 64, 16, 4, 0.1, FAKE,
+    expect(ss.SS_ERR_UNSUPPORTED, ss.ss_sparse_attention, FAKE, FAKE, FAKE, FAKE, None, 8, 1, 8, 2, 64, 16, 4, 0.1, FAKE,
            0, 0, 0)
-    expect(ss.SS_ERR_INVALID_ARG, ss.ss_sparse_attention, FAKE, FAKE, FAKE, FAKE, 8, 1, 8, 2, 128, 16, 4,
+    expect(ss.SS_ERR_INVALID_ARG, ss.ss_sparse_attention, FAKE, FAKE, FAKE, FAKE, None, 8, 1, 8, 2, 128, 16, 4,
            float("nan"), FAKE, 0, 0, 0)
 
 
@@ -81,7 +81,7 @@ def test_empty_work_is_a_no_op():
     ss.ss_score_blocks(None, None, None, 0, 8, 2, 16, 128, None, 0)
     ss.ss_select_topk(None, None, 0, 2, 16, 4, None, 0)
     ss.ss_gather_blocks(None, 0, None, None, None, None, None, None, 1, 1, 8192, 0)
-    ss.ss_sparse_attention(None, None, None, None, 8, 0, 8, 2, 128, 16, 4, 0.1, None, None, 0, 0)
+    ss.ss_sparse_attention(None, None, None, None, None, 8, 0, 8, 2, 128, 16, 4, 0.1, None, None, 0, 0)
 
 
 def test_score_topk_workspace_sizes():
@@ -97,7 +97,7 @@ def test_attention_workspace_sizes():
     w = ss.ss_sparse_attention_workspace(32, 32, 8, 128, 16, 128)
     assert w > 0 and w % (4 * 130) == 0
     assert ss.ss_sparse_attention_workspace(1, 8, 2, 64, 16, 16) == 0  # unsupported -> 0
-    expect(ss.SS_ERR_OOM, ss.ss_sparse_attention, FAKE, FAKE, FAKE, FAKE, 2048, 32, 32, 8, 128, 16, 128, 0.1, FAKE,
+    expect(ss.SS_ERR_OOM, ss.ss_sparse_attention, FAKE, FAKE, FAKE, FAKE, FAKE, 2048, 32, 32, 8, 128, 16, 128, 0.1, FAKE,
            FAKE, w - 1, 0)
 
 

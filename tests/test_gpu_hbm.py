@@ -279,6 +279,34 @@ def test_attention_skips_invalid_slots(ss, oracle_impl):
     assert np.all(out[0, 1] == 0)  # every entry skipped -> zero output
 
 
+def test_attention_bounds_slots_by_unit_capacity(ss, oracle_impl):
+    """With per-unit capacities, a slot at or above its unit's own capacity
+    is skipped even when it lies below slot_limit.  The over-capacity slots
+    sit in units that are not last, so each one addresses bytes inside the
+    allocation (in the unit's 64-record region): reading it would not fault,
+    and would change the output."""
+    w = workload("gqa1-blk32")  # B=2, Hq=Hkv=4, blk 32, 64 records per unit, k=8
+    cap = np.array([64, 10, 0, 30, 64, 5, 64, 20], np.int32)
+    slots = np.array([[[3, 9, 7, 40, 0, 63, 62, 5],
+                       [9, 10, 11, 40, 0, 1, 2, -1],
+                       [0, 1, 2, 3, 4, 5, 6, 7],
+                       [29, 30, 31, 50, 1, -1, 2, 3]],
+                      [[1, 2, 3, 4, 5, 6, 64, 65],
+                       [4, 5, 6, 7, 8, 0, 1, 63],
+                       [10, -1, 11, -1, 12, -1, 13, 60],
+                       [19, 20, 21, 0, 22, 1, 2, 3]]], np.int32)
+    assert np.any((slots >= cap.reshape(2, 4, 1)) & (slots < 64))
+    out = gu.run_attention(ss, w, torch.from_numpy(slots).cuda(), slot_limit=64,
+                           capacity=torch.from_numpy(cap).cuda()).cpu().numpy()
+    ora_slots = np.where((slots >= cap.reshape(2, 4, 1)) | (slots >= 64), -1, slots)
+    ref = oracle_impl.attention(w.q_host, w.kv_host, w.unit_off_host, ora_slots, w.Hkv, w.blk)
+    assert np.abs(out - ref).max() <= gu.ATTN_TOL
+    assert np.all(out[0, 2] == 0)  # capacity 0: every entry skipped
+    # without the capacities the same slots are read (the bound is what skips them)
+    out_nocap = gu.run_attention(ss, w, torch.from_numpy(slots).cuda(), slot_limit=64).cpu().numpy()
+    assert np.abs(out_nocap[0, 1] - ref[0, 1]).max() > 1e-3
+
+
 def test_runs_are_bitwise_deterministic(ss):
     w = workload("gqa7-blk8-ragged")
     meta = gu.run_metadata(ss, w)
