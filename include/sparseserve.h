@@ -118,8 +118,10 @@ ss_status ss_build_metadata(const void *kv_base, const int64_t *unit_off, const 
 #define SS_AGG_SUM 1     /* ... their sum (ranks as their mean does) */
 
 /* Mean-key metadata, the variant the paper cites first in Section 2.2: per
- * block and channel, the mean of K over the blk tokens, summed in fp32 in
- * token order, scaled by 1/blk and rounded to bf16 (nearest, ties to even).
+ * block and channel, the mean of K over the blk tokens rounded once to the
+ * nearest bf16 (ties to even).  The keys are summed in fp64 in token order,
+ * which is exact unless a block's keys span more than about 2^40 in
+ * magnitude, and scaled by 1/blk (exact).
  * Arguments as ss_build_metadata, except meta: device bf16
  * [B][Hkv][nblk_max][d] (4-byte aligned). */
 ss_status ss_build_metadata_mean(const void *kv_base, const int64_t *unit_off, const int32_t *nblk, int B, int Hkv,

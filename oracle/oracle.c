@@ -637,18 +637,42 @@ int oracle_schedule(const int64_t *ws, int n, int64_t m_avl, int32_t *admit, int
 /* ------------------------------------------------------------------------
  * O11  Mean-key block metadata (Section 2.2: the simplest metadata of the
  * DSAs the paper cites is the mean of the block's token keys).  One d-vector
- * per block, bf16.  The mean is rounded to bf16, a quantisation decision, so
- * it is taken in the precision a GPU kernel works in: the channel's keys are
- * summed in fp32 in token order, the sum divided by blk (a power of two, so
- * exactly), and the result rounded to the nearest bf16, ties to even.
+ * per block, bf16: per channel, the exact mean of the blk keys, rounded once
+ * to the nearest bf16 (ties to even).
+ * The keys are summed in fp64 in token order.  Each key is a bf16 value (8
+ * significant bits), so the sum is exact whenever the keys' magnitudes span
+ * less than about 2^40; every addition is checked with an error-free
+ * transformation, and a block whose sum would be rounded is refused (return
+ * 2) rather than given an inexact mean.  Dividing by blk is exact for any
+ * blk that is a power of two; otherwise the quotient is rounded to fp64
+ * first.
  * meta layout [B*Hkv][nblk_max][d]; blocks j >= nblk[b] are not written.
  * ---------------------------------------------------------------------- */
-static uint16_t f32_to_bf16_rne(float f)
+
+/* The bf16 value nearest to x, ties to the even significand, from the
+ * definition: bf16 carries 8 significant bits down to its smallest normal
+ * 2^-126 and a fixed quantum of 2^-133 below it, with the same exponent
+ * range as fp32.  x is scaled to that quantum (a power of two, so exactly),
+ * rounded to an integer with ties to even (nearbyint in the default
+ * rounding mode), and scaled back; the result is exactly representable in
+ * fp32, whose upper 16 bits are the bf16 pattern. */
+static uint16_t bf16_nearest(double x)
 {
+    if (x == 0.0)
+        return signbit(x) ? 0x8000u : 0u;
+    int e;
+    (void)frexp(x, &e);          /* |x| in [2^(e-1), 2^e) */
+    int qexp = e - 8;            /* quantum of an 8-bit significand */
+    if (qexp < -133)
+        qexp = -133;             /* subnormal range */
+    double r = ldexp(nearbyint(ldexp(x, -qexp)), qexp);
+    if (fabs(r) >= ldexp(1.0, 128))
+        return x > 0 ? 0x7F80u : 0xFF80u;  /* beyond the largest finite value */
+    float f = (float)r;          /* exact */
     uint32_t u;
     memcpy(&u, &f, sizeof u);
-    uint32_t lsb = (u >> 16) & 1u;
-    u += 0x7FFFu + lsb;
+    if (r == 0.0)                /* rounded to zero: keep the sign of x */
+        return signbit(x) ? 0x8000u : 0u;
     return (uint16_t)(u >> 16);
 }
 
@@ -666,10 +690,18 @@ int oracle_build_metadata_mean(const void *base, const int64_t *unit_off, const 
                 const uint16_t *rec = (const uint16_t *)(unit_base + (int64_t)j * (int64_t)record_bytes);
                 uint16_t *m = meta + ((int64_t)u * nblk_max + j) * d;
                 for (int c = 0; c < d; ++c) {
-                    float s = 0.0f;
-                    for (int t = 0; t < blk; ++t)
-                        s = s + (float)bf(rec[t * d + c]);
-                    m[c] = f32_to_bf16_rne(s / (float)blk);
+                    double s = 0.0;
+                    for (int t = 0; t < blk; ++t) {
+                        double v = bf(rec[t * d + c]);
+                        double sum = s + v;
+                        /* error of this addition (Knuth's two-sum); 0 iff exact */
+                        double vv = sum - s;
+                        double err = (s - (sum - vv)) + (v - vv);
+                        if (err != 0.0)
+                            return 2;
+                        s = sum;
+                    }
+                    m[c] = bf16_nearest(s / (double)blk);
                 }
             }
         }

@@ -8,7 +8,7 @@
 // block's last row, the wave takes the channel-wise min/max of the tile's K
 // rows (rows written by earlier launches, plus the new row from registers)
 // and writes the block's metadata row; for mean-key metadata it sums the
-// rows in fp32 in token order instead.  After all heads, one thread
+// rows in fp64 in token order instead and rounds the mean once to bf16.  After all heads, one thread
 // advances the sequence's token count and, on a fill, its block count; only
 // this workgroup touches them, so there is no race.  The work is a few
 // hundred bytes per head: the kernel is latency-bound by design and runs on
@@ -50,19 +50,19 @@ __global__ __launch_bounds__(WAVES * 64) void append_kernel(const uint32_t *__re
         vt[(2 * lane) * BLK + p] = (uint16_t)(v2 & 0xFFFFu);
         vt[(2 * lane + 1) * BLK + p] = (uint16_t)(v2 >> 16);
         if (record_meta && KIND == SS_META_MEAN) {
-            // the block's keys summed in fp32 in token order (the new token is the last row)
+            // the block's keys summed in fp64 in token order (the new token is the last row)
             const uint32_t *rows = reinterpret_cast<const uint32_t *>(rec);
-            float s0 = 0.0f, s1 = 0.0f;
+            double s0 = 0.0, s1 = 0.0;
 #pragma unroll 4
             for (int t = 0; t < BLK - 1; ++t) {
                 const uint32_t w = rows[t * (D / 2) + lane];
-                s0 = s0 + __uint_as_float(w << 16);
-                s1 = s1 + __uint_as_float(w & 0xFFFF0000u);
+                s0 = s0 + (double)__uint_as_float(w << 16);
+                s1 = s1 + (double)__uint_as_float(w & 0xFFFF0000u);
             }
-            s0 = s0 + __uint_as_float(k2 << 16);
-            s1 = s1 + __uint_as_float(k2 & 0xFFFF0000u);
+            s0 = s0 + (double)__uint_as_float(k2 << 16);
+            s1 = s1 + (double)__uint_as_float(k2 & 0xFFFF0000u);
             uint32_t *m = reinterpret_cast<uint32_t *>(meta + (u * nblk_max + j) * (size_t)(D * 2));
-            m[lane] = ss::pack_bf16_rne(s0 * (1.0f / BLK), s1 * (1.0f / BLK));
+            m[lane] = ss::pack_bf16_rne_f64(s0 * (1.0 / BLK), s1 * (1.0 / BLK));
         } else if (record_meta) {
             uint32_t lo0 = key16(k2 & 0xFFFFu), lo1 = key16(k2 >> 16);
             uint32_t hi0 = lo0, hi1 = lo1;

@@ -80,6 +80,26 @@ __device__ __forceinline__ uint32_t pack_bf16_rne(float a, float b)
     y += 0x7FFFu + ((y >> 16) & 1u);
     return (x >> 16) | (y & 0xFFFF0000u);
 }
+
+// fp64 -> fp32 rounded to odd: truncated toward zero, with the lowest
+// significand bit set if anything was cut off.  fp32 keeps 16 more
+// significand bits than bf16 (at every exponent, subnormals included), so
+// rounding this value to bf16, nearest-even, gives the bf16 nearest to the
+// fp64 value: one rounding, no double-rounding error.
+__device__ __forceinline__ float f64_to_f32_odd(double x)
+{
+    const float f = __double2float_rz(x);
+    uint32_t u = __float_as_uint(f);
+    if ((double)f != x) u |= 1u;
+    return __uint_as_float(u);
+}
+
+// two finite fp64 values rounded once to bf16 (nearest, ties to even),
+// packed low then high
+__device__ __forceinline__ uint32_t pack_bf16_rne_f64(double a, double b)
+{
+    return pack_bf16_rne(f64_to_f32_odd(a), f64_to_f32_odd(b));
+}
 }  // namespace ss
 
 // 8 x bf16 operand fragment of v_mfma_f32_16x16x32_bf16 and its fp32 accumulator.

@@ -119,9 +119,10 @@ __global__ __launch_bounds__(256) void meta_kernel(const uint8_t *__restrict__ k
 }
 
 // Mean key of each block: one wave per block record, each lane two
-// channels; rows are summed in fp32 in token order (each wave-wide load is
-// one contiguous 256-byte row), scaled by 1/blk (exact) and rounded to bf16,
-// ties to even.
+// channels; rows are summed in fp64 in token order (each wave-wide load is
+// one contiguous 256-byte row; the sum of blk bf16 keys is exact unless
+// their magnitudes span more than about 2^40), scaled by 1/blk (exact) and
+// rounded once to bf16, ties to even.
 template <int BLK>
 __global__ __launch_bounds__(256) void meta_mean_kernel(const uint8_t *__restrict__ kv_base,
                                                         const int64_t *__restrict__ unit_off,
@@ -142,13 +143,13 @@ __global__ __launch_bounds__(256) void meta_mean_kernel(const uint8_t *__restric
     uint32_t w[BLK];
 #pragma unroll
     for (int t = 0; t < BLK; ++t) w[t] = reinterpret_cast<const uint32_t *>(rec + t * row_stride)[lane];
-    float s0 = 0.0f, s1 = 0.0f;
+    double s0 = 0.0, s1 = 0.0;
 #pragma unroll
     for (int t = 0; t < BLK; ++t) {
-        s0 = s0 + __uint_as_float(w[t] << 16);
-        s1 = s1 + __uint_as_float(w[t] & 0xFFFF0000u);
+        s0 = s0 + (double)__uint_as_float(w[t] << 16);
+        s1 = s1 + (double)__uint_as_float(w[t] & 0xFFFF0000u);
     }
-    meta[(u * nblk_max + j) * (D / 2) + lane] = ss::pack_bf16_rne(s0 * (1.0f / BLK), s1 * (1.0f / BLK));
+    meta[(u * nblk_max + j) * (D / 2) + lane] = ss::pack_bf16_rne_f64(s0 * (1.0 / BLK), s1 * (1.0 / BLK));
 }
 
 }  // namespace

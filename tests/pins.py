@@ -713,22 +713,72 @@ def pin_meta_mean_exact_cases(O):
         np.testing.assert_array_equal(meta[1, 1, 2], Kb[1, 1, 2, 0])
 
 
+def _bf16_nearest_exact(x):
+    """bf16 bits of the rational x rounded to the nearest bf16, ties to the
+    even significand, in exact rational arithmetic (fractions): 8
+    significant bits above 2^-126, a fixed quantum of 2^-133 below."""
+    from fractions import Fraction
+    x = Fraction(x)
+    if x == 0:
+        return 0
+    a = abs(x)
+    e = a.numerator.bit_length() - a.denominator.bit_length()  # floor(log2 a) is e or e - 1
+    if Fraction(2) ** e > a:
+        e -= 1
+    q = Fraction(2) ** max(e - 7, -133)
+    r = round(a / q) * q  # Fraction rounding: half to even
+    bits = int(np.array(float(r), np.float32).view(np.uint32)) >> 16
+    return bits | (0x8000 if x < 0 else 0)
+
+
 def pin_meta_mean_rounding(O):
-    """Random keys: the mean key is the exact mean rounded to bf16, except
-    where the exact mean lies within fp32 rounding of a bf16 rounding
-    midpoint (then it may be the neighbour)."""
-    B, Hkv, nmax, blk, d = 1, 4, 64, 16, 128
+    """Random keys: every mean key equals the exact mean (a rational sum of
+    the bf16 keys over blk) rounded once to the nearest bf16, computed here
+    in exact rational arithmetic; no entry may differ."""
+    from fractions import Fraction
+    B, Hkv, nmax, blk, d = 1, 2, 16, 16, 128
     Kb = rand_bf16((B, Hkv, nmax, blk, d), 42)
+    Kb[0, 1, 3] = rand_bf16((blk, d), 43, scale=1e-4)  # small keys: other exponents
     rec = make_records(Kb, rand_bf16((B, Hkv, nmax, blk, d), 50))
     meta = O.build_metadata_mean(rec, dense_offsets(B * Hkv, nmax, blk, d), np.array([nmax], np.int32), B, Hkv,
                                  nmax, blk, d)
-    exact = bits_to_f64(Kb).mean(axis=3)
-    want = _bf16_rne_from_f64(exact)
-    diff = meta != want
-    assert diff.mean() < 1e-3
-    got = bits_to_f64(meta)
-    ulp = np.abs(bits_to_f64(want) - bits_to_f64(want ^ 1))  # spacing near the value
-    assert np.all(np.abs(got - exact) <= 0.5 * ulp * (1 + 2.0 ** -7) + 1e-30)
+    Kf = bits_to_f64(Kb)
+    for g in range(Hkv):
+        for j in range(nmax):
+            for c in range(d):
+                exact = sum((Fraction(float(v)) for v in Kf[0, g, j, :, c]), Fraction(0)) / blk
+                assert int(meta[0, g, j, c]) == _bf16_nearest_exact(exact), (g, j, c)
+
+
+def pin_meta_mean_fixture(O):
+    """Hand-worked fixture (golden/mean_key_rounding.txt): a mean just above
+    a rounding midpoint (where rounding through fp32 first would tie the
+    other way), exact midpoints tying to even both ways, and a negative
+    mean."""
+    fx = read_fixture("mean_key_rounding.txt")
+    blk = int(fx["blk"][0])
+    rows = [[float(x) for x in fx["token_0_to_29"]]] * 30 + [[float(x) for x in fx["token_30"]],
+                                                              [float(x) for x in fx["token_31"]]]
+    assert len(rows) == blk
+    Kb = f64_to_bits(np.array(rows))[None, None, None]  # [1][1][1][blk][d]
+    assert np.array_equal(bits_to_f64(Kb)[0, 0, 0], np.array(rows))  # every input is a bf16 value
+    d = Kb.shape[-1]
+    meta = O.build_metadata_mean(make_records(Kb, Kb), np.zeros(1, np.int64), np.array([1], np.int32), 1, 1, 1, blk,
+                                 d)
+    np.testing.assert_array_equal(bits_to_f64(meta[0, 0, 0]), [float(x) for x in fx["mean_key"]])
+
+
+def pin_meta_mean_refuses_inexact(O):
+    """Keys whose magnitudes are too far apart for an exact fp64 sum (2^100
+    and 2^-100) are refused instead of given a rounded mean."""
+    Kf = np.zeros((1, 1, 1, 2, 2))
+    Kf[0, 0, 0, :, 0] = [2.0 ** 100, 2.0 ** -100]
+    Kb = f64_to_bits(Kf)
+    try:
+        O.build_metadata_mean(make_records(Kb, Kb), np.zeros(1, np.int64), np.array([1], np.int32), 1, 1, 1, 2, 2)
+    except RuntimeError:
+        return
+    raise AssertionError("an inexact fp64 sum was accepted")
 
 
 def pin_score_variant_fixture(O):
@@ -833,7 +883,8 @@ GROUPS = {
     "append": [pin_append_record_layout, pin_append_ragged_positions, pin_append_capacity_error],
     "save": [pin_save_spans_blocks, pin_save_full_block_record, pin_save_capacity_error],
     "ws": [pin_ws_fixture, pin_ws_bruteforce, pin_ws_closed_forms],
-    "meta_mean": [pin_meta_mean_exact_cases, pin_meta_mean_rounding],
+    "meta_mean": [pin_meta_mean_exact_cases, pin_meta_mean_rounding, pin_meta_mean_fixture,
+                  pin_meta_mean_refuses_inexact],
     "prefill_plan": [pin_prefill_plan_fixture, pin_prefill_plan_invariants],
     "score_variant": [pin_score_variant_fixture, pin_score_mean_is_mean_of_dots, pin_score_aggregations_reduce_to_heads],
     "schedule": [pin_schedule_fixture, pin_schedule_invariants],

@@ -108,13 +108,51 @@ def test_scores_and_selection(ss, oracle_impl, name):
 
 @pytest.mark.parametrize("name", list(CASES))
 def test_metadata_mean_bitexact(ss, oracle_impl, name):
-    """Mean-key metadata: fp32 token-order sums rounded to bf16, bit-exact."""
+    """Mean-key metadata: the exact mean of each block's keys rounded once to bf16, bit-exact."""
     w = workload(name)
     meta = torch.empty(w.B, w.Hkv, w.nblk_max, w.d, dtype=torch.int16, device="cuda")
     ss.ss_build_metadata_mean(w.kv, w.unit_off, w.nblk, w.B, w.Hkv, w.nblk_max, w.blk, w.d, meta)
     torch.cuda.synchronize()
     om = oracle_impl.build_metadata_mean(w.kv_host, w.unit_off_host, w.nblk_host, w.B, w.Hkv, w.nblk_max, w.blk, w.d)
     valid_rows_equal(gu.u16(meta), om, w.nblk_host)
+
+
+def test_metadata_mean_rounds_once(ss):
+    """The hand-worked mean-key fixture (golden/mean_key_rounding.txt) on the
+    GPU, through ss_build_metadata_mean and through the fill path of
+    ss_append_kv: a mean 2^-25 above a rounding midpoint (which a rounding
+    through fp32 would tie the other way), exact midpoints tying to even
+    both ways, and a negative mean.  The fixture's 4 channels repeat over
+    the 128."""
+    import pins
+    fx = pins.read_fixture("mean_key_rounding.txt")
+    blk, d = int(fx["blk"][0]), 128
+    rows = [[float(x) for x in fx["token_0_to_29"]]] * 30 + [[float(x) for x in fx["token_30"]],
+                                                              [float(x) for x in fx["token_31"]]]
+    K = torch.tensor(np.tile(np.array(rows), (1, d // 4)), dtype=torch.float32).to(torch.bfloat16)  # [blk][d]
+    assert torch.equal(K.float(), torch.tensor(np.tile(np.array(rows), (1, d // 4)), dtype=torch.float32))
+    want = np.tile(np.array([float(x) for x in fx["mean_key"]]), d // 4)
+    rec = torch.zeros(2 * blk * d, dtype=torch.bfloat16)
+    rec[:blk * d] = K.reshape(-1)
+    rec = rec.cuda()
+    one = torch.ones(1, dtype=torch.int32, device="cuda")
+    meta = torch.zeros(1, 1, 1, d, dtype=torch.int16, device="cuda")
+    ss.ss_build_metadata_mean(rec, torch.zeros(1, dtype=torch.int64, device="cuda"), one, 1, 1, 1, blk, d, meta)
+    got = meta.view(torch.bfloat16).float().cpu().numpy().reshape(-1)
+    np.testing.assert_array_equal(got, want)
+    # the same block filled token by token: its metadata row is written by the append of token 31
+    length = torch.zeros(1, dtype=torch.int32, device="cuda")
+    nblk = torch.zeros(1, dtype=torch.int32, device="cuda")
+    open_rec = torch.zeros(1, 1, 2 * blk * d, dtype=torch.int16, device="cuda")
+    meta2 = torch.zeros(1, 1, 1, d, dtype=torch.int16, device="cuda")
+    for t in range(blk):
+        kv = torch.zeros(1, 1, 2, d, dtype=torch.bfloat16)
+        kv[0, 0, 0] = K[t]
+        ss.ss_append_kv(kv.cuda(), length, nblk, 1, 1, blk, d, 1, open_rec, meta2, None, meta_kind=ss.SS_META_MEAN)
+    torch.cuda.synchronize()
+    assert int(nblk.item()) == 1 and int(length.item()) == blk
+    got2 = meta2.view(torch.bfloat16).float().cpu().numpy().reshape(-1)
+    np.testing.assert_array_equal(got2, want)
 
 
 @pytest.mark.parametrize("kind,agg", [(0, 1), (1, 0), (1, 1)], ids=["cuboid-sum", "mean-max", "mean-sum"])

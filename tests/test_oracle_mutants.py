@@ -79,12 +79,20 @@ MUTANTS = [
     ("schedule-strict", "schedule", "if (used + ws[i] <= m_avl) {", "if (used + ws[i] < m_avl) {"),
     ("schedule-stops-at-first-reject", "schedule", "            admit[i] = 0;\n",
      "            admit[i] = 0;\n            m_avl = -1;\n"),
-    ("mean-divides-by-blk-minus-1", "meta_mean", "m[c] = f32_to_bf16_rne(s / (float)blk);",
-     "m[c] = f32_to_bf16_rne(s / (float)(blk > 1 ? blk - 1 : 1));"),
-    ("mean-skips-first-token", "meta_mean", "for (int t = 0; t < blk; ++t)\n                        s = s +",
-     "for (int t = 1; t < blk; ++t)\n                        s = s +"),
-    ("mean-truncates", "meta_mean", "    u += 0x7FFFu + lsb;\n", "    u += 0u * lsb;\n"),
-    ("mean-reads-v", "meta_mean", "s = s + (float)bf(rec[t * d + c]);", "s = s + (float)bf(rec[blk * d + c * blk + t]);"),
+    ("mean-divides-by-blk-minus-1", "meta_mean", "m[c] = bf16_nearest(s / (double)blk);",
+     "m[c] = bf16_nearest(s / (double)(blk > 1 ? blk - 1 : 1));"),
+    ("mean-skips-first-token", "meta_mean", "for (int t = 0; t < blk; ++t) {\n                        double v = bf(",
+     "for (int t = 1; t < blk; ++t) {\n                        double v = bf("),
+    ("mean-truncates", "meta_mean", "double r = ldexp(nearbyint(ldexp(x, -qexp)), qexp);",
+     "double r = ldexp(trunc(ldexp(x, -qexp)), qexp);"),
+    ("mean-ties-away-from-zero", "meta_mean", "double r = ldexp(nearbyint(ldexp(x, -qexp)), qexp);",
+     "double r = ldexp(round(ldexp(x, -qexp)), qexp);"),
+    ("mean-rounds-through-fp32", "meta_mean", "m[c] = bf16_nearest(s / (double)blk);",
+     "m[c] = bf16_nearest((double)(float)(s / (double)blk));"),
+    ("mean-nine-bit-significand", "meta_mean", "int qexp = e - 8;", "int qexp = e - 9;"),
+    ("mean-accepts-inexact-sums", "meta_mean", "                        if (err != 0.0)\n                            return 2;\n",
+     ""),
+    ("mean-reads-v", "meta_mean", "double v = bf(rec[t * d + c]);", "double v = bf(rec[blk * d + c * blk + t]);"),
     ("variant-mean-reads-hi", "score_variant", "s += bf(qh[c]) * bf(mj[c]);", "s += bf(qh[c]) * bf(mj[d + c]);"),
     ("variant-sum-is-max", "score_variant", "= agg == 0 ? best : total;", "= best;"),
     ("variant-sum-drops-last-head", "score_variant", "                    total += s;\n",
@@ -125,15 +133,23 @@ def test_mutant_is_caught(mid, group, pattern, repl, src):
         child = ctx.Process(target=_run_group, args=(lib, group))
         child.start()
         child.join(120)
-        if child.is_alive():
+        hung = child.is_alive()
+        if hung:
             child.kill()
             child.join()
+        # a child that hangs has not shown anything: only a pin failure or a
+        # crash counts as catching the mistake
+        assert not hung, f"pins of {group} did not finish for planted mistake {mid}"
         assert child.exitcode != 0, f"planted mistake {mid} passed every {group} pin"
 
 
 def _run_group(lib, group):
     import faulthandler
     faulthandler.disable()  # a crashing mutant is an expected outcome here
+    # the parent's intra-op thread pool does not survive fork(): run torch's
+    # CPU ops of the pins on this thread only
+    import torch
+    torch.set_num_threads(1)
     O = oracle.Oracle(oracle.load(lib))
     for pin in pins.GROUPS[group]:
         try:
