@@ -65,6 +65,7 @@ typedef int ss_status;
 #define SS_ERR_CAPACITY 3    /* a unit selects more blocks than it has cache slots */
 #define SS_ERR_OOM 4         /* host allocation failed, or a caller buffer is too small */
 #define SS_ERR_HIP 5         /* a HIP runtime call or kernel launch failed */
+#define SS_ERR_TIMEOUT 6     /* the host waited longer than its deadline for GPU work */
 
 #define SS_ABI_VERSION 3
 
@@ -466,8 +467,9 @@ ss_status ss_prefill_plan(int64_t T, int layers, int64_t max_inject, int32_t *it
  * itself (its start and end of execution, as ss_time_next_kernel does), and
  * events[7p+5..6] are recorded on `stream` before and after attention.
  * Streams and events are created for the device current at the call.
- * On error nothing further is enqueued; a resolve error leaves the cache
- * unchanged for the groups not yet resolved. */
+ * On error nothing further is enqueued; a resolve error or a wait past the
+ * deadline (ss_set_host_wait_timeout) leaves the cache unchanged for the
+ * groups not yet resolved. */
 typedef struct ss_layer_buffers {
     int B, Hq, Hkv, d, blk, nblk_max, k;
     float scale;
@@ -494,6 +496,14 @@ typedef struct ss_layer_buffers {
 
 ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, const void *q, float *out, void *stream,
                           void *const *events, int64_t *n_miss);
+
+/* Deadline of ss_decode_layer's host waits for a group's selection, in
+ * milliseconds, for every thread of the process (default 10000; ms <= 0
+ * restores it).  When a wait passes it, the call returns SS_ERR_TIMEOUT
+ * with the group and step in ss_last_error(): the work already enqueued
+ * stays enqueued and the block cache is unchanged for the groups not yet
+ * resolved, so the caller synchronises the device before going on. */
+ss_status ss_set_host_wait_timeout(int64_t ms);
 
 /* The decode step with the resolve on the GPU (ss_dev_cache, which takes
  * the place of L->cache; the host buffers sel_host, slots_host and

@@ -22,6 +22,7 @@ SS_ERR_UNSUPPORTED = 2
 SS_ERR_CAPACITY = 3
 SS_ERR_OOM = 4
 SS_ERR_HIP = 5
+SS_ERR_TIMEOUT = 6
 
 
 class SparseServeError(RuntimeError):
@@ -94,6 +95,7 @@ _SIGNATURES = {
     "ss_dev_cache_export": (_i32, [_vp, _vp, _vp]),
     "ss_dev_cache_total_misses": (_i32, [_vp, _vp]),
     "ss_decode_layer_dev": (_i32, [ctypes.POINTER(ss_layer_buffers), _vp, _i64, _vp, _vp, _vp, _vp]),
+    "ss_set_host_wait_timeout": (_i32, [_i64]),
 }
 
 
@@ -264,6 +266,10 @@ def ss_decode_layer(buffers, step, q, out, stream=None, events=None):
     _check(lib().ss_decode_layer(ctypes.byref(buffers), step, _ptr(q), _ptr(out), _stream(stream), ev,
                                  ctypes.byref(n)))
     return n.value
+
+
+def ss_set_host_wait_timeout(ms):
+    _check(lib().ss_set_host_wait_timeout(int(ms)))
 
 
 def ss_cache_set_blocks(handle, nblk):

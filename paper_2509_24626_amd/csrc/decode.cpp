@@ -18,6 +18,8 @@
 // previous one drains (no launch gap, no idle tail on the link).  Every hand-off is
 // a kernel on a compute queue: no copy-engine transfer, whose cross-engine
 // synchronisation costs tens of microseconds per hand-off, is on the path.
+#include <atomic>
+#include <chrono>
 #include <mutex>
 #include <new>
 #include <thread>
@@ -126,12 +128,23 @@ ss_status device_address(void *host, void **dev)
     return SS_OK;
 }
 
-ss_status wait_host(hipEvent_t ev)
+constexpr int64_t kDefaultWaitMs = 10000;
+std::atomic<int64_t> g_wait_ms{kDefaultWaitMs};
+
+// Polls until group p's selection is in host memory; a kernel that never
+// finishes makes the call fail after the deadline instead of spinning (and
+// holding g_exec_mu) for ever.
+ss_status wait_host(hipEvent_t ev, int p, int64_t step)
 {
+    const int64_t ms = g_wait_ms.load(std::memory_order_relaxed);
+    const auto deadline = std::chrono::steady_clock::now() + std::chrono::milliseconds(ms);
     for (;;) {
         hipError_t r = hipEventQuery(ev);
         if (r == hipSuccess) return SS_OK;
         if (r != hipErrorNotReady) return hip_check(r, "wait for a selection");
+        if (std::chrono::steady_clock::now() > deadline)
+            return ss::fail(SS_ERR_TIMEOUT, "ss_decode_layer: the selection of group %d at step %lld was not ready "
+                            "after %lld ms", p, (long long)step, (long long)ms);
         std::this_thread::yield();
     }
 }
@@ -218,7 +231,7 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
         // consecutive groups' gathers run on alternate transfer streams, so the
         // next gather is already streaming while the previous one drains
         hipStream_t x = ex->xfer[p & 1];
-        if ((st = wait_host(ex->sel_ready[p]))) return st;
+        if ((st = wait_host(ex->sel_ready[p], p, step))) return st;
         // miss rows of the step are kept compact: this group appends at `total`
         int64_t np = 0;
         st = ss_cache_resolve_range(L->cache, step, b0, b1, L->sel_host + row0, k, L->slots_host + row0,
@@ -353,5 +366,11 @@ extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache
         if (st) return st;
         if ((st = record(events, 7 * p + 6, s))) return st;
     }
+    return SS_OK;
+}
+
+extern "C" ss_status ss_set_host_wait_timeout(int64_t ms)
+{
+    g_wait_ms.store(ms > 0 ? ms : kDefaultWaitMs, std::memory_order_relaxed);
     return SS_OK;
 }

@@ -54,6 +54,7 @@ const char *ss_status_string(ss_status s)
     case SS_ERR_CAPACITY: return "selection exceeds cache capacity";
     case SS_ERR_OOM: return "out of memory or buffer too small";
     case SS_ERR_HIP: return "HIP runtime error";
+    case SS_ERR_TIMEOUT: return "timed out waiting for the GPU";
     default: return "unknown status";
     }
 }

@@ -23,6 +23,8 @@ int main(void)
 
     CHECK(ss_abi_version() == SS_ABI_VERSION);
     CHECK(strlen(ss_status_string(SS_OK)) > 0);
+    CHECK(strcmp(ss_status_string(SS_ERR_TIMEOUT), "unknown status") != 0);
+    CHECK(ss_set_host_wait_timeout(250) == SS_OK && ss_set_host_wait_timeout(0) == SS_OK);
 
     /* Algorithm 1 over 100 bytes: 30 fits, 50 fits (80), 10 fits (90), 40 does not */
     CHECK(ss_schedule_batch(ws, 4, 100, admit, &used) == SS_OK);

@@ -235,6 +235,48 @@ def test_hier_small_lockstep(ss, oracle_impl):
     assert 0 < np.mean(rate[1:]) < 1
 
 
+def test_decode_layer_wait_deadline(ss, oracle_impl):
+    """A host wait for a selection that passes the deadline set with
+    ss_set_host_wait_timeout returns SS_ERR_TIMEOUT and leaves the block
+    cache untouched.  The stream is held busy by ordinary work queued before
+    the step (four fp32 8192^3 products, tens of milliseconds) against a
+    2 ms deadline; after synchronising, the same step with the default
+    deadline matches the oracle, which never saw the failed call."""
+    from paper_2509_24626_amd import harness as H
+    cfg = SMALL
+    nblk = (synth.gen.lengths(cfg, 3) // cfg.blk).astype(np.int32)
+    _, total = H.pool_layout(cfg, nblk)
+    pool = H.HostPool(total)
+    try:
+        L = H.build_hier_layer(cfg, 3, 0, pool, 0, nblk, parts=2)
+        qs = H.query_stream(cfg, 3, 0, 2)
+        tr = Track(oracle_impl, cfg, L, pool, range(cfg.B), "deadline")
+        L.step(0, qs[0][1])
+        torch.cuda.synchronize()
+        tr.check(0, qs[0][1])
+        x = torch.randn(8192, 8192, device="cuda")
+        torch.cuda.synchronize()
+        ss.ss_set_host_wait_timeout(2)
+        try:
+            for _ in range(4):
+                x = x @ x * 1e-4
+            with pytest.raises(ss.SparseServeError) as e:
+                L.step(1, qs[1][1])
+            assert e.value.status == ss.SS_ERR_TIMEOUT, str(e.value)
+            assert "step 1" in str(e.value)
+        finally:
+            ss.ss_set_host_wait_timeout(0)
+        torch.cuda.synchronize()
+        for t in (1, 2):
+            L.step(t, qs[t][1])
+            torch.cuda.synchronize()
+            tr.check(t, qs[t][1])
+        assert not tr.diverged
+        L.close()
+    finally:
+        pool.close()
+
+
 @pytest.mark.parametrize("parts", [2, 3])
 def test_hier_small_pipelined_groups(ss, oracle_impl, parts):
     lockstep(oracle_impl, SMALL, seed=3, sample_b=range(SMALL.B), steps=6, parts=parts)
