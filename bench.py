@@ -9,7 +9,13 @@ decode path of that layer: block scoring, top-k selection, the host-side
 cache resolve (--resolve device runs it on the GPU instead), the gather of
 missed blocks from DRAM and sparse attention.
 Inputs are resident (pool in pinned DRAM, metadata and cache in HBM) when
-timing starts; the warm-up step fills the cold cache.
+timing starts.  The workload's cache state is fixed: the timed steps start
+from a cache that holds exactly the previous step's selection (one cold
+fill step right before them).  Warm-up steps beyond that one run first on
+a throwaway cache state, which is then emptied, so --warmup changes what is
+warmed (kernels, streams, host threads), never the timed workload.
+The same run then measures the full 32-layer decode step with ragged
+lengths (reported under "layers32"; --no-layers32 skips it).
 
 Prints one JSON line on stdout (progress goes to stderr):
   value      = B * steps / wall time of the timed steps (tokens/s)
@@ -19,7 +25,8 @@ Prints one JSON line on stdout (progress goes to stderr):
                intervals of the step's gather launches in the timed region)
   rooflines_isolated = scoring, top-k and attention each launched alone on
                the same data, against the HBM peak (8 TB/s)
-  cpu_baseline = the CPU oracle on a bounded sample of the same workload.
+  cpu_baseline = the CPU oracle on a bounded sample of the same workload
+  host       = the negotiated PCIe link of the GPU and the host's CPUs.
 """
 import argparse
 import json
@@ -44,7 +51,9 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed steps (default: the workload's)")
-    ap.add_argument("--warmup", type=int, default=1, help="untimed steps first (the first fills the cache)")
+    ap.add_argument("--warmup", type=int, default=1,
+                    help="untimed steps first: the last one fills the emptied cache (the workload's own warm-up "
+                         "step); the ones before it run on a throwaway cache state")
     ap.add_argument("--config", default="2", help="workload index or name (see synth/configs.py)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--parts", default="auto",
@@ -65,21 +74,35 @@ def parse():
     ap.add_argument("--resolve", choices=["host", "device"], default="host",
                     help="the slot-table resolve on host threads (ss_decode_layer, default) or on the GPU "
                          "(ss_decode_layer_dev)")
+    ap.add_argument("--layers32-resolve", choices=["host", "device"], default="host",
+                    help="the resolve of the 32-layer sub-record")
     ap.add_argument("--with-save", action="store_true",
                     help="every step also appends its new tokens (metadata on a fill) and saves them to DRAM "
-                         "(FlashD2H); single-layer workloads")
+                         "(FlashD2H); single-layer workloads, one warm-up step")
     ap.add_argument("--save-stream", choices=["own", "main"], default="own",
                     help="with --with-save: the FlashD2H copies on a stream of their own or on the main stream")
     ap.add_argument("--no-variants", action="store_true", help="skip the scoring-variant comparison")
     ap.add_argument("--no-working-set", action="store_true",
                     help="skip the working-set study and the batch-control comparison (Algorithm 1)")
     ap.add_argument("--no-prefill", action="store_true", help="skip the layer-segmented prefill measurement")
-    ap.add_argument("--no-save-bandwidth", action="store_true",
-                    help="skip the transfer comparisons: saving (FlashD2H, per-block copies, GPU-direct) and "
-                         "loading (the gather kernel against per-block copies)")
+    ap.add_argument("--no-save-bandwidth", action="store_true", help="skip FlashD2H saving against block size")
+    ap.add_argument("--comparisons", action="store_true",
+                    help="also time the paper's comparison transfers: one hipMemcpyAsync per block for loading "
+                         "and saving, and GPU-direct saving")
+    ap.add_argument("--no-layers32", action="store_true", help="skip the 32-layer sub-record")
     ap.add_argument("--pool-budget-gib", type=float, default=56.0,
                     help="pinned DRAM for KV records; layers beyond it reuse earlier layers' records")
     return ap.parse_args()
+
+
+def group_sizes(spec, B, H):
+    if spec == "auto":
+        return H.default_parts(B)
+    if spec.startswith("tent"):
+        return H.tent_parts(B, int(spec[4:]))
+    if "," in spec:
+        return [int(x) for x in spec.split(",")]
+    return int(spec)
 
 
 def main():
@@ -107,34 +130,90 @@ def main():
         sys.exit(2)
     ss.lib()
     cfg = synth.get(int(args.config)) if args.config.isdigit() else synth.get(args.config)
-    steps = args.steps if args.steps is not None else cfg.steps
-    warmup = max(args.warmup, 1)
     if cfg.placement != "host":
         print("bench.py times the hierarchical workloads (2, 3, 4); the all-HBM ones are parity cases",
               file=sys.stderr)
         sys.exit(2)
+    if args.with_save and (cfg.layers != 1 or args.warmup > 1):
+        print("--with-save runs single-layer workloads with one warm-up step", file=sys.stderr)
+        sys.exit(2)
+    steps = args.steps if args.steps is not None else cfg.steps
+    warmup = max(args.warmup, 1)
+    host = host_facts()
+    log(f"host: {host}")
 
-    # ------------------------------------------------------------ setup
+    run = measure(cfg, args, steps, warmup, args.resolve, args.parts, torch, ss, H, synth, studies=True)
+    result = {
+        "metric": "sparse decode-step tokens/sec at 1 GPU; % HBM roofline; gather host-link GB/s",
+        "value": run["value"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": run["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": run["config"],
+        "workload_conforms": True,
+        "warmup_note": ("the timed steps start from a cache holding exactly the previous step's selection, "
+                        "whatever --warmup is: warm-up steps before that fill step run on a throwaway cache "
+                        "state, which is emptied before the fill step"),
+        "roofline": run["roofline"],
+        "pipeline_ms": run["pipeline_ms"],
+        "step_ms_events": run["step_ms_events"],
+        "rooflines_isolated": run["rooflines_isolated"],
+        "parts": run["parts"],
+        "miss_rate": run["miss_rate"],
+        "miss_rate_per_step": run["miss_rate_per_step"],
+        "gather_GBps": run["roofline"]["achieved"],
+        "hbm_frac": {"score": run["rooflines_isolated"]["score"]["frac"],
+                     "attention": run["rooflines_isolated"]["attention"]["frac"]},
+        "metadata_build": run["metadata_build"],
+        "cpu_baseline": run.get("cpu_baseline"),
+        "host": host,
+    }
+    for key in ("save_side", "save_bandwidth", "load_comparison", "working_set", "batch_control", "score_variants",
+                "prefill"):
+        if run.get(key) is not None:
+            result[key] = run[key]
+
+    # ------------------------------------- the full 32-layer decode step
+    if cfg.layers == 1 and not args.with_save and not args.no_layers32:
+        c3 = synth.get(3)
+        sub = measure(c3, args, c3.steps, warmup, args.layers32_resolve, "auto", torch, ss, H, synth, studies=False)
+        result["layers32"] = {
+            "workload": sub["config"]["workload"], "value": sub["value"], "unit": "tokens/s",
+            "steps": c3.steps, "warmup": warmup, "ms_per_step": sub["ms_per_step"],
+            "layers": c3.layers, "layers_with_own_dram_records": sub["config"]["layers_with_own_dram_records"],
+            "resolve": args.layers32_resolve, "parts": sub["parts"], "miss_rate": sub["miss_rate"],
+            "gather": {k: sub["roofline"][k] for k in ("bound", "achieved", "peak", "unit", "frac",
+                                                        "bytes_per_step", "link_busy_ms_per_step")},
+            "pipeline_ms_per_layer": sub["pipeline_ms"], "step_ms_events": sub["step_ms_events"],
+            "rooflines_isolated": sub["rooflines_isolated"],
+            "note": ("all 32 layers in order in every step; ragged lengths U[8k, 64k]; 30% cache per layer; "
+                     "pipeline_ms is per layer (sampled on the first and last layer of every step)")}
+    print(json.dumps(result), flush=True)
+    exit_report()
+
+
+def measure(cfg, args, steps, warmup, resolve, parts_spec, torch, ss, H, synth, studies):
+    """Builds the workload, runs its warm-up, times `steps` steps and
+    measures each HBM kernel alone; with `studies` also runs the studies
+    and the CPU baseline on it.  Frees everything it allocated."""
     lens = synth.gen.lengths(cfg, args.seed)
     nblk = (lens // cfg.blk).astype(np.int32)
     _, per_layer = H.pool_layout(cfg, nblk)
-    n_distinct = H.distinct_layers(cfg, nblk, int(args.pool_budget_gib * 2**30))
+    budget = int(args.pool_budget_gib * 2**30)
+    n_distinct = H.distinct_layers(cfg, nblk, budget)
     log(f"workload {cfg.name}: {cfg.layers} layer(s), {n_distinct} with DRAM records of their own, "
         f"pool {per_layer * n_distinct / 2**30:.2f} GiB pinned")
-    meta_ms = []
-    if args.parts == "auto":
-        parts = H.default_parts(cfg.B)
-    elif args.parts.startswith("tent"):
-        parts = H.tent_parts(cfg.B, int(args.parts[4:]))
-    elif "," in args.parts:
-        parts = [int(x) for x in args.parts.split(",")]
-    else:
-        parts = int(args.parts)
+    parts = group_sizes(parts_spec, cfg.B, H)
     new_kv = None
+    res = {}
     if args.with_save:
-        if cfg.layers != 1:
-            print("--with-save runs single-layer workloads", file=sys.stderr)
-            sys.exit(2)
         reserve = (warmup + steps) // cfg.blk + 2
         off, total = H.pool_layout(cfg, nblk, reserve)
         pool = H.HostPool(total, args.pool_flags)
@@ -147,24 +226,198 @@ def main():
         new_kv = [synth.gen.new_tokens(cfg.B, cfg.Hkv, D, sK, sV, args.seed, 0, s, "cuda")
                   for s in range(warmup + steps)]
     else:
-        pool, layers, _ = H.build_hier_model(cfg, args.seed, nblk, args.pool_flags,
-                                             int(args.pool_budget_gib * 2**30), progress=log, parts=parts,
-                                             dev_cache=args.resolve == "device")
-    qstreams = [H.query_stream(cfg, args.seed, l, warmup + steps - 1) for l in range(cfg.layers)]
+        # pinned memory freed by an earlier workload of this process may not all
+        # be available again at once: a multi-layer model steps its budget down
+        for b in (budget, budget - (8 << 30), budget - (16 << 30)) if cfg.layers > 1 else (budget,):
+            try:
+                pool, layers, n_distinct = H.build_hier_model(cfg, args.seed, nblk, args.pool_flags, b,
+                                                              progress=log, parts=parts,
+                                                              dev_cache=resolve == "device")
+                break
+            except ss.SparseServeError as e:
+                if b == budget - (16 << 30) or cfg.layers == 1:
+                    raise
+                log(f"pool of {b / 2**30:.0f} GiB not available ({e}); trying a smaller one")
+    try:
+        # q index 0 is the workload's warm-up (cache fill) step, 1..steps the timed ones
+        qstreams = [H.query_stream(cfg, args.seed, l, steps) for l in range(cfg.layers)]
 
-    def run_step(L, l, s, events=None):
-        if new_kv is None:
-            L.step(s, qstreams[l][s][1], events)
-        else:
-            L.step_with_save(s, qstreams[l][s][1], new_kv[s], events)
-    # metadata build (setup path), timed on its own for one layer
-    L0 = layers[0]
+        def run_step(L, l, s, events=None):
+            if new_kv is None:
+                L.step(s, qstreams[l][s][1], events)
+            else:
+                L.step_with_save(s, qstreams[l][s][1], new_kv[s], events)
+
+        res["metadata_build"] = metadata_build_rate(cfg, pool, layers[0], nblk, ss, torch)
+
+        # --------------------------------------------------------- warm-up
+        # extra warm-up steps run on a throwaway cache state (queries of a
+        # separate stream), then every cache is emptied, so the fill step
+        # below leaves exactly its selection in the cache
+        if warmup > 1:
+            qthrow = [H.query_stream(cfg, args.seed + 1000, l, warmup - 2) for l in range(cfg.layers)]
+            for s in range(warmup - 1):
+                for l, L in enumerate(layers):
+                    L.step(s, qthrow[l][s][1])
+            torch.cuda.synchronize()
+            for L in layers:
+                L.reset_cache()
+        for l, L in enumerate(layers):
+            run_step(L, l, 0)
+        torch.cuda.synchronize()
+        log(f"warm-up done ({warmup} step(s), the last on an empty cache); timing {steps} step(s)")
+
+        # ----------------------------------------------------------- timed
+        P = layers[0].parts
+        ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(7 * P)] for _ in layers] for _ in range(steps)]
+        # every timing event is a barrier packet on its queue: events go only on the
+        # first and the last layer of a step (the step's start and end), and there
+        # only around each group's start, end and gather (the dominant kernel)
+        sampled = sorted({0, len(layers) - 1})
+        used = [False] * (7 * P)
+        used[0] = used[7 * (P - 1) + 6] = True
+        for p in range(P):
+            used[7 * p + 3] = used[7 * p + 4] = True
+        for row in ev:  # create the underlying events before timing
+            for es in row:
+                for e in es:
+                    e.record()
+        torch.cuda.synchronize()
+        n_miss = np.zeros((steps, len(layers)), np.int64)
+        dev_step = [[0] * len(layers) for _ in range(steps + 1)]
+        dev_step[0] = [ss.ss_dev_cache_total_misses(L.dev) if L.dev is not None else 0 for L in layers]
+        t0 = time.perf_counter()
+        for i in range(steps):
+            s = 1 + i
+            for l, L in enumerate(layers):
+                run_step(L, l, s, events=[e.cuda_event if used[j] else None for j, e in enumerate(ev[i][l])]
+                         if l in sampled else None)
+                n_miss[i, l] = L.last_n_miss or 0
+        if new_kv is not None:
+            for L in layers:  # the last step's save is part of the work
+                ss.ss_kv_save_wait(L.saver)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        for l, L in enumerate(layers):
+            if L.dev is not None:  # the device resolve counts its misses on the GPU: spread the total over the steps
+                n_miss[:, l] = (ss.ss_dev_cache_total_misses(L.dev) - dev_step[0][l]) / steps
+
+        # --------------------------------------------------- accounting
+        # Gathers of consecutive groups overlap (two transfer streams), so the
+        # link's busy time is the union of the gather intervals of a step.  Also
+        # per step: the ramp before the first gather starts, idle gaps inside
+        # the gather span, and the tail after the last gather ends.
+        pipe = {"ramp": [], "link_busy": [], "link_gaps": [], "tail": []}
+        gather_launch_ms = []
+        for i in range(steps):
+            for l in sampled:  # layers are alike (same lengths, shapes and drift): the sampled ones stand for all
+                e = ev[i][l]
+                iv = sorted((e[0].elapsed_time(e[7 * p + 3]), e[0].elapsed_time(e[7 * p + 4])) for p in range(P))
+                gather_launch_ms += [b - a for a, b in iv]
+                busy, cur_a, cur_b = 0.0, iv[0][0], iv[0][1]
+                for a, b in iv[1:]:
+                    if a > cur_b:
+                        busy += cur_b - cur_a
+                        cur_a, cur_b = a, b
+                    else:
+                        cur_b = max(cur_b, b)
+                busy += cur_b - cur_a
+                first, last = iv[0][0], max(b for _, b in iv)
+                pipe["ramp"].append(first)
+                pipe["link_busy"].append(busy)
+                pipe["link_gaps"].append(last - first - busy)
+                pipe["tail"].append(e[0].elapsed_time(e[7 * (P - 1) + 6]) - last)
+        pipe = {k: round(float(np.mean(v)), 4) for k, v in pipe.items()}
+        # each step on its own: from the first layer's first event to the last
+        # layer's last (GPU time; the wall-clock mean above includes host time
+        # between steps)
+        step_ms = np.array([ev[i][0][0].elapsed_time(ev[i][-1][7 * (P - 1) + 6]) for i in range(steps)])
+        units = cfg.B * cfg.Hkv
+        # the gather's algorithmic bytes per step: the missed block records (mean
+        # over the timed steps) over the host link, against the link's busy time
+        gather_bytes = float(n_miss.sum()) / steps * cfg.record_bytes
+        busy_ms = pipe["link_busy"] * len(layers)
+        ach = gather_bytes / (busy_ms * 1e-3) / 1e9 if busy_ms > 0 else 0.0
+        key = (cfg.name, args.seed, steps, tuple(layers[0].part_sizes), resolve)
+        value = cfg.B * steps / wall
+        miss_rate = float(n_miss.mean()) / (units * cfg.k)
+        log(f"{cfg.name}: {value:.0f} tokens/s, {wall / steps * 1e3:.3f} ms/step; gather {ach:.1f} GB/s; "
+            f"miss rate {miss_rate:.4f}; pipeline {pipe}")
+        res.update({
+            "value": round(value, 2), "ms_per_step": round(wall / steps * 1e3, 4),
+            "config": {"workload": cfg.name, "batch": cfg.B, "q_heads": cfg.Hq, "kv_heads": cfg.Hkv, "head_dim": D,
+                       "context": int(lens.max()), "block": cfg.blk, "topk_blocks": cfg.k,
+                       "cache_frac": cfg.cache_frac, "layers": cfg.layers,
+                       "layers_with_own_dram_records": n_distinct, "drift": cfg.drift, "seed": args.seed,
+                       "resolve": resolve},
+            "roofline": {"kernel": "gather", "bound": "host-link", "achieved": round(ach, 2),
+                         "peak": round(LINK_PEAK_GBS, 2), "unit": "GB/s", "frac": round(ach / LINK_PEAK_GBS, 4),
+                         "bytes_per_step": int(gather_bytes), "link_busy_ms_per_step": round(busy_ms, 4),
+                         "launches_per_step": len(layers) * P,
+                         "ms_per_launch": round(float(np.mean(gather_launch_ms)), 4),
+                         "traffic": traffic("gather", key)},
+            "pipeline_ms": pipe,
+            "step_ms_events": {"median": round(float(np.median(step_ms)), 4), "min": round(float(step_ms.min()), 4),
+                               "max": round(float(step_ms.max()), 4),
+                               "p90": round(float(np.percentile(step_ms, 90)), 4)},
+            "parts": layers[0].part_sizes,
+            "miss_rate": round(miss_rate, 4),
+            "miss_rate_per_step": [round(float(x), 4) for x in n_miss.mean(axis=1) / (units * cfg.k)],
+        })
+        if new_kv is not None:
+            L = layers[0]
+            res["config"]["with_save"] = True
+            res["save_side"] = {"blocks_filled_per_sequence": int((L.nblk.cpu().numpy() - nblk).max()),
+                                "overflow": int(L.overflow.item()),
+                                "note": "each timed step also appends its new tokens (metadata on a fill) and "
+                                        "saves them with FlashD2H; the last save is waited for inside the timed "
+                                        "region"}
+
+        # --------------------------------------- isolated kernel rates
+        # Each kernel alone over the whole batch (one launch, nothing else on the
+        # GPU), on the last timed step's data: the HBM kernels' own rates, which
+        # the overlapped step hides behind the host-link gather.
+        iso = isolated_rates(cfg, layers[0], qstreams[0][steps][1], ss, torch)
+        for name in iso:
+            iso[name]["traffic"] = traffic(name, key)
+        res["rooflines_isolated"] = iso
+        if not studies:
+            return res
+
+        single = new_kv is None and cfg.layers == 1
+        if single and not args.no_working_set:
+            res["working_set"] = working_set_study(cfg, layers[0], qstreams[0][-1][0], steps + 1, args.seed, ss,
+                                                   torch)
+            res["batch_control"] = batch_control_study(cfg, layers[0], pool, ss, torch, H, args.seed)
+        if single and not args.no_variants:
+            res["score_variants"] = score_variants_study(cfg, layers[0], qstreams[0][-1][1], pool, ss, torch)
+        if args.comparisons:
+            res["load_comparison"] = load_comparison(cfg, layers[0], pool, ss, torch)
+        if not args.no_save_bandwidth:
+            res["save_bandwidth"] = save_bandwidth(ss, torch, H, comparisons=args.comparisons)
+        if not args.no_prefill:
+            res["prefill"] = prefill_study(ss, torch, H)
+        if not args.no_cpu_baseline:
+            res["cpu_baseline"] = cpu_baseline(cfg, pool, layers[0], qstreams[0], nblk, args)
+        return res
+    finally:
+        for L in layers:
+            L.close()
+        pool.close()
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+
+
+def metadata_build_rate(cfg, pool, L0, nblk, ss, torch):
+    """The metadata build (setup path, when blocks fill) timed alone on one
+    sequence's records copied to HBM."""
     kv_one = torch.empty(cfg.Hkv * int(nblk[0]) * cfg.record_bytes, dtype=torch.uint8, device="cuda")
     kv_one.copy_(pool.t[int(L0.pool_off_host[0]):int(L0.pool_off_host[0]) + kv_one.numel()])
     off1 = torch.from_numpy(np.arange(cfg.Hkv, dtype=np.int64) * int(nblk[0]) * cfg.record_bytes).cuda()
     n1 = torch.tensor([int(nblk[0])], dtype=torch.int32, device="cuda")
     meta1 = torch.empty(cfg.Hkv, cfg.nblk_max, 2, D, dtype=torch.int16, device="cuda")
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    meta_ms = []
     for _ in range(3):
         e0.record()
         ss.ss_build_metadata(kv_one, off1, n1, 1, cfg.Hkv, cfg.nblk_max, cfg.blk, D, meta1)
@@ -172,187 +425,80 @@ def main():
         torch.cuda.synchronize()
         meta_ms.append(e0.elapsed_time(e1))
     meta_bytes = cfg.Hkv * int(nblk[0]) * (cfg.blk * D * 2 + 2 * D * 2)
-    del kv_one
+    ms = float(np.median(meta_ms))
+    return {"ms": round(ms, 4), "bytes": meta_bytes, "GBps": round(meta_bytes / (ms * 1e-3) / 1e9, 1),
+            "note": "setup path (when blocks fill), one sequence, not in the step"}
 
-    # ----------------------------------------------------------- warm-up
-    for s in range(warmup):
-        for l, L in enumerate(layers):
-            run_step(L, l, s)
-    torch.cuda.synchronize()
-    log(f"warm-up done ({warmup} step(s)); timing {steps} step(s)")
 
-    # ------------------------------------------------------------ timed
-    P = layers[0].parts
-    ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(7 * P)] for _ in layers] for _ in range(steps)]
-    # every timing event is a barrier packet on its queue: events go only on the
-    # first and the last layer of a step (the step's start and end), and there
-    # only around each group's start, end and gather (the dominant kernel)
-    sampled = sorted({0, len(layers) - 1})
-    used = [False] * (7 * P)
-    used[0] = used[7 * (P - 1) + 6] = True
-    for p in range(P):
-        used[7 * p + 3] = used[7 * p + 4] = True
-    for row in ev:  # create the underlying events before timing
-        for es in row:
-            for e in es:
-                e.record()
-    torch.cuda.synchronize()
-    n_miss = np.zeros((steps, len(layers)), np.int64)
-    dev_total0 = [ss.ss_dev_cache_total_misses(L.dev) if L.dev is not None else 0 for L in layers]
-    t0 = time.perf_counter()
-    for i in range(steps):
-        s = warmup + i
-        for l, L in enumerate(layers):
-            run_step(L, l, s, events=[e.cuda_event if used[j] else None for j, e in enumerate(ev[i][l])]
-                     if l in sampled else None)
-            n_miss[i, l] = L.last_n_miss or 0
-    if new_kv is not None:
-        for L in layers:  # the last step's save is part of the work
-            ss.ss_kv_save_wait(L.saver)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    for l, L in enumerate(layers):
-        if L.dev is not None:  # the device resolve counts its misses on the GPU: spread the total over the steps
-            n_miss[:, l] = (ss.ss_dev_cache_total_misses(L.dev) - dev_total0[l]) / steps
+def _read(path):
+    try:
+        with open(path) as fh:
+            return fh.read().strip()
+    except OSError:
+        return None
 
-    # ------------------------------------------------------- accounting
-    # Gathers of consecutive groups overlap (two transfer streams), so the
-    # link's busy time is the union of the gather intervals of a step.  Also
-    # per step: the ramp before the first gather starts, idle gaps inside
-    # the gather span, and the tail after the last gather ends.
-    pipe = {"ramp": [], "link_busy": [], "link_gaps": [], "tail": []}
-    gather_launch_ms = []
-    for i in range(steps):
-        for l in sampled:  # layers are alike (same lengths, shapes and drift): the sampled ones stand for all
-            e = ev[i][l]
-            iv = sorted((e[0].elapsed_time(e[7 * p + 3]), e[0].elapsed_time(e[7 * p + 4])) for p in range(P))
-            gather_launch_ms += [b - a for a, b in iv]
-            busy, cur_a, cur_b = 0.0, iv[0][0], iv[0][1]
-            for a, b in iv[1:]:
-                if a > cur_b:
-                    busy += cur_b - cur_a
-                    cur_a, cur_b = a, b
-                else:
-                    cur_b = max(cur_b, b)
-            busy += cur_b - cur_a
-            first, last = iv[0][0], max(b for _, b in iv)
-            pipe["ramp"].append(first)
-            pipe["link_busy"].append(busy)
-            pipe["link_gaps"].append(last - first - busy)
-            pipe["tail"].append(e[0].elapsed_time(e[7 * (P - 1) + 6]) - last)
-    pipe = {k: round(float(np.mean(v)), 4) for k, v in pipe.items()}
-    # each step on its own: from the first layer's first event to the last
-    # layer's last (GPU time; the wall-clock mean above includes host time
-    # between steps)
-    step_ms = np.array([ev[i][0][0].elapsed_time(ev[i][-1][7 * (P - 1) + 6]) for i in range(steps)])
-    step_stats = {"median": round(float(np.median(step_ms)), 4), "min": round(float(step_ms.min()), 4),
-                  "max": round(float(step_ms.max()), 4), "p90": round(float(np.percentile(step_ms, 90)), 4)}
-    units = cfg.B * cfg.Hkv
-    # the gather's algorithmic bytes per step: the missed block records (mean
-    # over the timed steps) over the host link, against the link's busy time
-    gather_bytes = float(n_miss.sum()) / steps * cfg.record_bytes
-    busy_ms = pipe["link_busy"] * len(layers)
-    ach = gather_bytes / (busy_ms * 1e-3) / 1e9 if busy_ms > 0 else 0.0
-    key = (cfg.name, args.seed, steps, warmup, tuple(layers[0].part_sizes), args.resolve)
-    roof = {"gather": {"bound": "host-link", "achieved": round(ach, 2), "peak": round(LINK_PEAK_GBS, 2),
-                       "unit": "GB/s", "frac": round(ach / LINK_PEAK_GBS, 4), "bytes_per_step": int(gather_bytes),
-                       "link_busy_ms_per_step": round(busy_ms, 4), "launches_per_step": len(layers) * P,
-                       "ms_per_launch": round(float(np.mean(gather_launch_ms)), 4),
-                       "traffic": traffic("gather", key)}}
-    dominant = "gather"  # pipeline_ms shows the link busy for most of the step
-    tokens = cfg.B * steps
-    value = tokens / wall
-    miss_rate = float(n_miss.mean()) / (units * cfg.k)
-    log(f"{value:.0f} tokens/s, {wall / steps * 1e3:.3f} ms/step; gather {ach:.1f} GB/s; pipeline {pipe}")
 
-    # ------------------------------------------- isolated kernel rates
-    # Each kernel alone over the whole batch (one launch, nothing else on the
-    # GPU), on the last timed step's data: the HBM kernels' own rates, which
-    # the overlapped step hides behind the host-link gather.
-    iso = isolated_rates(cfg, layers[0], qstreams[0][warmup + steps - 1][1], ss, torch)
-    for name in iso:
-        iso[name]["traffic"] = traffic(name, key)
+def host_facts():
+    """The GPU's PCIe link as negotiated (each device on the path from the
+    GPU to the root port: speed and width now and at most) and the host's
+    CPUs (count, affinity, cgroup quota, model)."""
+    import ctypes
+    facts = {}
+    try:
+        hip = ctypes.CDLL("libamdhip64.so")
+        buf = ctypes.create_string_buffer(64)
+        dev = ctypes.c_int(0)
+        hip.hipGetDevice(ctypes.byref(dev))
+        if hip.hipDeviceGetPCIBusId(buf, 64, dev) == 0:
+            bus = buf.value.decode().lower()
+            path = os.path.realpath(f"/sys/bus/pci/devices/{bus}")
+            chain = []
+            while os.path.basename(path).count(":") == 2:  # PCI addresses dddd:bb:dd.f
+                chain.append({"device": os.path.basename(path),
+                              "current_link_speed": _read(os.path.join(path, "current_link_speed")),
+                              "current_link_width": _read(os.path.join(path, "current_link_width")),
+                              "max_link_speed": _read(os.path.join(path, "max_link_speed")),
+                              "max_link_width": _read(os.path.join(path, "max_link_width"))})
+                path = os.path.dirname(path)
+            facts["pcie_bus_id"] = bus
+            facts["pcie_path_gpu_to_root"] = chain
+    except OSError as e:
+        facts["pcie_error"] = str(e)
+    facts["os_cpu_count"] = os.cpu_count()
+    facts["affinity_cpus"] = len(os.sched_getaffinity(0))
+    quota = _read("/sys/fs/cgroup/cpu.max")
+    if quota:
+        facts["cgroup_cpu_max"] = quota
+        q, per = quota.split()[:2]
+        if q != "max":
+            facts["cgroup_cpus"] = round(int(q) / int(per), 2)
+    info = {}
+    try:
+        for line in open("/proc/cpuinfo"):
+            if ":" not in line:
+                if info:
+                    break
+                continue
+            k, v = (x.strip() for x in line.split(":", 1))
+            if k in ("vendor_id", "cpu family", "model", "model name", "stepping") and k not in info:
+                info[k] = v
+    except OSError:
+        pass
+    facts["cpu"] = info
+    return facts
 
-    # ------------------------------------------- working sets (Section 3.3)
-    ws_study = None
-    if new_kv is None and cfg.layers == 1 and not args.no_working_set:
-        ws_study = working_set_study(cfg, layers[0], qstreams[0][-1][0], warmup + steps, args.seed, ss, torch)
 
-    # ------------------------------------------- batch control (Algorithm 1)
-    batch_ctl = None
-    if new_kv is None and cfg.layers == 1 and not args.no_working_set:
-        batch_ctl = batch_control_study(cfg, layers[0], pool, ss, torch, H, args.seed)
-
-    # ------------------------------------------- scoring variants
-    variants = None
-    if new_kv is None and cfg.layers == 1 and not args.no_variants:
-        variants = score_variants_study(cfg, layers[0], qstreams[0][-1][1], pool, ss, torch)
-
-    # ------------------------------------------- transfer comparisons
-    load_cmp = None if args.no_save_bandwidth else load_comparison(cfg, layers[0], pool, ss, torch)
-    save_bw = None if args.no_save_bandwidth else save_bandwidth(ss, torch, H)
-
-    # ------------------------------------------- layer-segmented prefill
-    prefill = None if args.no_prefill else prefill_study(ss, torch, H)
-
-    # ------------------------------------------------------ CPU baseline
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(cfg, pool, layers[0], qstreams[0], nblk, args, warmup)
-
-    result = {
-        "metric": "sparse decode-step tokens/sec at 1 GPU; % HBM roofline; gather host-link GB/s",
-        "value": round(value, 2),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": steps,
-        "warmup": warmup,
-        "ms_per_step": round(wall / steps * 1e3, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": cfg.name, "batch": cfg.B, "q_heads": cfg.Hq, "kv_heads": cfg.Hkv, "head_dim": D,
-                   "context": int(lens.max()), "block": cfg.blk, "topk_blocks": cfg.k, "cache_frac": cfg.cache_frac,
-                   "layers": cfg.layers, "layers_with_own_dram_records": n_distinct, "drift": cfg.drift,
-                   "seed": args.seed, "resolve": args.resolve},
-        "roofline": dict(kernel=dominant, **roof[dominant]),
-        "pipeline_ms": pipe,
-        "step_ms_events": step_stats,
-        "rooflines_isolated": iso,
-        "parts": layers[0].part_sizes,
-        "miss_rate": round(miss_rate, 4),
-        "gather_GBps": roof["gather"]["achieved"],
-        "hbm_frac": {"score": iso["score"]["frac"], "attention": iso["attention"]["frac"]},
-        "metadata_build": {"ms": round(float(np.median(meta_ms)), 4), "bytes": meta_bytes,
-                           "GBps": round(meta_bytes / (np.median(meta_ms) * 1e-3) / 1e9, 1),
-                           "note": "setup path (when blocks fill), one sequence, not in the step"},
-        "cpu_baseline": cpu,
-    }
-    if new_kv is not None:
-        L = layers[0]
-        result["config"]["with_save"] = True
-        result["save_side"] = {"blocks_filled_per_sequence": int((L.nblk.cpu().numpy() - nblk).max()),
-                               "overflow": int(L.overflow.item()),
-                               "note": "each timed step also appends its new tokens (metadata on a fill) and saves "
-                                       "them with FlashD2H; the last save is waited for inside the timed region"}
-    if save_bw is not None:
-        result["save_bandwidth"] = save_bw
-    if load_cmp is not None:
-        result["load_comparison"] = load_cmp
-    if ws_study is not None:
-        result["working_set"] = ws_study
-    if batch_ctl is not None:
-        result["batch_control"] = batch_ctl
-    if variants is not None:
-        result["score_variants"] = variants
-    if prefill is not None:
-        result["prefill"] = prefill
-    print(json.dumps(result), flush=True)
-    for L in layers:
-        L.close()
-    pool.close()
+def exit_report():
+    """Lists what is still alive as the script ends (child processes,
+    threads), so a run that leaves anything behind shows it on stderr."""
+    import threading
+    try:
+        import psutil
+        kids = [f"{c.pid}:{c.name()}" for c in psutil.Process().children(recursive=True)]
+    except Exception as e:  # psutil missing or a process gone meanwhile
+        kids = [f"unknown ({e})"]
+    threads = [t.name for t in threading.enumerate() if t is not threading.main_thread()]
+    log(f"exit: child processes {kids or 'none'}; Python threads {threads or 'none'}")
 
 
 # ------------------------------------------------------- HBM traffic
@@ -368,8 +514,8 @@ KERNEL_SOURCES = {
     "topk": ["topk.hip"],
     "attention": ["attention.hip"],
 }
-# hierarchical 128k-context layer, seed 0, 16 timed steps after 1 warm-up, groups 2,4,10,20,18,8,2, host resolve
-_KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 16, 1, [2, 4, 10, 20, 18, 8, 2], "host"]
+# hierarchical 128k-context layer, seed 0, 16 timed steps, groups 2,4,10,20,18,8,2, host resolve
+_KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 16, [2, 4, 10, 20, 18, 8, 2], "host"]
 TRAFFIC = {
     "gather": {"key": _KEY, "digest": "b6afd93dae4c85a6", "bytes": 260492263, "fetch": 131095015,
               "write": 129397248},
@@ -394,7 +540,7 @@ def source_digest(kernel):
 
 def traffic(kernel, key):
     rec = TRAFFIC.get(kernel)
-    norm = lambda k: (k[0], int(k[1]), int(k[2]), int(k[3]), tuple(int(x) for x in k[4]), k[5] if len(k) > 5 else "host")
+    norm = lambda k: (k[0], int(k[1]), int(k[2]), tuple(int(x) for x in k[3]), k[4])
     if not rec or norm(rec["key"]) != norm(key):
         return None
     if rec["digest"] != source_digest(kernel):
@@ -463,7 +609,7 @@ def summarize_pmc(args):
             # the isolated full-batch launches are each kernel's last 10 dispatches
             vals = [v for n, _, v in rows if tag in n][-10:]
             out.setdefault(name, {})[c] = float(np.median(vals)) * 1024 * scale[c]
-    key = [bench["config"]["workload"], bench["config"]["seed"], steps, warmup, bench["parts"],
+    key = [bench["config"]["workload"], bench["config"]["seed"], steps, bench["parts"],
            bench["config"].get("resolve", "host")]
     algo = {"gather": bench["roofline"]["bytes_per_step"]}
     for name in ("score", "topk", "attention"):
@@ -780,12 +926,13 @@ def load_comparison(cfg, L, pool, ss, torch, reps=3):
     return res
 
 
-def save_bandwidth(ss, torch, H, B=4, n=8192, Hkv=8, reps=3):
+def save_bandwidth(ss, torch, H, B=4, n=8192, Hkv=8, reps=3, comparisons=False):
     """Saving a prefill-sized batch of new KV (B sequences x n tokens x Hkv
     heads, 128 MiB) to a pinned DRAM pool as block records, for blocks of 8,
-    16 and 32 tokens, three ways (the comparison of Section 3.2.2):
+    16 and 32 tokens (Section 3.2.2):
       flashd2h   one device-to-host copy of the contiguous tensor, then the
                  library's host threads place the tokens (ss_kv_save)
+    and, with `comparisons`, the paper's alternatives:
       per_block  one hipMemcpyAsync per block record from HBM (issued from
                  Python; ~1 us of its overhead per call)
       gpu_direct a kernel stores the records into mapped host memory (the
@@ -820,6 +967,10 @@ def save_bandwidth(ss, torch, H, B=4, n=8192, Hkv=8, reps=3):
                 out["flashd2h"] = round(nbytes / float(np.median(ts)) / 1e9, 2)
             finally:
                 ss.ss_kv_saver_destroy(saver)
+            if not comparisons:
+                res[f"blk{blk}"] = out
+                log(f"saving {nbytes >> 20} MiB, blk {blk}: {out} GB/s")
+                continue
             stream = torch.cuda.current_stream().cuda_stream
             src0 = rec_dev.data_ptr()
             ts = []
@@ -901,17 +1052,18 @@ def isolated_rates(cfg, L, q, ss, torch, reps=10):
     return res
 
 
-def cpu_baseline(cfg, pool, L, qs, nblk, args, warmup):
+def cpu_baseline(cfg, pool, L, qs, nblk, args):
     """The oracle on the first `cpu_seqs` sequences of layer 0: its own
     metadata (untimed), a cache-fill step (untimed), then `cpu_steps` timed
     steps of score, select, LRU resolve, gather and attention, one thread
-    per sequence."""
+    per sequence, on every CPU the process may run on."""
     import oracle
     from synth import gen
     O = oracle.Oracle()
     nseq = min(args.cpu_seqs, cfg.B)
     nsteps = min(args.cpu_steps, len(qs) - 1)
-    threads = min(16, os.cpu_count() or 1, nseq)
+    allowed = len(os.sched_getaffinity(0))
+    threads = min(allowed, nseq)
     rb, Hkv = cfg.record_bytes, cfg.Hkv
     qh = [gen.to_u16(qs[s][1]) for s in range(nsteps + 1)]
     log(f"cpu baseline: oracle on {nseq} sequences x {nsteps} steps, {threads} threads")
@@ -949,19 +1101,13 @@ def cpu_baseline(cfg, pool, L, qs, nblk, args, warmup):
         for s in range(1, nsteps + 1):
             step(b, states1[b], s)
     wall1 = time.perf_counter() - t0
-    cpu_model = ""
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                cpu_model = line.split(":", 1)[1].strip()
-                break
-    except OSError:
-        pass
+    hf = host_facts()
     return {"value": round(nseq * nsteps / wall, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
             "sample": f"{nseq} of {cfg.B} sequences (all {Hkv} KV heads each) x {nsteps} decode steps of layer 0 "
                       f"after an untimed cache-fill step; score, select, LRU resolve, gather, attention; "
                       f"{wall:.2f} s wall, {threads} threads, one sequence per thread",
-            "cpu": cpu_model,
+            "os_cpu_count": hf["os_cpu_count"], "affinity_cpus": allowed,
+            "cgroup_cpus": hf.get("cgroup_cpus"), "cpu": hf["cpu"],
             "single_thread": {"value": round(n1 * nsteps / wall1, 3), "unit": "tokens/s", "cores": 1,
                               "sample": f"{n1} sequences x {nsteps} steps on one thread, {wall1:.2f} s"}}
 

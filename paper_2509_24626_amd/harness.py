@@ -178,6 +178,25 @@ class HierLayer:
             self.last_n_miss = ss.ss_decode_layer(self.buffers, t, q, self.out, None, events)
         return self.out
 
+    def reset_cache(self):
+        """Empties the block cache: a fresh slot table over the same regions
+        (host or GPU), so that the next step starts from a cold cache.  The
+        HBM bytes stay as they are; every slot is empty, so none of them is
+        read before a gather writes it."""
+        torch.cuda.synchronize()
+        cfg = self.cfg
+        if self.dev is not None:
+            ss.ss_dev_cache_destroy(self.dev)
+            self.dev = None
+            self.dev = ss.ss_dev_cache_create(cfg.B, cfg.Hkv, self.nblk_host + self.reserve, self.capacity)
+        old = self.handle
+        self.handle = ss.ss_cache_create(cfg.B, cfg.Hkv, self.nblk_host, self.capacity, cfg.record_bytes)
+        ss.ss_cache_destroy(old)
+        off = np.empty(self.units, np.int64)
+        ss.ss_cache_region_offsets(self.handle, off)
+        assert np.array_equal(off, self.cache_off_host)
+        self.buffers.cache = self.handle
+
     def dev_miss_rows(self):
         """Device resolve: (per-unit miss counts, rows [units][k][4], error flags) of the last step."""
         counts, err = ss.ss_dev_cache_miss_counts(self.dev, self.units)
