@@ -25,6 +25,10 @@ def lib():
     """Load liboracle.so, compiling it first if it is not there."""
     global _lib
     if _lib is None:
+        other = os.environ.get("ORACLE_LIBRARY")  # another build of oracle.c (a sanitizer build)
+        if other:
+            _lib = load(other)
+            return _lib
         if not os.path.exists(_build.LIB) or os.path.getmtime(_build.LIB) < os.path.getmtime(_build.SRC):
             _build.build()
         _lib = load(_build.LIB)

@@ -12,7 +12,9 @@ import ctypes
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "_lib", "libsparseserve.so")
+# SS_LIBRARY names another build of the same library (the sanitizer builds
+# of build_sanitized.py); there is still no fallback
+LIB_PATH = os.environ.get("SS_LIBRARY") or os.path.join(_HERE, "_lib", "libsparseserve.so")
 
 _lib = None
 
