@@ -314,6 +314,21 @@ ss_status ss_sparse_attention(const void *q, const void *kv_base, const int64_t 
                               const int32_t *capacity, int32_t slot_limit, int B, int Hq, int Hkv, int d, int blk,
                               int k, float scale, float *out, void *workspace, size_t ws_bytes, void *stream);
 
+/* ss_sparse_attention without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  The split partials go to a static
+ * device array of 9 MiB that the library holds on each GPU it runs on until
+ * the process ends; every supported shape fits it (SS_ERR_OOM otherwise).
+ * The first call on a device looks the array up (hipGetSymbolAddress);
+ * no call allocates or frees memory.  All calls on one GPU share the array,
+ * so calls that overlap on one GPU (on different streams, or from several
+ * threads) race and must be serialised by the caller; every partial a call
+ * reads is written by that call first, so nothing carries over between
+ * calls.  Arguments and results as ss_sparse_attention. */
+ss_status ss_sparse_attention_static(const void *q, const void *kv_base, const int64_t *region_off,
+                                     const int32_t *slots, const int32_t *capacity, int32_t slot_limit, int B,
+                                     int Hq, int Hkv, int d, int blk, int k, float scale, float *out, void *stream);
+
 /* ------------------------------------------------------ appending tokens
  * The decode step's new KV (Section 3.2.2: each layer's new KV tensor, one
  * token per sequence and KV head, goes into the free slot of the

@@ -98,6 +98,8 @@ _SIGNATURES = {
     "ss_dev_cache_total_misses": (_i32, [_vp, _vp]),
     "ss_decode_layer_dev": (_i32, [ctypes.POINTER(ss_layer_buffers), _vp, _i64, _vp, _vp, _vp, _vp]),
     "ss_set_host_wait_timeout": (_i32, [_i64]),
+    "ss_sparse_attention_static": (_i32, [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32,
+                                          _vp, _vp]),
 }
 
 
@@ -256,6 +258,13 @@ def ss_sparse_attention(q, kv_base, region_off, slots, capacity, slot_limit, B, 
     _check(lib().ss_sparse_attention(_ptr(q), _ptr(kv_base), _ptr(region_off), _ptr(slots), _ptr(capacity),
                                      slot_limit, B, Hq, Hkv, d, blk, k, float(scale), _ptr(out), _ptr(workspace),
                                      ws_bytes, _stream(stream)))
+
+
+def ss_sparse_attention_static(q, kv_base, region_off, slots, capacity, slot_limit, B, Hq, Hkv, d, blk, k, scale,
+                               out, stream=None):
+    _check(lib().ss_sparse_attention_static(_ptr(q), _ptr(kv_base), _ptr(region_off), _ptr(slots), _ptr(capacity),
+                                            slot_limit, B, Hq, Hkv, d, blk, k, float(scale), _ptr(out),
+                                            _stream(stream)))
 
 
 def ss_decode_layer(buffers, step, q, out, stream=None, events=None):

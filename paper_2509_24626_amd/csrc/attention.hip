@@ -35,6 +35,9 @@
 // are merged in LDS in wave order, and with several splits a second kernel
 // merges the split partials in split order.  All merges run in a fixed
 // order, so results do not depend on scheduling.
+#include <mutex>
+#include <unordered_map>
+
 #include "internal.hpp"
 
 namespace {
@@ -349,4 +352,59 @@ extern "C" ss_status ss_sparse_attention(const void *q, const void *kv_base, con
     if (st != SS_OK || sp.splits == 1) return st;
     combine_kernel<<<dim3(units, G), dim3(D), 0, s>>>(ws, Hq, Hkv, G, sp.splits, out);
     return ss::check_launch("ss_sparse_attention(combine)");
+}
+
+// ------------------------------------------------- allocation-free variant
+// The split partials of ss_sparse_attention_static live in this file-scope
+// device array instead of a caller workspace.  Every supported shape fits:
+// with more than one split, units * splits < units + 512 <= 1023 and
+// G <= 16, so the partials take at most 1023 * 16 * (128 + 2) * 4 bytes.
+// Host code never uses the array's name as an address: each device's copy
+// is looked up once with hipGetSymbolAddress and that pointer is passed on.
+namespace {
+constexpr size_t kStaticScratchBytes = 9u << 20;
+__device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
+std::mutex g_scratch_mu;
+std::unordered_map<int, void *> g_scratch_addr;  // by device
+
+ss_status scratch_address(void **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return ss::fail(SS_ERR_HIP, "ss_sparse_attention_static: hipGetDevice: %s", hipGetErrorString(e));
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    auto it = g_scratch_addr.find(dev);
+    if (it != g_scratch_addr.end()) {
+        *out = it->second;
+        return SS_OK;
+    }
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+        return ss::fail(SS_ERR_HIP, "ss_sparse_attention_static: hipGetSymbolAddress of the scratch array: %s",
+                        hipGetErrorString(e));
+    g_scratch_addr[dev] = p;
+    *out = p;
+    return SS_OK;
+}
+}  // namespace
+
+extern "C" ss_status ss_sparse_attention_static(const void *q, const void *kv_base, const int64_t *region_off,
+                                                const int32_t *slots, const int32_t *capacity, int32_t slot_limit,
+                                                int B, int Hq, int Hkv, int d, int blk, int k, float scale,
+                                                float *out, void *stream)
+{
+    // shapes the main entry point rejects are rejected there; this only sizes the partials
+    const size_t need = ss_sparse_attention_workspace(B, Hq, Hkv, d, blk, k);
+    if (need > kStaticScratchBytes)
+        return ss::fail(SS_ERR_OOM, "ss_sparse_attention_static: %zu bytes of split partials exceed the %zu-byte "
+                        "static scratch", need, kStaticScratchBytes);
+    void *ws = nullptr;
+    if (need) {
+        ss_status st = scratch_address(&ws);
+        if (st) return st;
+    }
+    return ss_sparse_attention(q, kv_base, region_off, slots, capacity, slot_limit, B, Hq, Hkv, d, blk, k, scale,
+                               out, ws, need, stream);
 }
