@@ -71,10 +71,10 @@ def parse():
                     help="rocprofv3 --pmc output folders of this script (FETCH_SIZE, WRITE_SIZE) and of "
                          "--calibrate-copy; prints the traffic summary and exits (no GPU)")
     ap.add_argument("--bench-json", help="with --summarize-pmc: the JSON line the profiled run printed")
-    ap.add_argument("--resolve", choices=["host", "device"], default="host",
-                    help="the slot-table resolve on host threads (ss_decode_layer, default) or on the GPU "
-                         "(ss_decode_layer_dev)")
-    ap.add_argument("--layers32-resolve", choices=["host", "device"], default="host",
+    ap.add_argument("--resolve", choices=["auto", "host", "device"], default="auto",
+                    help="the slot-table resolve on host threads (ss_decode_layer) or on the GPU "
+                         "(ss_decode_layer_dev); auto: host for one layer, GPU for multi-layer workloads")
+    ap.add_argument("--layers32-resolve", choices=["host", "device"], default="device",
                     help="the resolve of the 32-layer sub-record")
     ap.add_argument("--with-save", action="store_true",
                     help="every step also appends its new tokens (metadata on a fill) and saves them to DRAM "
@@ -139,6 +139,11 @@ def main():
         sys.exit(2)
     steps = args.steps if args.steps is not None else cfg.steps
     warmup = max(args.warmup, 1)
+    if args.resolve == "auto":
+        # the host resolve (the paper's arrangement) for one layer; with many layers
+        # each layer's ramp pays the host's reaction, and the GPU resolve measured
+        # 2-3% more tokens/s on the 32-layer workload over seeds 0-2
+        args.resolve = "device" if cfg.layers > 1 else "host"
     host = host_facts()
     log(f"host: {host}")
 

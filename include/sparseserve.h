@@ -67,7 +67,7 @@ typedef int ss_status;
 #define SS_ERR_HIP 5         /* a HIP runtime call or kernel launch failed */
 #define SS_ERR_TIMEOUT 6     /* the host waited longer than its deadline for GPU work */
 
-#define SS_ABI_VERSION 3
+#define SS_ABI_VERSION 4
 
 int ss_abi_version(void);
 const char *ss_status_string(ss_status status);
@@ -525,16 +525,23 @@ ss_status ss_set_host_wait_timeout(int64_t ms);
  * miss_host are not used).  The first group's scoring, top-k, resolve,
  * gather and attention run in order on `stream`.  Each later group's
  * scoring, top-k and resolve run on a compute stream the library creates
- * once per device (default priority), its gather on a transfer stream
- * behind the resolve, and its attention on `stream` behind the gather; all
- * of it is ordered after the work already on `stream`, and `stream` holds
- * every attention, so work enqueued on `stream` afterwards sees the whole
- * step.  The host enqueues the step and returns without waiting; the misses
- * are counted in the cache (ss_dev_cache_miss_counts).  L->miss_dev holds
- * each unit's miss rows at row u*k.  events as for ss_decode_layer
- * (events[7p+0..2] on the stream that runs group p's scoring;
- * events[7p+2] after the resolve).  The block cache's regions must be laid
- * out as ss_cache_region_offsets gives them for the same capacities. */
+ * once per device (default priority).  A middle group's gather runs on a
+ * transfer stream behind its resolve and its attention on the compute
+ * stream behind the gather; the last group's gather runs on `stream`, with
+ * its attention right behind it.  Everything is ordered after the work
+ * already on `stream`, and `stream` waits for the compute stream at the end,
+ * so work enqueued on `stream` afterwards sees the whole step.  The host
+ * enqueues the step and returns without waiting; the misses are counted in
+ * the cache (ss_dev_cache_miss_counts).  L->miss_dev holds each unit's miss
+ * rows at row u*k.  Attentions of two groups run at once, so with three
+ * groups or more L->attn_ws_bytes must hold two regions, each the largest
+ * ss_sparse_attention_workspace of a group rounded up to 256 bytes
+ * (SS_ERR_OOM otherwise).  events as for ss_decode_layer, except that
+ * events[7p+0..2] are recorded on the stream that runs group p's scoring
+ * (events[7p+2] after the resolve), events[7p+5..6] on the stream that runs
+ * its attention, and the last group's events[7p+6] on `stream` once the
+ * whole step is done.  The block cache's regions must be laid out as
+ * ss_cache_region_offsets gives them for the same capacities. */
 ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache *cache, int64_t step, const void *q,
                               float *out, void *stream, void *const *events);
 

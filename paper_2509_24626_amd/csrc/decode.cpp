@@ -60,6 +60,7 @@ struct exec_state {
     hipStream_t xfer[2] = {nullptr, nullptr};  // groups alternate between them
     hipStream_t comp = nullptr;                // device resolve: scoring chain of groups after the first
     hipEvent_t start = nullptr;
+    hipEvent_t comp_done = nullptr;  // device resolve: the attentions on the compute stream are done
     std::vector<hipEvent_t> sel_ready, gathered;
 };
 
@@ -268,11 +269,17 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
 // The same step with the slot table resolved on the GPU (ss_dev_cache).  The
 // first group's scoring, top-k, resolve, gather and attention run in order
 // on `stream`, so the link starts with no cross-queue hand-off (each costs
-// ~20 us).  The later groups' scoring, top-k and resolve run on a compute
-// stream of the library's, in parallel with the first group's; each such
-// group's gather runs on a transfer stream behind an event recorded after
-// its resolve, and its attention on `stream` behind the gather.  The host
-// enqueues the whole step and returns without waiting for any of it.
+// 10-30 us in the traces).  The later groups' scoring, top-k and resolve run
+// on a compute stream of the library's, in parallel with the first group's.
+// A middle group's gather runs on a transfer stream (the two alternate)
+// behind an event recorded after its resolve, and its attention on the
+// compute stream behind the gather, after every group's resolve so that no
+// resolve waits for a gather.  The last group's gather runs on `stream`
+// (still beside the previous group's gather on its transfer stream) with its
+// attention right behind it, so no hand-off between queues lies between the
+// link's last byte and the end of the step; `stream` then waits for the
+// compute stream.  The host enqueues the whole step and returns without
+// waiting for any of it.
 extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache *dc, int64_t step, const void *q,
                                          float *out, void *stream, void *const *events)
 {
@@ -296,6 +303,23 @@ extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache
             SS_CHECK_ARG(L->part_end[p] > (p ? L->part_end[p - 1] : 0),
                          "ss_decode_layer_dev: part_end must be strictly increasing");
     }
+    const int32_t *pe = L->part_end;
+    auto b_of = [&](int p) { return p == 0 ? 0 : (pe ? pe[p - 1] : (int)((int64_t)B * p / P)); };
+    // attention workspace: one region for the attentions on `stream`, one for
+    // those on the compute stream (the two run at the same time)
+    size_t ws_one = 0;
+    for (int p = 0; p < P; ++p) {
+        const size_t w = ss_sparse_attention_workspace(b_of(p + 1) - b_of(p), Hq, Hkv, d, L->blk, k);
+        ws_one = w > ws_one ? w : ws_one;
+    }
+    ws_one = (ws_one + 255) & ~(size_t)255;
+    const bool comp_attn = P > 2;  // the middle groups attend on the compute stream
+    const size_t ws_need = ws_one * (comp_attn ? 2 : 1);
+    if (L->attn_ws_bytes < ws_need || (ws_need && !L->attn_ws))
+        return ss::fail(SS_ERR_OOM, "ss_decode_layer_dev: attention workspace %zu bytes < %zu", L->attn_ws_bytes,
+                        ws_need);
+    char *ws_s = static_cast<char *>(L->attn_ws);
+    char *ws_c = ws_s ? ws_s + ws_one : nullptr;
     ss_status st = ss::dev_cache_check_step(dc, step, k);
     if (st) return st;
     std::lock_guard<std::mutex> lock(g_exec_mu);
@@ -306,25 +330,32 @@ extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache
     const size_t meta_row = (size_t)(L->meta_kind == SS_META_MEAN ? 1 : 2) * d * 2;
     const char *q8 = static_cast<const char *>(q);
     const char *meta8 = static_cast<const char *>(L->meta);
-    const int32_t *pe = L->part_end;
-    auto b_of = [&](int p) { return p == 0 ? 0 : (pe ? pe[p - 1] : (int)((int64_t)B * p / P)); };
     int32_t *counts = ss::dev_cache_counts(dc);
 
     if (P > 1 && !ex->comp &&
         (st = hip_check(hipStreamCreateWithFlags(&ex->comp, hipStreamNonBlocking), "create compute stream")))
+        return st;
+    if (comp_attn && !ex->comp_done &&
+        (st = hip_check(hipEventCreateWithFlags(&ex->comp_done, hipEventDisableTiming), "create event")))
         return st;
     if ((st = hip_check(hipEventRecord(ex->start, s), "record")) ||
         (st = hip_check(hipStreamWaitEvent(ex->xfer[0], ex->start, 0), "order transfer stream")) ||
         (st = hip_check(hipStreamWaitEvent(ex->xfer[1], ex->start, 0), "order transfer stream")) ||
         (P > 1 && (st = hip_check(hipStreamWaitEvent(ex->comp, ex->start, 0), "order compute stream"))))
         return st;
+    auto attend = [&](int p, hipStream_t on, char *ws) {
+        const int b0 = b_of(p), Bp = b_of(p + 1) - b0;
+        return ss_sparse_attention(q8 + (size_t)b0 * Hq * d * 2, L->cache_base, L->cache_off_dev + b0 * Hkv,
+                                   L->slots_dev + b0 * rows_per_seq,
+                                   L->capacity_dev ? L->capacity_dev + b0 * Hkv : nullptr, L->slot_limit, Bp, Hq,
+                                   Hkv, d, L->blk, k, L->scale, out + (size_t)b0 * Hq * d, ws, ws_one, on);
+    };
     for (int p = 0; p < P; ++p) {
         const int b0 = b_of(p), b1 = b_of(p + 1), Bp = b1 - b0;
         const int64_t row0 = b0 * rows_per_seq;
-        // the first group's chain and gather on `stream`; later groups' chains on
-        // the compute stream, their gathers on alternate transfer streams
+        const bool last = p == P - 1;
+        // the first group's chain on `stream`; later groups' chains on the compute stream
         const hipStream_t c = p == 0 ? s : ex->comp;
-        const hipStream_t x = p == 0 ? s : ex->xfer[p & 1];
         if ((st = record(events, 7 * p + 0, c))) return st;
         st = ss_score_blocks_variant(q8 + (size_t)b0 * Hq * d * 2, meta8 + (size_t)b0 * Hkv * L->nblk_max * meta_row,
                                      L->meta_kind, L->agg, L->nblk_dev + b0, Bp, Hq, Hkv, L->nblk_max, d,
@@ -338,8 +369,11 @@ extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache
                                   L->miss_dev, c);
         if (st) return st;
         if ((st = record(events, 7 * p + 2, c))) return st;
+        // the group's transfer: the first and the last group's on `stream`, the
+        // middle groups' on alternate transfer streams
+        const hipStream_t x = (p == 0 || last) ? s : ex->xfer[p & 1];
         if (p > 0 && ((st = hip_check(hipEventRecord(ex->sel_ready[p], c), "record")) ||
-                      (st = hip_check(hipStreamWaitEvent(x, ex->sel_ready[p], 0), "order gather after resolve"))))
+                      (st = hip_check(hipStreamWaitEvent(x, ex->sel_ready[p], 0), "order transfer after resolve"))))
             return st;
         hipEvent_t g0 = events ? reinterpret_cast<hipEvent_t>(events[7 * p + 3]) : nullptr;
         hipEvent_t g1 = events ? reinterpret_cast<hipEvent_t>(events[7 * p + 4]) : nullptr;
@@ -351,21 +385,27 @@ extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache
         if ((unused.start && (st = hip_check(hipEventRecord(unused.start, x), "record timing event"))) ||
             (unused.stop && (st = hip_check(hipEventRecord(unused.stop, x), "record timing event"))))
             return st;
-        if (p > 0 && (st = hip_check(hipEventRecord(ex->gathered[p], x), "record"))) return st;
+        if (p == 0 || last) {
+            // the first and the last group attend right behind their gathers, on `stream`
+            if ((st = record(events, 7 * p + 5, s))) return st;
+            if ((st = attend(p, s, ws_s))) return st;
+            if (!last && (st = record(events, 7 * p + 6, s))) return st;
+        }
+        if (p > 0 && !last && (st = hip_check(hipEventRecord(ex->gathered[p], x), "record"))) return st;
     }
-    for (int p = 0; p < P; ++p) {
-        const int b0 = b_of(p), b1 = b_of(p + 1), Bp = b1 - b0;
-        const int64_t row0 = b0 * rows_per_seq;
-        if (p > 0 && (st = hip_check(hipStreamWaitEvent(s, ex->gathered[p], 0), "order attention after gather")))
+    // the middle groups' attentions on the compute stream, each behind its gather
+    for (int p = 1; p < P - 1; ++p) {
+        if ((st = hip_check(hipStreamWaitEvent(ex->comp, ex->gathered[p], 0), "order attention after gather")))
             return st;
-        if ((st = record(events, 7 * p + 5, s))) return st;
-        st = ss_sparse_attention(q8 + (size_t)b0 * Hq * d * 2, L->cache_base, L->cache_off_dev + b0 * Hkv,
-                                 L->slots_dev + row0, L->capacity_dev ? L->capacity_dev + b0 * Hkv : nullptr,
-                                 L->slot_limit, Bp, Hq, Hkv, d, L->blk, k, L->scale,
-                                 out + (size_t)b0 * Hq * d, L->attn_ws, L->attn_ws_bytes, stream);
-        if (st) return st;
-        if ((st = record(events, 7 * p + 6, s))) return st;
+        if ((st = record(events, 7 * p + 5, ex->comp))) return st;
+        if ((st = attend(p, ex->comp, ws_c))) return st;
+        if ((st = record(events, 7 * p + 6, ex->comp))) return st;
     }
+    if (comp_attn && ((st = hip_check(hipEventRecord(ex->comp_done, ex->comp), "record")) ||
+                      (st = hip_check(hipStreamWaitEvent(s, ex->comp_done, 0), "order stream after attention"))))
+        return st;
+    // the last group's end event, once everything of the step is done on `stream`
+    if ((st = record(events, 7 * (P - 1) + 6, s))) return st;
     return SS_OK;
 }
 

@@ -151,8 +151,10 @@ class HierLayer:
         self.slots_h = st[self.units * k:2 * self.units * k].view(B, Hkv, k)
         self.miss_h = st[2 * self.units * k:2 * self.units * k + 4 * self.miss_cap].view(self.miss_cap, 4)
         self.out = torch.empty(B, cfg.Hq, D, dtype=torch.float32, device="cuda")
-        # attention runs per sequence group; one workspace serves the groups in turn
-        self.ws_bytes = max(ss.ss_sparse_attention_workspace(b, cfg.Hq, Hkv, D, cfg.blk, k) for b in set(self.part_sizes))
+        # attention runs per sequence group; with the resolve on the GPU the groups'
+        # attentions run on two streams at once, each with its own region
+        one = max(ss.ss_sparse_attention_workspace(b, cfg.Hq, Hkv, D, cfg.blk, k) for b in set(self.part_sizes))
+        self.ws_bytes = 2 * ((one + 255) // 256 * 256)
         self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device="cuda")
         p = ss._ptr
         self.buffers = ss.ss_layer_buffers(

@@ -25,7 +25,7 @@ def declared_functions():
 def test_library_builds_and_loads():
     assert os.path.exists(ss.LIB_PATH)
     header = open(os.path.join(ROOT, "include", "sparseserve.h")).read()
-    assert ss.ss_abi_version() == int(re.search(r"#define SS_ABI_VERSION (\d+)", header).group(1)) == 3
+    assert ss.ss_abi_version() == int(re.search(r"#define SS_ABI_VERSION (\d+)", header).group(1)) == 4
 
 
 def test_every_declared_symbol_is_exported():
