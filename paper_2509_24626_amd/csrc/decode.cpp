@@ -277,8 +277,9 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
 // resolve waits for a gather.  The last group's gather runs on `stream`
 // (still beside the previous group's gather on its transfer stream) with its
 // attention right behind it, so no hand-off between queues lies between the
-// link's last byte and the end of the step; `stream` then waits for the
-// compute stream.  The host enqueues the whole step and returns without
+// link's last byte and the end of the step when that gather ends last, as
+// with groups that grow to the end.  `stream` then waits for the compute
+// stream.  The host enqueues the whole step and returns without
 // waiting for any of it.
 extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache *dc, int64_t step, const void *q,
                                          float *out, void *stream, void *const *events)
