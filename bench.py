@@ -15,7 +15,8 @@ fill step right before them).  Warm-up steps beyond that one run first on
 a throwaway cache state, which is then emptied, so --warmup changes what is
 warmed (kernels, streams, host threads), never the timed workload.
 The same run then measures the full 32-layer decode step with ragged
-lengths (reported under "layers32"; --no-layers32 skips it).
+lengths (reported under "layers32"; --no-layers32 skips it), by default
+with the sequence groups pipelined across layers (ss_decode_step_dev).
 
 Prints one JSON line on stdout (progress goes to stderr):
   value      = B * steps / wall time of the timed steps (tokens/s)
@@ -76,6 +77,13 @@ def parse():
                          "(ss_decode_layer_dev); auto: host for one layer, GPU for multi-layer workloads")
     ap.add_argument("--layers32-resolve", choices=["host", "device"], default="device",
                     help="the resolve of the 32-layer sub-record")
+    ap.add_argument("--schedule", choices=["auto", "layers", "groups"], default="auto",
+                    help="multi-layer workloads: each layer's step in turn (layers), or the sequence groups "
+                         "pipelined across layers (groups: ss_decode_step_dev, device resolve only); auto: "
+                         "groups with the device resolve, layers otherwise")
+    ap.add_argument("--layers32-schedule", choices=["auto", "layers", "groups"], default="auto",
+                    help="the schedule of the 32-layer sub-record")
+    ap.add_argument("--layers32-parts", default="auto", help="the sequence groups of the 32-layer sub-record")
     ap.add_argument("--with-save", action="store_true",
                     help="every step also appends its new tokens (metadata on a fill) and saves them to DRAM "
                          "(FlashD2H); single-layer workloads, one warm-up step")
@@ -95,9 +103,9 @@ def parse():
     return ap.parse_args()
 
 
-def group_sizes(spec, B, H):
+def group_sizes(spec, B, H, schedule="layers"):
     if spec == "auto":
-        return H.default_parts(B)
+        return H.default_parts(B, schedule)
     if spec.startswith("tent"):
         return H.tent_parts(B, int(spec[4:]))
     if "," in spec:
@@ -147,7 +155,9 @@ def main():
     host = host_facts()
     log(f"host: {host}")
 
-    run = measure(cfg, args, steps, warmup, args.resolve, args.parts, torch, ss, H, synth, studies=True)
+    schedule = pick_schedule(args.schedule, cfg, args.resolve)
+    run = measure(cfg, args, steps, warmup, args.resolve, args.parts, torch, ss, H, synth, studies=True,
+                  schedule=schedule)
     result = {
         "metric": "sparse decode-step tokens/sec at 1 GPU; % HBM roofline; gather host-link GB/s",
         "value": run["value"],
@@ -188,26 +198,46 @@ def main():
     # ------------------------------------- the full 32-layer decode step
     if cfg.layers == 1 and not args.with_save and not args.no_layers32:
         c3 = synth.get(3)
-        sub = measure(c3, args, c3.steps, warmup, args.layers32_resolve, "auto", torch, ss, H, synth, studies=False)
+        sched3 = pick_schedule(args.layers32_schedule, c3, args.layers32_resolve)
+        sub = measure(c3, args, c3.steps, warmup, args.layers32_resolve, args.layers32_parts, torch, ss, H, synth,
+                      studies=False, schedule=sched3)
         result["layers32"] = {
             "workload": sub["config"]["workload"], "value": sub["value"], "unit": "tokens/s",
             "steps": c3.steps, "warmup": warmup, "ms_per_step": sub["ms_per_step"],
             "layers": c3.layers, "layers_with_own_dram_records": sub["config"]["layers_with_own_dram_records"],
-            "resolve": args.layers32_resolve, "parts": sub["parts"], "miss_rate": sub["miss_rate"],
+            "resolve": args.layers32_resolve, "schedule": sched3, "parts": sub["parts"],
+            "miss_rate": sub["miss_rate"],
             "gather": {k: sub["roofline"][k] for k in ("bound", "achieved", "peak", "unit", "frac",
                                                         "bytes_per_step", "link_busy_ms_per_step")},
             "pipeline_ms_per_layer": sub["pipeline_ms"], "step_ms_events": sub["step_ms_events"],
+            **({"pipeline_ms_per_step": sub["pipeline_ms_per_step"]} if "pipeline_ms_per_step" in sub else {}),
             "rooflines_isolated": sub["rooflines_isolated"],
-            "note": ("all 32 layers in order in every step; ragged lengths U[8k, 64k]; 30% cache per layer; "
-                     "pipeline_ms is per layer (sampled on the first and last layer of every step)")}
+            "note": ("all 32 layers in every step; ragged lengths U[8k, 64k]; 30% cache per layer; " +
+                     ("groups schedule: each sequence group runs its layers in order on its own stream, its "
+                      "layer l+1 after its layer-l attention, and the next step starts after the whole step; "
+                      "pipeline_ms_per_step from events on every gather, pipeline_ms_per_layer = per step / 32"
+                      if sched3 == "groups" else
+                      "layers schedule: each layer's step in turn; pipeline_ms is per layer (sampled on the "
+                      "first and last layer of every step)"))}
     print(json.dumps(result), flush=True)
     exit_report()
 
 
-def measure(cfg, args, steps, warmup, resolve, parts_spec, torch, ss, H, synth, studies):
+def pick_schedule(spec, cfg, resolve):
+    if spec == "auto":
+        return "groups" if cfg.layers > 1 and resolve == "device" else "layers"
+    if spec == "groups" and resolve != "device":
+        print("--schedule groups needs the device resolve", file=sys.stderr)
+        sys.exit(2)
+    return spec
+
+
+def measure(cfg, args, steps, warmup, resolve, parts_spec, torch, ss, H, synth, studies, schedule="layers"):
     """Builds the workload, runs its warm-up, times `steps` steps and
     measures each HBM kernel alone; with `studies` also runs the studies
-    and the CPU baseline on it.  Frees everything it allocated."""
+    and the CPU baseline on it.  Frees everything it allocated.
+    schedule: "layers" (each layer's step in turn) or "groups" (the groups
+    pipelined across layers, one ss_decode_step_dev call per step)."""
     lens = synth.gen.lengths(cfg, args.seed)
     nblk = (lens // cfg.blk).astype(np.int32)
     _, per_layer = H.pool_layout(cfg, nblk)
@@ -215,7 +245,7 @@ def measure(cfg, args, steps, warmup, resolve, parts_spec, torch, ss, H, synth, 
     n_distinct = H.distinct_layers(cfg, nblk, budget)
     log(f"workload {cfg.name}: {cfg.layers} layer(s), {n_distinct} with DRAM records of their own, "
         f"pool {per_layer * n_distinct / 2**30:.2f} GiB pinned")
-    parts = group_sizes(parts_spec, cfg.B, H)
+    parts = group_sizes(parts_spec, cfg.B, H, schedule)
     new_kv = None
     res = {}
     if args.with_save:
@@ -253,6 +283,26 @@ def measure(cfg, args, steps, warmup, resolve, parts_spec, torch, ss, H, synth, 
             else:
                 L.step_with_save(s, qstreams[l][s][1], new_kv[s], events)
 
+        def run_studies():
+            single = new_kv is None and cfg.layers == 1
+            if single and not args.no_working_set:
+                res["working_set"] = working_set_study(cfg, layers[0], qstreams[0][-1][0], steps + 1, args.seed, ss,
+                                                       torch)
+                res["batch_control"] = batch_control_study(cfg, layers[0], pool, ss, torch, H, args.seed)
+            if single and not args.no_variants:
+                res["score_variants"] = score_variants_study(cfg, layers[0], qstreams[0][-1][1], pool, ss, torch)
+            if args.comparisons:
+                res["load_comparison"] = load_comparison(cfg, layers[0], pool, ss, torch)
+            if not args.no_save_bandwidth:
+                res["save_bandwidth"] = save_bandwidth(ss, torch, H, comparisons=args.comparisons)
+            if not args.no_prefill:
+                res["prefill"] = prefill_study(ss, torch, H)
+            if not args.no_cpu_baseline:
+                res["cpu_baseline"] = cpu_baseline(cfg, pool, layers[0], qstreams[0], nblk, args)
+
+        groups = schedule == "groups"
+        assert not groups or (new_kv is None and resolve == "device")
+
         res["metadata_build"] = metadata_build_rate(cfg, pool, layers[0], nblk, ss, torch)
 
         # --------------------------------------------------------- warm-up
@@ -262,18 +312,34 @@ def measure(cfg, args, steps, warmup, resolve, parts_spec, torch, ss, H, synth, 
         if warmup > 1:
             qthrow = [H.query_stream(cfg, args.seed + 1000, l, warmup - 2) for l in range(cfg.layers)]
             for s in range(warmup - 1):
+                if groups:
+                    H.decode_step_groups(layers, s, [qthrow[l][s][1] for l in range(len(layers))])
+                    continue
                 for l, L in enumerate(layers):
                     L.step(s, qthrow[l][s][1])
             torch.cuda.synchronize()
             for L in layers:
                 L.reset_cache()
-        for l, L in enumerate(layers):
-            run_step(L, l, 0)
+        if groups:
+            H.decode_step_groups(layers, 0, [qstreams[l][0][1] for l in range(len(layers))])
+        else:
+            for l, L in enumerate(layers):
+                run_step(L, l, 0)
         torch.cuda.synchronize()
         log(f"warm-up done ({warmup} step(s), the last on an empty cache); timing {steps} step(s)")
 
         # ----------------------------------------------------------- timed
         P = layers[0].parts
+        if groups:
+            res.update(timed_groups(cfg, layers, qstreams, steps, resolve, args, torch, ss, H, lens, n_distinct))
+            iso = isolated_rates(cfg, layers[0], qstreams[0][steps][1], ss, torch)
+            key = (cfg.name, args.seed, steps, tuple(layers[0].part_sizes), resolve, schedule)
+            for name in iso:
+                iso[name]["traffic"] = traffic(name, key)
+            res["rooflines_isolated"] = iso
+            if studies:
+                run_studies()
+            return res
         ev = [[[torch.cuda.Event(enable_timing=True) for _ in range(7 * P)] for _ in layers] for _ in range(steps)]
         # every timing event is a barrier packet on its queue: events go only on the
         # first and the last layer of a step (the step's start and end), and there
@@ -388,22 +454,7 @@ def measure(cfg, args, steps, warmup, resolve, parts_spec, torch, ss, H, synth, 
         res["rooflines_isolated"] = iso
         if not studies:
             return res
-
-        single = new_kv is None and cfg.layers == 1
-        if single and not args.no_working_set:
-            res["working_set"] = working_set_study(cfg, layers[0], qstreams[0][-1][0], steps + 1, args.seed, ss,
-                                                   torch)
-            res["batch_control"] = batch_control_study(cfg, layers[0], pool, ss, torch, H, args.seed)
-        if single and not args.no_variants:
-            res["score_variants"] = score_variants_study(cfg, layers[0], qstreams[0][-1][1], pool, ss, torch)
-        if args.comparisons:
-            res["load_comparison"] = load_comparison(cfg, layers[0], pool, ss, torch)
-        if not args.no_save_bandwidth:
-            res["save_bandwidth"] = save_bandwidth(ss, torch, H, comparisons=args.comparisons)
-        if not args.no_prefill:
-            res["prefill"] = prefill_study(ss, torch, H)
-        if not args.no_cpu_baseline:
-            res["cpu_baseline"] = cpu_baseline(cfg, pool, layers[0], qstreams[0], nblk, args)
+        run_studies()
         return res
     finally:
         for L in layers:
@@ -411,6 +462,90 @@ def measure(cfg, args, steps, warmup, resolve, parts_spec, torch, ss, H, synth, 
         pool.close()
         torch.cuda.synchronize()
         torch.cuda.empty_cache()
+
+
+def union_ms(iv):
+    """Busy time of a set of (start, end) intervals."""
+    iv = sorted(iv)
+    busy, a0, b0 = 0.0, iv[0][0], iv[0][1]
+    for a, b in iv[1:]:
+        if a > b0:
+            busy += b0 - a0
+            a0, b0 = a, b
+        else:
+            b0 = max(b0, b)
+    return busy + b0 - a0
+
+
+def timed_groups(cfg, layers, qstreams, steps, resolve, args, torch, ss, H, lens, n_distinct):
+    """The timed steps with the sequence groups pipelined across layers (one
+    ss_decode_step_dev call per step).  Every gather of every layer carries
+    start/end events on its own dispatch; the step's start and end are
+    events on the caller's stream around the call."""
+    P = layers[0].parts
+    n = len(layers)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * n * P + 2)] for _ in range(steps)]
+    for row in ev:  # create the underlying events before timing
+        for e in row:
+            e.record()
+    torch.cuda.synchronize()
+    tot0 = [ss.ss_dev_cache_total_misses(L.dev) for L in layers]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        s = 1 + i
+        e = ev[i]
+        e[-2].record()
+        H.decode_step_groups(layers, s, [qstreams[l][s][1] for l in range(n)],
+                             events=[x.cuda_event for x in e[:2 * n * P]])
+        e[-1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    miss = sum(ss.ss_dev_cache_total_misses(L.dev) - m0 for L, m0 in zip(layers, tot0)) / steps
+    pipe = {"ramp": [], "link_busy": [], "link_gaps": [], "tail": []}
+    gather_launch_ms, step_ms = [], []
+    for i in range(steps):
+        e = ev[i]
+        st = e[-2]
+        iv = [(st.elapsed_time(e[2 * j]), st.elapsed_time(e[2 * j + 1])) for j in range(n * P)]
+        gather_launch_ms += [b - a for a, b in iv]
+        busy = union_ms(iv)
+        first, last = min(a for a, _ in iv), max(b for _, b in iv)
+        end = st.elapsed_time(e[-1])
+        step_ms.append(end)
+        pipe["ramp"].append(first)
+        pipe["link_busy"].append(busy)
+        pipe["link_gaps"].append(last - first - busy)
+        pipe["tail"].append(end - last)
+    per_step = {k: float(np.mean(v)) for k, v in pipe.items()}
+    step_ms = np.array(step_ms)
+    units = cfg.B * cfg.Hkv
+    gather_bytes = miss * cfg.record_bytes
+    busy_ms = per_step["link_busy"]
+    ach = gather_bytes / (busy_ms * 1e-3) / 1e9 if busy_ms > 0 else 0.0
+    value = cfg.B * steps / wall
+    miss_rate = miss / (n * units * cfg.k)
+    pipe_layer = {k: round(v / n, 4) for k, v in per_step.items()}
+    log(f"{cfg.name} (groups across layers): {value:.0f} tokens/s, {wall / steps * 1e3:.3f} ms/step; gather "
+        f"{ach:.1f} GB/s; miss rate {miss_rate:.4f}; per step {per_step}")
+    return {
+        "value": round(value, 2), "ms_per_step": round(wall / steps * 1e3, 4),
+        "config": {"workload": cfg.name, "batch": cfg.B, "q_heads": cfg.Hq, "kv_heads": cfg.Hkv, "head_dim": D,
+                   "context": int(lens.max()), "block": cfg.blk, "topk_blocks": cfg.k, "cache_frac": cfg.cache_frac,
+                   "layers": cfg.layers, "layers_with_own_dram_records": n_distinct, "drift": cfg.drift,
+                   "seed": args.seed, "resolve": resolve, "schedule": "groups"},
+        "roofline": {"kernel": "gather", "bound": "host-link", "achieved": round(ach, 2),
+                     "peak": round(LINK_PEAK_GBS, 2), "unit": "GB/s", "frac": round(ach / LINK_PEAK_GBS, 4),
+                     "bytes_per_step": int(gather_bytes), "link_busy_ms_per_step": round(busy_ms, 4),
+                     "launches_per_step": n * P, "ms_per_launch": round(float(np.mean(gather_launch_ms)), 4),
+                     "traffic": None},
+        "pipeline_ms": pipe_layer,
+        "pipeline_ms_per_step": {k: round(v, 4) for k, v in per_step.items()},
+        "step_ms_events": {"median": round(float(np.median(step_ms)), 4), "min": round(float(step_ms.min()), 4),
+                           "max": round(float(step_ms.max()), 4), "p90": round(float(np.percentile(step_ms, 90)), 4)},
+        "parts": layers[0].part_sizes,
+        "miss_rate": round(miss_rate, 4),
+        "miss_rate_per_step": None,
+    }
 
 
 def metadata_build_rate(cfg, pool, L0, nblk, ss, torch):

@@ -67,7 +67,7 @@ typedef int ss_status;
 #define SS_ERR_HIP 5         /* a HIP runtime call or kernel launch failed */
 #define SS_ERR_TIMEOUT 6     /* the host waited longer than its deadline for GPU work */
 
-#define SS_ABI_VERSION 4
+#define SS_ABI_VERSION 5
 
 int ss_abi_version(void);
 const char *ss_status_string(ss_status status);
@@ -544,6 +544,44 @@ ss_status ss_set_host_wait_timeout(int64_t ms);
  * ss_cache_region_offsets gives them for the same capacities. */
 ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache *cache, int64_t step, const void *q,
                               float *out, void *stream, void *const *events);
+
+/* The decode step of n_layers layers with the resolve on the GPU, the
+ * sequence groups pipelined across layers (Section 3.1's executor / cache
+ * manager exchange, layer after layer).  A sequence's attention reads only
+ * its own blocks, and its next layer depends only on its own output of this
+ * one, so group p (the groups of layers[0], the same in every layer) runs
+ * score, top-k, resolve, gather and attention of layer 0, then of layer 1,
+ * ..., in order on one stream: group 0 on `stream`, groups 1..3 on streams
+ * the library creates once per device (default priority), group p > 3
+ * behind group p mod 4 on its stream.  Group p's layer l+1 therefore starts
+ * as soon as its layer l is attended, beside the other groups' gathers of
+ * layer l.  Everything is ordered after the work already on `stream`, and
+ * `stream` waits for every group stream at the end (also after an error, so
+ * that a synchronisation sees all that was enqueued).  The host enqueues the
+ * whole step and returns without waiting.
+ *   layers, caches, q, out: host arrays [n_layers]; layer l is decoded with
+ *       layers[l] and caches[l] (as ss_decode_layer_dev), its queries q[l]
+ *       (device bf16 [B][Hq][d]) and its output out[l] (device fp32
+ *       [B][Hq][d]).  Every layer has the same B, Hq, Hkv, d and k; each
+ *       layers[l]->attn_ws_bytes must hold min(groups, 4) regions of the
+ *       largest ss_sparse_attention_workspace of a group, each rounded up to
+ *       256 bytes (SS_ERR_OOM otherwise).
+ *   between: NULL, or a callback the call makes on the calling thread,
+ *       while enqueueing, for every layer l < n_layers-1 and group p: after
+ *       group p's layer-l attention is enqueued and before its layer-(l+1)
+ *       scoring, with the group's sequences [b_begin, b_end) and its stream.
+ *       The caller enqueues on that stream the work that turns the group's
+ *       rows of out[l] into its rows of q[l+1] (the rest of the model's layer)
+ *       and returns SS_OK; any other value stops the call with that status.
+ *       With NULL the queries are taken as they are.
+ *   events: NULL, or 2*n_layers*groups hipEvent_t (any entry may be NULL):
+ *       events[2*(l*groups+p)+0..1] are attached to group p's layer-l gather
+ *       kernel itself (start and end of its execution).
+ * On error the calls already enqueued stay enqueued. */
+typedef ss_status (*ss_between_fn)(void *ctx, int layer, int b_begin, int b_end, void *stream);
+ss_status ss_decode_step_dev(const ss_layer_buffers *const *layers, ss_dev_cache *const *caches, int n_layers,
+                             int64_t step, const void *const *q, float *const *out, void *stream,
+                             ss_between_fn between, void *ctx, void *const *events);
 
 #ifdef __cplusplus
 }

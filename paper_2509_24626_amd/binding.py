@@ -98,6 +98,7 @@ _SIGNATURES = {
     "ss_dev_cache_total_misses": (_i32, [_vp, _vp]),
     "ss_decode_layer_dev": (_i32, [ctypes.POINTER(ss_layer_buffers), _vp, _i64, _vp, _vp, _vp, _vp]),
     "ss_set_host_wait_timeout": (_i32, [_i64]),
+    "ss_decode_step_dev": (_i32, [_vp, _vp, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp]),
     "ss_sparse_attention_static": (_i32, [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32,
                                           _vp, _vp]),
 }
@@ -452,6 +453,49 @@ def ss_decode_layer_dev(buffers, handle, step, q, out, stream=None, events=None)
     if events is not None:
         ev = (ctypes.c_void_p * len(events))(*events)
     _check(lib().ss_decode_layer_dev(ctypes.byref(buffers), handle, step, _ptr(q), _ptr(out), _stream(stream), ev))
+
+
+# int (*)(void *ctx, int layer, int b_begin, int b_end, void *stream)
+SS_BETWEEN_FN = ctypes.CFUNCTYPE(_i32, _vp, _i32, _i32, _i32, _vp)
+
+
+def _addr_array(xs):
+    if isinstance(xs, ctypes.Array):
+        return xs
+    return (ctypes.c_void_p * len(xs))(*[_ptr(x) if not isinstance(x, ss_layer_buffers) else ctypes.addressof(x)
+                                         for x in xs])
+
+
+def ss_decode_step_dev(buffers, handles, step, qs, outs, stream=None, between=None, events=None):
+    """The step over len(buffers) layers, groups pipelined across layers.
+    buffers: ss_layer_buffers per layer; handles: ss_dev_cache per layer;
+    qs, outs: per-layer tensors or device addresses (or prebuilt ctypes
+    arrays of addresses).  between: None, or a callable (layer, b_begin,
+    b_end, stream_handle) that enqueues on that HIP stream the work producing
+    the group's next-layer queries; an exception it raises stops the call and
+    is raised again here.  events: None or 2*layers*groups raw hipEvent_t
+    handles (None entries allowed)."""
+    n = len(buffers)
+    arrs = [_addr_array(buffers), _addr_array(handles), _addr_array(qs), _addr_array(outs)]
+    ev = None
+    if events is not None:
+        ev = (ctypes.c_void_p * len(events))(*events)
+    raised = []
+    cb = None
+    if between is not None:
+        def _cb(_ctx, layer, b0, b1, stream_handle):
+            try:
+                between(layer, b0, b1, stream_handle)
+                return SS_OK
+            except BaseException as e:  # noqa: BLE001 -- re-raised after the call
+                raised.append(e)
+                return SS_ERR_INVALID_ARG
+        cb = SS_BETWEEN_FN(_cb)
+    st = lib().ss_decode_step_dev(arrs[0], arrs[1], n, step, arrs[2], arrs[3], _stream(stream),
+                                  ctypes.cast(cb, ctypes.c_void_p) if cb is not None else None, None, ev)
+    if raised:
+        raise raised[0]
+    _check(st)
 
 
 def ss_dev_cache_total_misses(handle):

@@ -62,6 +62,7 @@ struct exec_state {
     hipEvent_t start = nullptr;
     hipEvent_t comp_done = nullptr;  // device resolve: the attentions on the compute stream are done
     std::vector<hipEvent_t> sel_ready, gathered;
+    std::vector<hipEvent_t> link_order;  // multi-layer step: one per (layer, group) gather
 };
 
 std::mutex g_exec_mu;
@@ -414,4 +415,173 @@ extern "C" ss_status ss_set_host_wait_timeout(int64_t ms)
 {
     g_wait_ms.store(ms > 0 ? ms : kDefaultWaitMs, std::memory_order_relaxed);
     return SS_OK;
+}
+
+// The decode step over many layers with the resolve on the GPU, the sequence
+// groups pipelined across layers.  Within a layer the groups are independent
+// (each sequence's attention reads only its own blocks), and a group's next
+// layer depends only on its own output of this layer.  So group p runs its
+// whole chain -- score, top-k, resolve, gather, attention -- layer after
+// layer on one stream of its own: its layer l+1 starts as soon as its layer l
+// is attended, while the other groups' gathers of layer l still hold the
+// link.  The link then fills and drains once per step instead of once per
+// layer, and no event is waited for between queues inside the step.  Group
+// 0 runs on `stream`, groups 1..3 on the library's compute and transfer
+// streams (the hardware queues a process has); with more than four groups,
+// group p shares the stream of group p mod 4 and runs behind it.
+extern "C" ss_status ss_decode_step_dev(const ss_layer_buffers *const *layers, ss_dev_cache *const *caches,
+                                        int n_layers, int64_t step, const void *const *q, float *const *out,
+                                        void *stream, ss_between_fn between, void *ctx, void *const *events)
+{
+    SS_CHECK_ARG(n_layers >= 0, "ss_decode_step_dev: n_layers=%d", n_layers);
+    if (n_layers == 0) return SS_OK;
+    SS_CHECK_ARG(layers && caches && q && out, "ss_decode_step_dev: null argument");
+    const ss_layer_buffers *L0 = layers[0];
+    SS_CHECK_ARG(L0, "ss_decode_step_dev: null layer 0");
+    const int B = L0->B, Hkv = L0->Hkv, Hq = L0->Hq, k = L0->k, d = L0->d;
+    int P = L0->parts < 1 ? 1 : (L0->parts > B ? B : L0->parts);
+    if (L0->part_end) P = L0->parts;
+    SS_CHECK_ARG(B >= 0 && P >= 1, "ss_decode_step_dev: B=%d parts=%d", B, L0->parts);
+    if (B == 0) return SS_OK;
+    const int32_t *pe = L0->part_end;
+    if (pe) {
+        SS_CHECK_ARG(pe[P - 1] == B, "ss_decode_step_dev: part_end must end at B=%d", B);
+        for (int p = 0; p < P; ++p)
+            SS_CHECK_ARG(pe[p] > (p ? pe[p - 1] : 0), "ss_decode_step_dev: part_end must be strictly increasing");
+    }
+    auto b_of = [&](int p) { return p == 0 ? 0 : (pe ? pe[p - 1] : (int)((int64_t)B * p / P)); };
+    const int NS = P < 4 ? P : 4;  // group streams
+    const int64_t rows_per_seq = (int64_t)Hkv * k;
+    std::vector<size_t> ws_one(n_layers);
+    for (int l = 0; l < n_layers; ++l) {
+        const ss_layer_buffers *L = layers[l];
+        ss_dev_cache *dc = caches[l];
+        SS_CHECK_ARG(L && dc && q[l] && out[l], "ss_decode_step_dev: null argument for layer %d", l);
+        SS_CHECK_ARG(L->sel_dev && L->slots_dev && L->miss_dev && L->scores && L->meta && L->nblk_dev,
+                     "ss_decode_step_dev: null buffer in layer %d", l);
+        SS_CHECK_ARG(L->B == B && L->Hkv == Hkv && L->Hq == Hq && L->k == k && L->d == d,
+                     "ss_decode_step_dev: layer %d's shape differs from layer 0's", l);
+        SS_CHECK_ARG(L->B == ss::dev_cache_batch(dc) && L->Hkv == ss::dev_cache_kv_heads(dc),
+                     "ss_decode_step_dev: layer %d's shape differs from its cache's", l);
+        SS_CHECK_ARG(L->miss_cap >= (int64_t)B * rows_per_seq, "ss_decode_step_dev: layer %d: miss_cap %lld < B*Hkv*k",
+                     l, (long long)L->miss_cap);
+        SS_CHECK_ARG(L->meta_kind == SS_META_CUBOID || L->meta_kind == SS_META_MEAN,
+                     "ss_decode_step_dev: layer %d: metadata kind %d", l, L->meta_kind);
+        size_t w1 = 0;
+        for (int p = 0; p < P; ++p) {
+            const size_t w = ss_sparse_attention_workspace(b_of(p + 1) - b_of(p), Hq, Hkv, d, L->blk, k);
+            w1 = w > w1 ? w : w1;
+        }
+        w1 = (w1 + 255) & ~(size_t)255;
+        ws_one[l] = w1;
+        if (L->attn_ws_bytes < w1 * NS || (w1 && !L->attn_ws))
+            return ss::fail(SS_ERR_OOM, "ss_decode_step_dev: layer %d: attention workspace %zu bytes < %zu", l,
+                            L->attn_ws_bytes, w1 * NS);
+    }
+    ss_status st;
+    for (int l = 0; l < n_layers; ++l)
+        if ((st = ss::dev_cache_check_step(caches[l], step, k))) return st;
+    std::lock_guard<std::mutex> lock(g_exec_mu);
+    exec_state *ex = nullptr;
+    if ((st = get_exec(P, &ex))) return st;
+    const hipStream_t s = ss::as_stream(stream);
+    if (NS > 1 && !ex->comp &&
+        (st = hip_check(hipStreamCreateWithFlags(&ex->comp, hipStreamNonBlocking), "create compute stream")))
+        return st;
+    const hipStream_t gs[4] = {s, ex->comp, ex->xfer[0], ex->xfer[1]};
+    const int64_t n_gathers = (int64_t)n_layers * P;
+    while ((int64_t)ex->link_order.size() < n_gathers) {
+        hipEvent_t e = nullptr;
+        if ((st = hip_check(hipEventCreateWithFlags(&e, hipEventDisableTiming), "create event"))) return st;
+        try {
+            ex->link_order.push_back(e);
+        } catch (const std::bad_alloc &) {
+            (void)hipEventDestroy(e);
+            return ss::fail(SS_ERR_OOM, "ss_decode_step_dev: out of memory");
+        }
+    }
+    if ((st = hip_check(hipEventRecord(ex->start, s), "record"))) return st;
+    for (int i = 1; i < NS; ++i)
+        if ((st = hip_check(hipStreamWaitEvent(gs[i], ex->start, 0), "order group stream"))) return st;
+
+    auto enqueue = [&]() -> ss_status {
+        ss_status e;
+        for (int l = 0; l < n_layers; ++l) {
+            const ss_layer_buffers *L = layers[l];
+            ss_dev_cache *dc = caches[l];
+            const size_t rec = (size_t)2 * L->blk * d * 2;
+            const size_t meta_row = (size_t)(L->meta_kind == SS_META_MEAN ? 1 : 2) * d * 2;
+            const char *q8 = static_cast<const char *>(q[l]);
+            const char *meta8 = static_cast<const char *>(L->meta);
+            int32_t *counts = ss::dev_cache_counts(dc);
+            for (int p = 0; p < P; ++p) {
+                const int i = p % NS;
+                const hipStream_t g = gs[i];
+                const int b0 = b_of(p), b1 = b_of(p + 1), Bp = b1 - b0;
+                const int64_t row0 = b0 * rows_per_seq;
+                if (l > 0 && between) {
+                    // the caller's work that turns the group's layer l-1 output into its layer l queries
+                    const ss_status r = between(ctx, l - 1, b0, b1, g);
+                    if (r != SS_OK)
+                        return ss::fail(r, "ss_decode_step_dev: the between-layer callback returned %d for layer %d, "
+                                        "sequences [%d, %d)", (int)r, l - 1, b0, b1);
+                }
+                e = ss_score_blocks_variant(q8 + (size_t)b0 * Hq * d * 2,
+                                            meta8 + (size_t)b0 * Hkv * L->nblk_max * meta_row, L->meta_kind, L->agg,
+                                            L->nblk_dev + b0, Bp, Hq, Hkv, L->nblk_max, d,
+                                            L->scores + (size_t)b0 * Hkv * L->nblk_max, g);
+                if (e) return e;
+                e = ss::launch_topk(L->scores + (size_t)b0 * Hkv * L->nblk_max, L->nblk_dev + b0, Bp, Hkv,
+                                    L->nblk_max, k, L->sel_dev + row0, nullptr, g);
+                if (e) return e;
+                e = ss::dev_cache_launch(dc, step, b0, b1, L->sel_dev + row0, k, L->nblk_dev, L->slots_dev + row0,
+                                         L->miss_dev, g);
+                if (e) return e;
+                // The link takes the gathers in (layer, group) order: gather j starts
+                // once gather j-(NS-1) has ended, so group p's gather of layer l waits
+                // for group p+1's of layer l-1 and at most NS-1 share the link.
+                // Equal groups left to share the link freely fall into step with each
+                // other (all gather, then all score and select while the link idles);
+                // in this order each group scores, selects and resolves under the
+                // other groups' transfers.
+                const int64_t j = (int64_t)l * P + p;
+                const int depth = NS - 1;
+                if (depth > 0 && j >= depth) {
+                    const int pj = (int)((j - depth) % P);
+                    if (gs[pj % NS] != g &&
+                        (e = hip_check(hipStreamWaitEvent(g, ex->link_order[j - depth], 0), "order the gathers")))
+                        return e;
+                }
+                const int ev = 2 * (l * P + p);
+                hipEvent_t g0 = events ? reinterpret_cast<hipEvent_t>(events[ev]) : nullptr;
+                hipEvent_t g1 = events ? reinterpret_cast<hipEvent_t>(events[ev + 1]) : nullptr;
+                ss::set_kernel_timing(g0, g1);
+                e = ss::launch_gather_units(L->miss_dev, counts, b0 * Hkv, b1 * Hkv, k, L->pool, L->pool_off_dev,
+                                            L->cache_base, L->cache_off_dev, L->nblk_dev, L->capacity_dev, B, Hkv,
+                                            rec, g);
+                const ss::kernel_timing unused = ss::take_kernel_timing();
+                if (e) return e;
+                if ((unused.start && (e = hip_check(hipEventRecord(unused.start, g), "record timing event"))) ||
+                    (unused.stop && (e = hip_check(hipEventRecord(unused.stop, g), "record timing event"))))
+                    return e;
+                if ((e = hip_check(hipEventRecord(ex->link_order[j], g), "record"))) return e;
+                e = ss_sparse_attention(q8 + (size_t)b0 * Hq * d * 2, L->cache_base, L->cache_off_dev + b0 * Hkv,
+                                        L->slots_dev + row0, L->capacity_dev ? L->capacity_dev + b0 * Hkv : nullptr,
+                                        L->slot_limit, Bp, Hq, Hkv, d, L->blk, k, L->scale,
+                                        out[l] + (size_t)b0 * Hq * d, static_cast<char *>(L->attn_ws) + i * ws_one[l],
+                                        ws_one[l], g);
+                if (e) return e;
+            }
+        }
+        return SS_OK;
+    };
+    st = enqueue();
+    // `stream` waits for every group stream, also after an error, so that work
+    // enqueued on it later (or a synchronisation) sees whatever was enqueued
+    for (int i = 1; i < NS; ++i) {
+        ss_status j = hip_check(hipEventRecord(ex->gathered[i], gs[i]), "record");
+        if (!j) j = hip_check(hipStreamWaitEvent(s, ex->gathered[i], 0), "order stream after the group streams");
+        if (j && !st) st = j;
+    }
+    return st;
 }

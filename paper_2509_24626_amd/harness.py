@@ -152,9 +152,10 @@ class HierLayer:
         self.miss_h = st[2 * self.units * k:2 * self.units * k + 4 * self.miss_cap].view(self.miss_cap, 4)
         self.out = torch.empty(B, cfg.Hq, D, dtype=torch.float32, device="cuda")
         # attention runs per sequence group; with the resolve on the GPU the groups'
-        # attentions run on two streams at once, each with its own region
+        # attentions run on up to four streams at once (two in a one-layer call,
+        # four when the groups are pipelined across layers), each with its own region
         one = max(ss.ss_sparse_attention_workspace(b, cfg.Hq, Hkv, D, cfg.blk, k) for b in set(self.part_sizes))
-        self.ws_bytes = 2 * ((one + 255) // 256 * 256)
+        self.ws_bytes = min(4, self.parts) * ((one + 255) // 256 * 256)
         self.ws = torch.empty(max(self.ws_bytes, 16), dtype=torch.uint8, device="cuda")
         p = ss._ptr
         self.buffers = ss.ss_layer_buffers(
@@ -314,11 +315,15 @@ def ramp_parts(B, weights=(1, 2, 5, 10, 9, 4, 1)):
     return [int(x) for x in sizes]
 
 
-def default_parts(B):
-    """The decode step's automatic sequence groups: seven ramp-shaped groups
-    for batches of 40 or more, four (weights 2, 3, 5, 6) for 8 to 39, and
-    otherwise one or two equal groups (per-group costs, a top-k launch and a
-    resolve, favour few groups)."""
+def default_parts(B, schedule="layers"):
+    """The decode step's automatic sequence groups.  One layer at a time
+    ("layers"): seven ramp-shaped groups for batches of 40 or more, four
+    (weights 2, 3, 5, 6) for 8 to 39, and otherwise one or two equal groups
+    (per-group costs, a top-k launch and a resolve, favour few groups).
+    Groups pipelined across layers ("groups"): the link fills and drains
+    once per step, so the groups are equal, four of them (one per stream)."""
+    if schedule == "groups":
+        return max(1, min(4, B))
     if B >= 40:
         return ramp_parts(B)
     if B >= 8:
@@ -373,6 +378,17 @@ def query_stream(cfg, seed, layer, steps, device="cuda"):
 # the MI355X hosts measured (the total over all allocation kinds); the rest
 # of this allowance is left for step buffers.
 POOL_BUDGET = 56 << 30
+
+
+def decode_step_groups(layers, t, qs, events=None, between=None, stream=None):
+    """Step t of every layer with the device resolve, the sequence groups
+    pipelined across layers (ss_decode_step_dev): group p's layer l+1 runs
+    as soon as its layer l is attended.  qs: per-layer query tensors.
+    Returns the per-layer outputs."""
+    assert layers and all(L.dev is not None for L in layers), "the groups schedule needs the device resolve"
+    ss.ss_decode_step_dev([L.buffers for L in layers], [L.dev for L in layers], t, qs, [L.out for L in layers],
+                          stream, between, events)
+    return [L.out for L in layers]
 
 
 def distinct_layers(cfg, nblk, budget=POOL_BUDGET):

@@ -25,6 +25,10 @@ int main(void)
     CHECK(strlen(ss_status_string(SS_OK)) > 0);
     CHECK(strcmp(ss_status_string(SS_ERR_TIMEOUT), "unknown status") != 0);
     CHECK(ss_set_host_wait_timeout(250) == SS_OK && ss_set_host_wait_timeout(0) == SS_OK);
+    /* the multi-layer step: no layers is no work; bad counts and null arrays are errors */
+    CHECK(ss_decode_step_dev(NULL, NULL, 0, 0, NULL, NULL, NULL, NULL, NULL, NULL) == SS_OK);
+    CHECK(ss_decode_step_dev(NULL, NULL, 1, 0, NULL, NULL, NULL, NULL, NULL, NULL) == SS_ERR_INVALID_ARG);
+    CHECK(ss_decode_step_dev(NULL, NULL, -1, 0, NULL, NULL, NULL, NULL, NULL, NULL) == SS_ERR_INVALID_ARG);
 
     /* Algorithm 1 over 100 bytes: 30 fits, 50 fits (80), 10 fits (90), 40 does not */
     CHECK(ss_schedule_batch(ws, 4, 100, admit, &used) == SS_OK);

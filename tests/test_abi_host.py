@@ -17,6 +17,7 @@ def declared_functions():
     for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
         text = open(h).read()
         text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        text = re.sub(r"typedef[^;]*;", "", text)  # function-pointer types are not functions
         for m in re.finditer(r"\b(ss_\w+)\s*\(", text):
             names.add(m.group(1))
     return sorted(names)
@@ -25,7 +26,7 @@ def declared_functions():
 def test_library_builds_and_loads():
     assert os.path.exists(ss.LIB_PATH)
     header = open(os.path.join(ROOT, "include", "sparseserve.h")).read()
-    assert ss.ss_abi_version() == int(re.search(r"#define SS_ABI_VERSION (\d+)", header).group(1)) == 4
+    assert ss.ss_abi_version() == int(re.search(r"#define SS_ABI_VERSION (\d+)", header).group(1)) == 5
 
 
 def test_every_declared_symbol_is_exported():
@@ -73,6 +74,9 @@ def test_null_pointers_rejected():
     expect(ss.SS_ERR_INVALID_ARG, ss.ss_build_metadata, None, FAKE, FAKE, 1, 1, 4, 16, 128, FAKE, 0)
     expect(ss.SS_ERR_INVALID_ARG, ss.ss_score_topk, FAKE, FAKE, FAKE, 1, 8, 2, 4, 128, 2, FAKE, None, 0)
     expect(ss.SS_ERR_INVALID_ARG, ss.ss_gather_blocks, None, 3, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1, 1, 8192, 0)
+    # a layer of the multi-layer step with no device buffers
+    L = ss.ss_layer_buffers(B=2, Hq=8, Hkv=2, d=128, blk=16, nblk_max=16, k=4, parts=1)
+    expect(ss.SS_ERR_INVALID_ARG, ss.ss_decode_step_dev, [L], [FAKE], 0, [FAKE], [FAKE], 0)
 
 
 def test_empty_work_is_a_no_op():
@@ -82,6 +86,8 @@ def test_empty_work_is_a_no_op():
     ss.ss_select_topk(None, None, 0, 2, 16, 4, None, 0)
     ss.ss_gather_blocks(None, 0, None, None, None, None, None, None, 1, 1, 8192, 0)
     ss.ss_sparse_attention(None, None, None, None, None, 8, 0, 8, 2, 128, 16, 4, 0.1, None, None, 0, 0)
+    ss.ss_decode_step_dev([], [], 0, [], [], 0)
+    ss.ss_decode_step_dev([ss.ss_layer_buffers(B=0, Hq=8, Hkv=2, d=128, k=4)], [FAKE], 0, [FAKE], [FAKE], 0)
 
 
 def test_score_topk_workspace_sizes():
