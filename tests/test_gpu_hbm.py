@@ -299,6 +299,35 @@ def test_topk_random_scores_match(ss, oracle_impl):
         np.testing.assert_array_equal(sel.cpu().numpy(), ref)
 
 
+def test_topk_clustered_scores(ss, oracle_impl):
+    """Score rows whose first radix digit takes one or a few values (a narrow
+    band with far outliers, mixed signs, a single value with one larger),
+    rows shorter than k and empty rows: the selections equal the oracle's."""
+    rng = np.random.default_rng(11)
+    B, Hkv, nmax, k = 4, 4, 8192, 128
+    rows = []
+    band = 30 + 1e-3 * rng.standard_normal(nmax)
+    out = band.copy()
+    out[::97] += 5e4  # 85 outliers, then the band
+    rows.append(out)
+    rows.append(0.5 * rng.standard_normal(nmax))  # mixed signs around zero
+    one = np.full(nmax, 7.0)
+    one[4000] = 8.0
+    rows.append(one)  # massive ties below one larger value
+    rows.append(np.concatenate([np.full(nmax // 2, -1.0), 1e-30 * np.arange(nmax // 2)]))  # subnormals and -1
+    rows.append(np.where(rng.random(nmax) < 0.02, 1e6, 1.0) + 1e-3 * rng.standard_normal(nmax))  # ~164 above the rest
+    rows.append(np.round(rng.standard_normal(nmax), 1))  # few distinct values
+    while len(rows) < B * Hkv:
+        rows.append(246 + 21 * rng.standard_normal(nmax))
+    sc = np.stack(rows).reshape(B, Hkv, nmax).astype(np.float32)
+    for nblk in ([nmax] * B, [nmax, 100, 0, 129]):
+        sel = torch.empty(B, Hkv, k, dtype=torch.int32, device="cuda")
+        ss.ss_select_topk(torch.from_numpy(sc).cuda(), torch.tensor(nblk, dtype=torch.int32, device="cuda"), B, Hkv,
+                          nmax, k, sel)
+        ref = oracle_impl.select(sc.astype(np.float64), np.array(nblk, np.int32), k)
+        np.testing.assert_array_equal(sel.cpu().numpy(), ref)
+
+
 def test_attention_skips_invalid_slots(ss, oracle_impl):
     """-1 entries anywhere and slots >= slot_limit are skipped."""
     w = workload("gqa1-blk32")  # B=2, Hq=Hkv=4, blk 32, 64 blocks, k=8
