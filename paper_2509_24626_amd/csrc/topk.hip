@@ -41,7 +41,7 @@ __global__ __launch_bounds__(NT) void topk_kernel(const float *__restrict__ scor
                                                   int32_t *__restrict__ mirror)
 {
     constexpr int NW = NT / 64;
-    constexpr bool kStaged = NT * R <= 8192;  // the row staged through LDS (up to 32 KiB)
+    constexpr bool kStaged = NT * R <= 16384;  // the row staged through LDS (up to 64 KiB)
     static_assert(R % 4 == 0 && (R & (R - 1)) == 0, "R: a power of two, at least 4");
     __shared__ __align__(16) int stage[kStaged ? NT * R : 4];
     __shared__ __align__(16) int rep[256 * kCopies];  // the first pass's histogram copies, bin-major
