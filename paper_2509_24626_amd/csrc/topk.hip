@@ -20,8 +20,9 @@
 // plus the first (m - #{above}) keys in the bucket in index order; because
 // threads own consecutive indices, one block-wide exclusive scan of two
 // counts gives every thread its output positions in ascending block order.
-// On MI355X this took the kernel from 26.2 to 14.6 us for 512 units of
-// 8192 blocks (k = 128) and from 15.7 to 10.7 us for 16 units.
+// On MI355X this took the kernel from 26.2 to 14.2 us for 512 units of
+// 8192 blocks (k = 128), from 15.7 to 10.3 us for 16 units and from 27.1
+// to 15.2 us for 192 units of 16384 blocks.
 #include "internal.hpp"
 
 namespace {
