@@ -178,6 +178,7 @@ def main():
                         "state, which is emptied before the fill step"),
         "roofline": run["roofline"],
         "pipeline_ms": run["pipeline_ms"],
+        **({"pipeline_ms_per_step": run["pipeline_ms_per_step"]} if "pipeline_ms_per_step" in run else {}),
         "step_ms_events": run["step_ms_events"],
         "rooflines_isolated": run["rooflines_isolated"],
         "parts": run["parts"],
@@ -658,11 +659,11 @@ KERNEL_SOURCES = {
 # 2,4,10,20,18,8,2, host resolve
 _KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 20, [2, 4, 10, 20, 18, 8, 2], "host"]
 TRAFFIC = {
-    "gather": {"key": _KEY, "digest": "403ade252186b2c7", "bytes": 245801386, "fetch": 123713962,
+    "gather": {"key": _KEY, "digest": "b9c4c3d482208f82", "bytes": 245799082, "fetch": 123711658,
               "write": 122087424},
-    "score": {"key": _KEY, "digest": "c9510f2bf97a7ac5", "bytes": 2168518623, "fetch": 2151712223,
-              "write": 16806400},
-    "topk": {"key": _KEY, "digest": "42708fbdeead668e", "bytes": 17173117, "fetch": 16910973,
+    "score": {"key": _KEY, "digest": "c9510f2bf97a7ac5", "bytes": 2168519871, "fetch": 2151712607,
+              "write": 16807264},
+    "topk": {"key": _KEY, "digest": "1d38913edab606c6", "bytes": 17217148, "fetch": 16955004,
               "write": 262144},
     "attention": {"key": _KEY, "digest": "9e23bba1c2251224", "bytes": 539142244, "fetch": 538093668,
               "write": 1048576},
