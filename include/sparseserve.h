@@ -573,7 +573,9 @@ ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache *cache, in
  *       The caller enqueues on that stream the work that turns the group's
  *       rows of out[l] into its rows of q[l+1] (the rest of the model's layer)
  *       and returns SS_OK; any other value stops the call with that status.
- *       With NULL the queries are taken as they are.
+ *       It must not call ss_decode_layer, ss_decode_layer_dev or
+ *       ss_decode_step_dev (they return SS_ERR_INVALID_ARG there: the step
+ *       holds their lock).  With NULL the queries are taken as they are.
  *   events: NULL, or 2*n_layers*groups hipEvent_t (any entry may be NULL):
  *       events[2*(l*groups+p)+0..1] are attached to group p's layer-l gather
  *       kernel itself (start and end of its execution).

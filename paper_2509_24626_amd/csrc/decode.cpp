@@ -66,6 +66,9 @@ struct exec_state {
 };
 
 std::mutex g_exec_mu;
+// set on the thread running ss_decode_step_dev's between-layer callback: the
+// step calls hold g_exec_mu, so a step call from inside the callback is refused
+thread_local bool t_in_callback = false;
 std::unordered_map<int, exec_state *> g_exec;  // by device
 
 ss_status hip_check(hipError_t e, const char *what)
@@ -162,6 +165,7 @@ ss_status record(void *const *events, int i, hipStream_t s)
 extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, const void *q, float *out, void *stream,
                                      void *const *events, int64_t *n_miss)
 {
+    SS_CHECK_ARG(!t_in_callback, "ss_decode_layer: called from a between-layer callback of ss_decode_step_dev");
     SS_CHECK_ARG(L && q && out && n_miss, "ss_decode_layer: null argument");
     SS_CHECK_ARG(L->cache && L->sel_host && L->slots_host && L->miss_host && L->sel_dev && L->slots_dev &&
                      L->miss_dev && L->scores && L->meta && L->nblk_dev,
@@ -285,6 +289,7 @@ extern "C" ss_status ss_decode_layer(const ss_layer_buffers *L, int64_t step, co
 extern "C" ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache *dc, int64_t step, const void *q,
                                          float *out, void *stream, void *const *events)
 {
+    SS_CHECK_ARG(!t_in_callback, "ss_decode_layer_dev: called from a between-layer callback of ss_decode_step_dev");
     SS_CHECK_ARG(L && dc && q && out, "ss_decode_layer_dev: null argument");
     SS_CHECK_ARG(L->sel_dev && L->slots_dev && L->miss_dev && L->scores && L->meta && L->nblk_dev,
                  "ss_decode_layer_dev: null buffer");
@@ -433,6 +438,7 @@ extern "C" ss_status ss_decode_step_dev(const ss_layer_buffers *const *layers, s
                                         int n_layers, int64_t step, const void *const *q, float *const *out,
                                         void *stream, ss_between_fn between, void *ctx, void *const *events)
 {
+    SS_CHECK_ARG(!t_in_callback, "ss_decode_step_dev: called from its own between-layer callback");
     SS_CHECK_ARG(n_layers >= 0, "ss_decode_step_dev: n_layers=%d", n_layers);
     if (n_layers == 0) return SS_OK;
     SS_CHECK_ARG(layers && caches && q && out, "ss_decode_step_dev: null argument");
@@ -521,7 +527,9 @@ extern "C" ss_status ss_decode_step_dev(const ss_layer_buffers *const *layers, s
                 const int64_t row0 = b0 * rows_per_seq;
                 if (l > 0 && between) {
                     // the caller's work that turns the group's layer l-1 output into its layer l queries
+                    t_in_callback = true;
                     const ss_status r = between(ctx, l - 1, b0, b1, g);
+                    t_in_callback = false;
                     if (r != SS_OK)
                         return ss::fail(r, "ss_decode_step_dev: the between-layer callback returned %d for layer %d, "
                                         "sequences [%d, %d)", (int)r, l - 1, b0, b1);

@@ -156,7 +156,7 @@ def test_groups_schedule_without_callback_and_events(ss):
 def test_groups_schedule_callback_error_and_checks(ss):
     """An exception in the callback stops the call and is raised; what was
     enqueued finishes, the caller's stream is ordered after it, and the next
-    step runs.  Layers of different shapes and a workspace short of one
+    step runs.  A step call made from inside the callback is refused.  Layers of different shapes and a workspace short of one
     region per stream are rejected before anything is enqueued."""
     from paper_2509_24626_amd import harness as H
     cfg, seed = small_cfg(layers=3), 7
@@ -170,6 +170,13 @@ def test_groups_schedule_callback_error_and_checks(ss):
 
         with pytest.raises(RuntimeError, match="callback stopped"):
             H.decode_step_groups(Ls, 0, [qs[l][0][1] for l in range(cfg.layers)], between=boom)
+        torch.cuda.synchronize()
+
+        def reenter(l, b0, b1, handle):  # a step call from inside the callback is refused, not deadlocked
+            Ls[0].step(1, qs[0][1][1])
+
+        with pytest.raises(ss.SparseServeError, match="between-layer callback"):
+            H.decode_step_groups(Ls, 0, [qs[l][0][1] for l in range(cfg.layers)], between=reenter)
         torch.cuda.synchronize()
         H.decode_step_groups(Ls, 1, [qs[l][1][1] for l in range(cfg.layers)])
         torch.cuda.synchronize()
