@@ -14,6 +14,10 @@
 // workload, against 2.58-2.63 with 64, 2.70 with 128, 2.55-2.64 with 16-24
 // and 3.0 with 8); the grid scales inversely with the record size so that
 // each launch keeps the same bytes in flight.
+// Loads and stores both carry the non-temporal cache policy: each record
+// passes through once (inside the decode step the stores measured 0.3-0.5%
+// more tokens/s than with the default policy, on the 128k and the 32-layer
+// workloads alike).
 // The decode step also hands the kernel a small side copy (the group's slot
 // table, from mapped host memory to HBM) so that no copy-engine transfer,
 // and no cross-engine synchronisation, sits between resolve and attention.
@@ -72,7 +76,7 @@ __global__ __launch_bounds__(256) void gather_kernel(const int4 *__restrict__ mi
         for (int r = 0; r < RPI; ++r)
             if (ok[r]) {
 #pragma unroll
-                for (int c = 0; c < CH; ++c) dst[r][c * 256 + t] = v[r][c];
+                for (int c = 0; c < CH; ++c) __builtin_nontemporal_store(v[r][c], &dst[r][c * 256 + t]);
             }
     }
 }
@@ -172,7 +176,7 @@ __global__ __launch_bounds__(256) void gather_units_kernel(const int4 *__restric
             for (int r = 0; r < RPI; ++r)
                 if (ok[r]) {
 #pragma unroll
-                    for (int c2 = 0; c2 < CH; ++c2) dst[r][c2 * 256 + t] = v[r][c2];
+                    for (int c2 = 0; c2 < CH; ++c2) __builtin_nontemporal_store(v[r][c2], &dst[r][c2 * 256 + t]);
                 }
         }
         __syncthreads();  // every wave is done with s_pre before the next chunk overwrites it
