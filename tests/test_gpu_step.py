@@ -63,14 +63,16 @@ def _stream_of(handle):
     return torch.cuda.ExternalStream(handle) if handle else torch.cuda.default_stream()
 
 
-@pytest.mark.parametrize("parts", [1, 4, 6, [2, 3, 5, 2]])
-def test_groups_schedule_equals_layer_by_layer(ss, parts):
+@pytest.mark.parametrize("B,layers,parts", [(12, 4, 1), (12, 4, 4), (12, 4, 6), (12, 4, [2, 3, 5, 2]), (13, 3, 4),
+                                            (12, 1, 4)])
+def test_groups_schedule_equals_layer_by_layer(ss, B, layers, parts):
     """Groups pipelined across layers, with the between-layer callback, give
     the per-layer path's results bit for bit at every step and layer; 6
-    groups share the four streams, and the uneven groups put groups of
-    different sizes on one stream's attention workspace."""
+    groups share the four streams, the uneven groups put groups of different
+    sizes on one stream's attention workspace, 13 sequences do not divide
+    into the groups evenly, and a single layer makes no callback."""
     from paper_2509_24626_amd import harness as H
-    cfg, seed = small_cfg(), 3
+    cfg, seed = small_cfg(B=B, layers=layers), 3
     pa, A = build(cfg, seed, parts)
     pb, Bm = build(cfg, seed, parts)
     try:
