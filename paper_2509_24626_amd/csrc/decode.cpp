@@ -430,10 +430,11 @@ extern "C" ss_status ss_set_host_wait_timeout(int64_t ms)
 // layer on one stream of its own: its layer l+1 starts as soon as its layer l
 // is attended, while the other groups' gathers of layer l still hold the
 // link.  The link then fills and drains once per step instead of once per
-// layer, and no event is waited for between queues inside the step.  Group
-// 0 runs on `stream`, groups 1..3 on the library's compute and transfer
-// streams (the hardware queues a process has); with more than four groups,
-// group p shares the stream of group p mod 4 and runs behind it.
+// layer.  Inside a group's chain nothing waits for another queue; the only
+// waits between queues order the gathers on the link (below).  Group 0 runs
+// on `stream`, groups 1..3 on the library's compute and transfer streams
+// (the hardware queues a process has); with more than four groups, group p
+// shares the stream of group p mod 4 and runs behind it.
 extern "C" ss_status ss_decode_step_dev(const ss_layer_buffers *const *layers, ss_dev_cache *const *caches,
                                         int n_layers, int64_t step, const void *const *q, float *const *out,
                                         void *stream, ss_between_fn between, void *ctx, void *const *events)
