@@ -158,8 +158,9 @@ def test_groups_schedule_without_callback_and_events(ss):
 def test_groups_schedule_callback_error_and_checks(ss):
     """An exception in the callback stops the call and is raised; what was
     enqueued finishes, the caller's stream is ordered after it, and the next
-    step runs.  A step call made from inside the callback is refused.  Layers of different shapes and a workspace short of one
-    region per stream are rejected before anything is enqueued."""
+    step runs.  A step call made from inside the callback is refused.  Layers
+    of different shapes and a workspace short of one region per stream are
+    rejected before anything is enqueued."""
     from paper_2509_24626_amd import harness as H
     cfg, seed = small_cfg(layers=3), 7
     pool, Ls = build(cfg, seed, 4)
