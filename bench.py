@@ -60,8 +60,8 @@ def parse():
     ap.add_argument("--parts", default="auto",
                     help="sequence groups pipelined within a layer step: auto (B >= 40: seven groups that grow "
                          "then shrink, 2,4,10,20,18,8,2 at B=64; 8 <= B < 40: four growing groups, 2,3,5,6 at "
-                         "B=16; smaller B: one or two), N (equal), tentN (small first/last), or comma-separated "
-                         "sizes")
+                         "B=16; smaller B: one or two; with the groups schedule four equal groups), N (equal), "
+                         "tentN (small first/last), or comma-separated sizes")
     ap.add_argument("--cpu-seqs", type=int, default=64, help="sequences in the CPU-oracle sample")
     ap.add_argument("--cpu-steps", type=int, default=8, help="timed steps in the CPU-oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
