@@ -134,3 +134,11 @@ def test_header_and_host_calls_from_plain_c(tmp_path):
         src = tmp_path / "h.cpp"
         src.write_text('#include "sparseserve.h"\nint main() { return ss_abi_version() == SS_ABI_VERSION ? 0 : 1; }\n')
         subprocess.run([cxx, "-std=c++11", "-Wall", "-Werror", "-fsyntax-only", "-I", inc, str(src)], check=True)
+
+
+def test_c_decode_step_program_builds(tmp_path):
+    """tests/c_gpu_step.c, a whole decode step through the C ABI alone (run
+    on the GPU by tests/test_gpu_c_abi.py), compiles as strict C99."""
+    import c_step_build
+    if c_step_build.build(str(tmp_path / "c_gpu_step")) is None:
+        pytest.skip("no C compiler")
