@@ -16,7 +16,9 @@ a throwaway cache state, which is then emptied, so --warmup changes what is
 warmed (kernels, streams, host threads), never the timed workload.
 The same run then measures the full 32-layer decode step with ragged
 lengths (reported under "layers32"; --no-layers32 skips it), by default
-with the sequence groups pipelined across layers (ss_decode_step_dev).
+with the sequence groups pipelined across layers and the slot tables on
+the GPU (ss_decode_step_dev), and again with them on host threads
+(ss_decode_step, under "other_resolve").
 
 Prints one JSON line on stdout (progress goes to stderr):
   value      = B * steps / wall time of the timed steps (tokens/s)
@@ -79,8 +81,8 @@ def parse():
                     help="the resolve of the 32-layer sub-record")
     ap.add_argument("--schedule", choices=["auto", "layers", "groups"], default="auto",
                     help="multi-layer workloads: each layer's step in turn (layers), or the sequence groups "
-                         "pipelined across layers (groups: ss_decode_step_dev, device resolve only); auto: "
-                         "groups with the device resolve, layers otherwise")
+                         "pipelined across layers (groups: ss_decode_step with the host resolve, "
+                         "ss_decode_step_dev with the device resolve); auto: groups for multi-layer workloads")
     ap.add_argument("--layers32-schedule", choices=["auto", "layers", "groups"], default="auto",
                     help="the schedule of the 32-layer sub-record")
     ap.add_argument("--layers32-parts", default="auto", help="the sequence groups of the 32-layer sub-record")
@@ -220,16 +222,22 @@ def main():
                       if sched3 == "groups" else
                       "layers schedule: each layer's step in turn; pipeline_ms is per layer (sampled on the "
                       "first and last layer of every step)"))}
+        # the same step with the slot tables resolved the other way (host threads, the paper's cache
+        # manager, when the default is the GPU), same schedule, same run
+        other = "host" if args.layers32_resolve == "device" else "device"
+        sub2 = measure(c3, args, c3.steps, warmup, other, args.layers32_parts, torch, ss, H, synth, studies=False,
+                       schedule=pick_schedule(args.layers32_schedule, c3, other))
+        result["layers32"]["other_resolve"] = {
+            "resolve": other, "value": sub2["value"], "ms_per_step": sub2["ms_per_step"],
+            "miss_rate": sub2["miss_rate"], "gather_frac": sub2["roofline"]["frac"],
+            **({"pipeline_ms_per_step": sub2["pipeline_ms_per_step"]} if "pipeline_ms_per_step" in sub2 else {})}
     print(json.dumps(result), flush=True)
     exit_report()
 
 
 def pick_schedule(spec, cfg, resolve):
     if spec == "auto":
-        return "groups" if cfg.layers > 1 and resolve == "device" else "layers"
-    if spec == "groups" and resolve != "device":
-        print("--schedule groups needs the device resolve", file=sys.stderr)
-        sys.exit(2)
+        return "groups" if cfg.layers > 1 else "layers"
     return spec
 
 
@@ -302,7 +310,7 @@ def measure(cfg, args, steps, warmup, resolve, parts_spec, torch, ss, H, synth, 
                 res["cpu_baseline"] = cpu_baseline(cfg, pool, layers[0], qstreams[0], nblk, args)
 
         groups = schedule == "groups"
-        assert not groups or (new_kv is None and resolve == "device")
+        assert not groups or new_kv is None
 
         res["metadata_build"] = metadata_build_rate(cfg, pool, layers[0], nblk, ss, torch)
 
@@ -485,12 +493,14 @@ def timed_groups(cfg, layers, qstreams, steps, resolve, args, torch, ss, H, lens
     events on the caller's stream around the call."""
     P = layers[0].parts
     n = len(layers)
+    dev = layers[0].dev is not None
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2 * n * P + 2)] for _ in range(steps)]
     for row in ev:  # create the underlying events before timing
         for e in row:
             e.record()
     torch.cuda.synchronize()
-    tot0 = [ss.ss_dev_cache_total_misses(L.dev) for L in layers]
+    tot0 = [ss.ss_dev_cache_total_misses(L.dev) for L in layers] if dev else None
+    host_miss = 0  # the host resolve returns its misses with each call
     t0 = time.perf_counter()
     for i in range(steps):
         s = 1 + i
@@ -499,9 +509,14 @@ def timed_groups(cfg, layers, qstreams, steps, resolve, args, torch, ss, H, lens
         H.decode_step_groups(layers, s, [qstreams[l][s][1] for l in range(n)],
                              events=[x.cuda_event for x in e[:2 * n * P]])
         e[-1].record()
+        if not dev:
+            host_miss += sum(L.last_n_miss for L in layers)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    miss = sum(ss.ss_dev_cache_total_misses(L.dev) - m0 for L, m0 in zip(layers, tot0)) / steps
+    if dev:
+        miss = sum(ss.ss_dev_cache_total_misses(L.dev) - m0 for L, m0 in zip(layers, tot0)) / steps
+    else:
+        miss = host_miss / steps
     pipe = {"ramp": [], "link_busy": [], "link_gaps": [], "tail": []}
     gather_launch_ms, step_ms = [], []
     for i in range(steps):

@@ -573,9 +573,9 @@ ss_status ss_decode_layer_dev(const ss_layer_buffers *L, ss_dev_cache *cache, in
  *       The caller enqueues on that stream the work that turns the group's
  *       rows of out[l] into its rows of q[l+1] (the rest of the model's layer)
  *       and returns SS_OK; any other value stops the call with that status.
- *       It must not call ss_decode_layer, ss_decode_layer_dev or
- *       ss_decode_step_dev (they return SS_ERR_INVALID_ARG there: the step
- *       holds their lock).  With NULL the queries are taken as they are.
+ *       It must not call ss_decode_layer, ss_decode_layer_dev,
+ *       ss_decode_step_dev or ss_decode_step (they return SS_ERR_INVALID_ARG
+ *       there: the step holds their lock).  With NULL the queries are taken as they are.
  *   events: NULL, or 2*n_layers*groups hipEvent_t (any entry may be NULL):
  *       events[2*(l*groups+p)+0..1] are attached to group p's layer-l gather
  *       kernel itself (start and end of its execution).
@@ -584,6 +584,29 @@ typedef ss_status (*ss_between_fn)(void *ctx, int layer, int b_begin, int b_end,
 ss_status ss_decode_step_dev(const ss_layer_buffers *const *layers, ss_dev_cache *const *caches, int n_layers,
                              int64_t step, const void *const *q, float *const *out, void *stream,
                              ss_between_fn between, void *ctx, void *const *events);
+
+/* The step of n_layers layers with the groups pipelined across layers as in
+ * ss_decode_step_dev, with each layer's slot table resolved on host threads
+ * (layers[l]->cache, as ss_decode_layer; Section 3.1's cache manager on the
+ * CPU).  Each group's scoring and top-k run on the group's stream and leave
+ * the selection in the layer's mapped sel_host rows as well; the host takes
+ * the (layer, group) pairs in order, waits for the pair's selection (with
+ * the deadline of ss_set_host_wait_timeout), resolves it into the layer's
+ * mapped slots_host and miss_host rows (the layer's miss rows kept compact
+ * in group order), and enqueues on the group's stream the gather (in the
+ * link order of ss_decode_step_dev; it also copies the group's slots to
+ * slots_dev), the attention, the between-layer callback and the next
+ * layer's scoring and top-k.  The call returns once everything is enqueued;
+ * `stream` waits for every group stream at the end.
+ *   layers, q, out, between, ctx, events: as ss_decode_step_dev; each layer
+ *       needs the buffers ss_decode_layer needs and an attention workspace of
+ *       min(groups, 4) regions as ss_decode_step_dev.
+ *   n_miss: NULL or host int64 [n_layers], each layer's missed blocks.
+ * On error the calls already enqueued stay enqueued; the slot tables of the
+ * (layer, group) pairs not yet resolved are unchanged. */
+ss_status ss_decode_step(const ss_layer_buffers *const *layers, int n_layers, int64_t step, const void *const *q,
+                         float *const *out, void *stream, ss_between_fn between, void *ctx, void *const *events,
+                         int64_t *n_miss);
 
 #ifdef __cplusplus
 }

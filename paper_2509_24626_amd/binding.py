@@ -99,6 +99,7 @@ _SIGNATURES = {
     "ss_decode_layer_dev": (_i32, [ctypes.POINTER(ss_layer_buffers), _vp, _i64, _vp, _vp, _vp, _vp]),
     "ss_set_host_wait_timeout": (_i32, [_i64]),
     "ss_decode_step_dev": (_i32, [_vp, _vp, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp]),
+    "ss_decode_step": (_i32, [_vp, _i32, _i64, _vp, _vp, _vp, _vp, _vp, _vp, _vp]),
     "ss_sparse_attention_static": (_i32, [_vp, _vp, _vp, _vp, _vp, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _f32,
                                           _vp, _vp]),
 }
@@ -466,6 +467,42 @@ def _addr_array(xs):
                                          for x in xs])
 
 
+def _between_cb(between, raised):
+    if between is None:
+        return None
+
+    def _cb(_ctx, layer, b0, b1, stream_handle):
+        try:
+            between(layer, b0, b1, stream_handle)
+            return SS_OK
+        except BaseException as e:  # noqa: BLE001 -- re-raised after the call
+            raised.append(e)
+            return SS_ERR_INVALID_ARG
+    return SS_BETWEEN_FN(_cb)
+
+
+def ss_decode_step(buffers, step, qs, outs, stream=None, between=None, events=None):
+    """The step over len(buffers) layers with the host resolve (each layer's
+    buffers.cache), groups pipelined across layers.  Arguments as
+    ss_decode_step_dev.  Returns each layer's missed blocks (numpy int64)."""
+    import numpy as np
+    n = len(buffers)
+    arrs = [_addr_array(buffers), _addr_array(qs), _addr_array(outs)]
+    ev = None
+    if events is not None:
+        ev = (ctypes.c_void_p * len(events))(*events)
+    raised = []
+    cb = _between_cb(between, raised)
+    n_miss = np.zeros(max(n, 1), np.int64)
+    st = lib().ss_decode_step(arrs[0], n, step, arrs[1], arrs[2], _stream(stream),
+                              ctypes.cast(cb, ctypes.c_void_p) if cb is not None else None, None, ev,
+                              n_miss.ctypes.data)
+    if raised:
+        raise raised[0]
+    _check(st)
+    return n_miss[:n]
+
+
 def ss_decode_step_dev(buffers, handles, step, qs, outs, stream=None, between=None, events=None):
     """The step over len(buffers) layers, groups pipelined across layers.
     buffers: ss_layer_buffers per layer; handles: ss_dev_cache per layer;
@@ -481,16 +518,7 @@ def ss_decode_step_dev(buffers, handles, step, qs, outs, stream=None, between=No
     if events is not None:
         ev = (ctypes.c_void_p * len(events))(*events)
     raised = []
-    cb = None
-    if between is not None:
-        def _cb(_ctx, layer, b0, b1, stream_handle):
-            try:
-                between(layer, b0, b1, stream_handle)
-                return SS_OK
-            except BaseException as e:  # noqa: BLE001 -- re-raised after the call
-                raised.append(e)
-                return SS_ERR_INVALID_ARG
-        cb = SS_BETWEEN_FN(_cb)
+    cb = _between_cb(between, raised)
     st = lib().ss_decode_step_dev(arrs[0], arrs[1], n, step, arrs[2], arrs[3], _stream(stream),
                                   ctypes.cast(cb, ctypes.c_void_p) if cb is not None else None, None, ev)
     if raised:

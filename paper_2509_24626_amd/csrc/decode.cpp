@@ -62,8 +62,26 @@ struct exec_state {
     hipEvent_t start = nullptr;
     hipEvent_t comp_done = nullptr;  // device resolve: the attentions on the compute stream are done
     std::vector<hipEvent_t> sel_ready, gathered;
-    std::vector<hipEvent_t> link_order;  // multi-layer step: one per (layer, group) gather
+    std::vector<hipEvent_t> link_order;  // multi-layer steps: one per (layer, group) gather
+    std::vector<hipEvent_t> step_sel;    // multi-layer step, host resolve: one per (layer, group) selection
 };
+
+// Grows `v` to n events (disable-timing).
+ss_status grow_events(std::vector<hipEvent_t> &v, int64_t n, const char *who)
+{
+    while ((int64_t)v.size() < n) {
+        hipEvent_t e = nullptr;
+        if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess)
+            return ss::fail(SS_ERR_HIP, "%s: create event", who);
+        try {
+            v.push_back(e);
+        } catch (const std::bad_alloc &) {
+            (void)hipEventDestroy(e);
+            return ss::fail(SS_ERR_OOM, "%s: out of memory", who);
+        }
+    }
+    return SS_OK;
+}
 
 std::mutex g_exec_mu;
 // set on the thread running ss_decode_step_dev's between-layer callback: the
@@ -496,17 +514,7 @@ extern "C" ss_status ss_decode_step_dev(const ss_layer_buffers *const *layers, s
         (st = hip_check(hipStreamCreateWithFlags(&ex->comp, hipStreamNonBlocking), "create compute stream")))
         return st;
     const hipStream_t gs[4] = {s, ex->comp, ex->xfer[0], ex->xfer[1]};
-    const int64_t n_gathers = (int64_t)n_layers * P;
-    while ((int64_t)ex->link_order.size() < n_gathers) {
-        hipEvent_t e = nullptr;
-        if ((st = hip_check(hipEventCreateWithFlags(&e, hipEventDisableTiming), "create event"))) return st;
-        try {
-            ex->link_order.push_back(e);
-        } catch (const std::bad_alloc &) {
-            (void)hipEventDestroy(e);
-            return ss::fail(SS_ERR_OOM, "ss_decode_step_dev: out of memory");
-        }
-    }
+    if ((st = grow_events(ex->link_order, (int64_t)n_layers * P, "ss_decode_step_dev"))) return st;
     if ((st = hip_check(hipEventRecord(ex->start, s), "record"))) return st;
     for (int i = 1; i < NS; ++i)
         if ((st = hip_check(hipStreamWaitEvent(gs[i], ex->start, 0), "order group stream"))) return st;
@@ -592,5 +600,177 @@ extern "C" ss_status ss_decode_step_dev(const ss_layer_buffers *const *layers, s
         if (!j) j = hip_check(hipStreamWaitEvent(s, ex->gathered[i], 0), "order stream after the group streams");
         if (j && !st) st = j;
     }
+    return st;
+}
+
+// The same schedule with the slot table resolved on host threads (the
+// paper's cache manager): each group's score and top-k run on its stream and
+// leave the selection in mapped host memory; the host takes the (layer,
+// group) pairs in order, waits for the pair's selection, resolves it, and
+// enqueues on the group's stream the gather (in the link order above), the
+// attention, the caller's between-layer work and the next layer's score and
+// top-k.  A group's host resolve is hidden under the other groups' gathers.
+extern "C" ss_status ss_decode_step(const ss_layer_buffers *const *layers, int n_layers, int64_t step,
+                                    const void *const *q, float *const *out, void *stream, ss_between_fn between,
+                                    void *ctx, void *const *events, int64_t *n_miss)
+{
+    SS_CHECK_ARG(!t_in_callback, "ss_decode_step: called from a between-layer callback");
+    SS_CHECK_ARG(n_layers >= 0, "ss_decode_step: n_layers=%d", n_layers);
+    if (n_layers == 0) return SS_OK;
+    SS_CHECK_ARG(layers && q && out, "ss_decode_step: null argument");
+    const ss_layer_buffers *L0 = layers[0];
+    SS_CHECK_ARG(L0, "ss_decode_step: null layer 0");
+    const int B = L0->B, Hkv = L0->Hkv, Hq = L0->Hq, k = L0->k, d = L0->d;
+    int P = L0->parts < 1 ? 1 : (L0->parts > B ? B : L0->parts);
+    if (L0->part_end) P = L0->parts;
+    SS_CHECK_ARG(B >= 0 && P >= 1 && k > 0, "ss_decode_step: B=%d parts=%d k=%d", B, L0->parts, k);
+    if (n_miss)
+        for (int l = 0; l < n_layers; ++l) n_miss[l] = 0;
+    if (B == 0) return SS_OK;
+    const int32_t *pe = L0->part_end;
+    if (pe) {
+        SS_CHECK_ARG(pe[P - 1] == B, "ss_decode_step: part_end must end at B=%d", B);
+        for (int p = 0; p < P; ++p)
+            SS_CHECK_ARG(pe[p] > (p ? pe[p - 1] : 0), "ss_decode_step: part_end must be strictly increasing");
+    }
+    auto b_of = [&](int p) { return p == 0 ? 0 : (pe ? pe[p - 1] : (int)((int64_t)B * p / P)); };
+    const int NS = P < 4 ? P : 4;  // group streams
+    const int64_t rows_per_seq = (int64_t)Hkv * k;
+    std::vector<size_t> ws_one(n_layers);
+    std::vector<int32_t *> sel_hd(n_layers), slots_hd(n_layers), miss_hd(n_layers);  // device views
+    ss_status st;
+    for (int l = 0; l < n_layers; ++l) {
+        const ss_layer_buffers *L = layers[l];
+        SS_CHECK_ARG(L && q[l] && out[l], "ss_decode_step: null argument for layer %d", l);
+        SS_CHECK_ARG(L->cache && L->sel_host && L->slots_host && L->miss_host && L->sel_dev && L->slots_dev &&
+                         L->scores && L->meta && L->nblk_dev,
+                     "ss_decode_step: null buffer in layer %d", l);
+        SS_CHECK_ARG(L->B == B && L->Hkv == Hkv && L->Hq == Hq && L->k == k && L->d == d,
+                     "ss_decode_step: layer %d's shape differs from layer 0's", l);
+        SS_CHECK_ARG(L->B == ss::cache_batch(L->cache) && L->Hkv == ss::cache_kv_heads(L->cache),
+                     "ss_decode_step: layer %d's shape differs from its cache handle's", l);
+        SS_CHECK_ARG(L->miss_cap >= (int64_t)B * rows_per_seq, "ss_decode_step: layer %d: miss_cap %lld < B*Hkv*k",
+                     l, (long long)L->miss_cap);
+        SS_CHECK_ARG(L->meta_kind == SS_META_CUBOID || L->meta_kind == SS_META_MEAN,
+                     "ss_decode_step: layer %d: metadata kind %d", l, L->meta_kind);
+        size_t w1 = 0;
+        for (int p = 0; p < P; ++p) {
+            const size_t w = ss_sparse_attention_workspace(b_of(p + 1) - b_of(p), Hq, Hkv, d, L->blk, k);
+            w1 = w > w1 ? w : w1;
+        }
+        w1 = (w1 + 255) & ~(size_t)255;
+        ws_one[l] = w1;
+        if (L->attn_ws_bytes < w1 * NS || (w1 && !L->attn_ws))
+            return ss::fail(SS_ERR_OOM, "ss_decode_step: layer %d: attention workspace %zu bytes < %zu", l,
+                            L->attn_ws_bytes, w1 * NS);
+        if ((st = device_address(L->sel_host, (void **)&sel_hd[l])) ||
+            (st = device_address(L->slots_host, (void **)&slots_hd[l])) ||
+            (st = device_address(L->miss_host, (void **)&miss_hd[l])))
+            return st;
+    }
+    std::lock_guard<std::mutex> lock(g_exec_mu);
+    exec_state *ex = nullptr;
+    if ((st = get_exec(P, &ex))) return st;
+    const hipStream_t s = ss::as_stream(stream);
+    if (NS > 1 && !ex->comp &&
+        (st = hip_check(hipStreamCreateWithFlags(&ex->comp, hipStreamNonBlocking), "create compute stream")))
+        return st;
+    if ((st = grow_events(ex->link_order, (int64_t)n_layers * P, "ss_decode_step")) ||
+        (st = grow_events(ex->step_sel, (int64_t)n_layers * P, "ss_decode_step")))
+        return st;
+    const hipStream_t gs[4] = {s, ex->comp, ex->xfer[0], ex->xfer[1]};
+    if ((st = hip_check(hipEventRecord(ex->start, s), "record"))) return st;
+    for (int i = 1; i < NS; ++i)
+        if ((st = hip_check(hipStreamWaitEvent(gs[i], ex->start, 0), "order group stream"))) return st;
+
+    // score and top-k of (layer l, group p) on the group's stream; the
+    // selection lands in HBM and in mapped host memory
+    auto select = [&](int l, int p) -> ss_status {
+        const ss_layer_buffers *L = layers[l];
+        const hipStream_t g = gs[p % NS];
+        const int b0 = b_of(p), Bp = b_of(p + 1) - b0;
+        const int64_t row0 = b0 * rows_per_seq;
+        const size_t meta_row = (size_t)(L->meta_kind == SS_META_MEAN ? 1 : 2) * d * 2;
+        ss_status e = ss_score_blocks_variant(static_cast<const char *>(q[l]) + (size_t)b0 * Hq * d * 2,
+                                              static_cast<const char *>(L->meta) +
+                                                  (size_t)b0 * Hkv * L->nblk_max * meta_row,
+                                              L->meta_kind, L->agg, L->nblk_dev + b0, Bp, Hq, Hkv, L->nblk_max, d,
+                                              L->scores + (size_t)b0 * Hkv * L->nblk_max, g);
+        if (e) return e;
+        e = ss::launch_topk(L->scores + (size_t)b0 * Hkv * L->nblk_max, L->nblk_dev + b0, Bp, Hkv, L->nblk_max, k,
+                            L->sel_dev + row0, sel_hd[l] + row0, g);
+        if (e) return e;
+        return hip_check(hipEventRecord(ex->step_sel[(size_t)l * P + p], g), "record");
+    };
+    std::vector<int64_t> total(n_layers, 0);  // each layer's miss rows so far (kept compact)
+    auto run = [&]() -> ss_status {
+        ss_status e;
+        for (int p = 0; p < P; ++p)
+            if ((e = select(0, p))) return e;
+        for (int l = 0; l < n_layers; ++l) {
+            const ss_layer_buffers *L = layers[l];
+            const size_t rec = (size_t)2 * L->blk * d * 2;
+            for (int p = 0; p < P; ++p) {
+                const int i = p % NS;
+                const hipStream_t g = gs[i];
+                const int b0 = b_of(p), b1 = b_of(p + 1), Bp = b1 - b0;
+                const int64_t row0 = b0 * rows_per_seq;
+                const int64_t j = (int64_t)l * P + p;
+                if ((e = wait_host(ex->step_sel[j], p, step))) return e;
+                int64_t np = 0;
+                e = ss_cache_resolve_range(L->cache, step, b0, b1, L->sel_host + row0, k, L->slots_host + row0,
+                                           L->miss_host + 4 * total[l], L->miss_cap - total[l], &np);
+                if (e) return e;
+                // the link order of ss_decode_step_dev
+                const int depth = NS - 1;
+                if (depth > 0 && j >= depth) {
+                    const int pj = (int)((j - depth) % P);
+                    if (gs[pj % NS] != g &&
+                        (e = hip_check(hipStreamWaitEvent(g, ex->link_order[j - depth], 0), "order the gathers")))
+                        return e;
+                }
+                const int ev = 2 * (int)j;
+                hipEvent_t g0 = events ? reinterpret_cast<hipEvent_t>(events[ev]) : nullptr;
+                hipEvent_t g1 = events ? reinterpret_cast<hipEvent_t>(events[ev + 1]) : nullptr;
+                ss::set_kernel_timing(g0, g1);
+                e = ss::launch_gather(miss_hd[l] + 4 * total[l], np, L->pool, L->pool_off_dev, L->cache_base,
+                                      L->cache_off_dev, L->nblk_dev, L->capacity_dev, B, Hkv, rec,
+                                      slots_hd[l] + row0, L->slots_dev + row0, (int64_t)Bp * rows_per_seq, g);
+                const ss::kernel_timing unused = ss::take_kernel_timing();
+                if (e) return e;
+                if ((unused.start && (e = hip_check(hipEventRecord(unused.start, g), "record timing event"))) ||
+                    (unused.stop && (e = hip_check(hipEventRecord(unused.stop, g), "record timing event"))) ||
+                    (e = hip_check(hipEventRecord(ex->link_order[j], g), "record")))
+                    return e;
+                total[l] += np;
+                e = ss_sparse_attention(static_cast<const char *>(q[l]) + (size_t)b0 * Hq * d * 2, L->cache_base,
+                                        L->cache_off_dev + b0 * Hkv, L->slots_dev + row0,
+                                        L->capacity_dev ? L->capacity_dev + b0 * Hkv : nullptr, L->slot_limit, Bp, Hq,
+                                        Hkv, d, L->blk, k, L->scale, out[l] + (size_t)b0 * Hq * d,
+                                        static_cast<char *>(L->attn_ws) + i * ws_one[l], ws_one[l], g);
+                if (e) return e;
+                if (l + 1 < n_layers) {
+                    if (between) {
+                        t_in_callback = true;
+                        const ss_status r = between(ctx, l, b0, b1, g);
+                        t_in_callback = false;
+                        if (r != SS_OK)
+                            return ss::fail(r, "ss_decode_step: the between-layer callback returned %d for layer %d, "
+                                            "sequences [%d, %d)", (int)r, l, b0, b1);
+                    }
+                    if ((e = select(l + 1, p))) return e;
+                }
+            }
+        }
+        return SS_OK;
+    };
+    st = run();
+    for (int i = 1; i < NS; ++i) {
+        ss_status j = hip_check(hipEventRecord(ex->gathered[i], gs[i]), "record");
+        if (!j) j = hip_check(hipStreamWaitEvent(s, ex->gathered[i], 0), "order stream after the group streams");
+        if (j && !st) st = j;
+    }
+    if (n_miss)
+        for (int l = 0; l < n_layers; ++l) n_miss[l] = total[l];
     return st;
 }

@@ -381,13 +381,22 @@ POOL_BUDGET = 56 << 30
 
 
 def decode_step_groups(layers, t, qs, events=None, between=None, stream=None):
-    """Step t of every layer with the device resolve, the sequence groups
-    pipelined across layers (ss_decode_step_dev): group p's layer l+1 runs
-    as soon as its layer l is attended.  qs: per-layer query tensors.
-    Returns the per-layer outputs."""
-    assert layers and all(L.dev is not None for L in layers), "the groups schedule needs the device resolve"
-    ss.ss_decode_step_dev([L.buffers for L in layers], [L.dev for L in layers], t, qs, [L.out for L in layers],
-                          stream, between, events)
+    """Step t of every layer, the sequence groups pipelined across layers:
+    group p's layer l+1 runs as soon as its layer l is attended.  With the
+    device resolve (every layer built with dev_cache) ss_decode_step_dev,
+    else ss_decode_step with the host resolve (each layer's last_n_miss is
+    then set).  qs: per-layer query tensors.  Returns the per-layer outputs."""
+    assert layers
+    dev = [L.dev is not None for L in layers]
+    assert all(dev) or not any(dev), "every layer resolves the same way"
+    if all(dev):
+        ss.ss_decode_step_dev([L.buffers for L in layers], [L.dev for L in layers], t, qs, [L.out for L in layers],
+                              stream, between, events)
+    else:
+        n_miss = ss.ss_decode_step([L.buffers for L in layers], t, qs, [L.out for L in layers], stream, between,
+                                   events)
+        for L, m in zip(layers, n_miss):
+            L.last_n_miss = int(m)
     return [L.out for L in layers]
 
 

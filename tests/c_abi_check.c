@@ -29,6 +29,8 @@ int main(void)
     CHECK(ss_decode_step_dev(NULL, NULL, 0, 0, NULL, NULL, NULL, NULL, NULL, NULL) == SS_OK);
     CHECK(ss_decode_step_dev(NULL, NULL, 1, 0, NULL, NULL, NULL, NULL, NULL, NULL) == SS_ERR_INVALID_ARG);
     CHECK(ss_decode_step_dev(NULL, NULL, -1, 0, NULL, NULL, NULL, NULL, NULL, NULL) == SS_ERR_INVALID_ARG);
+    CHECK(ss_decode_step(NULL, 0, 0, NULL, NULL, NULL, NULL, NULL, NULL, NULL) == SS_OK);
+    CHECK(ss_decode_step(NULL, 1, 0, NULL, NULL, NULL, NULL, NULL, NULL, NULL) == SS_ERR_INVALID_ARG);
 
     /* Algorithm 1 over 100 bytes: 30 fits, 50 fits (80), 10 fits (90), 40 does not */
     CHECK(ss_schedule_batch(ws, 4, 100, admit, &used) == SS_OK);

@@ -77,6 +77,7 @@ def test_null_pointers_rejected():
     # a layer of the multi-layer step with no device buffers
     L = ss.ss_layer_buffers(B=2, Hq=8, Hkv=2, d=128, blk=16, nblk_max=16, k=4, parts=1)
     expect(ss.SS_ERR_INVALID_ARG, ss.ss_decode_step_dev, [L], [FAKE], 0, [FAKE], [FAKE], 0)
+    expect(ss.SS_ERR_INVALID_ARG, ss.ss_decode_step, [L], 0, [FAKE], [FAKE], 0)
 
 
 def test_empty_work_is_a_no_op():
@@ -87,6 +88,7 @@ def test_empty_work_is_a_no_op():
     ss.ss_gather_blocks(None, 0, None, None, None, None, None, None, 1, 1, 8192, 0)
     ss.ss_sparse_attention(None, None, None, None, None, 8, 0, 8, 2, 128, 16, 4, 0.1, None, None, 0, 0)
     ss.ss_decode_step_dev([], [], 0, [], [], 0)
+    assert len(ss.ss_decode_step([], 0, [], [], 0)) == 0
     ss.ss_decode_step_dev([ss.ss_layer_buffers(B=0, Hq=8, Hkv=2, d=128, k=4)], [FAKE], 0, [FAKE], [FAKE], 0)
 
 

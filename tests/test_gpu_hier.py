@@ -600,7 +600,7 @@ def test_hier_gqa7_full_size_device_resolve_every_unit(ss, oracle_impl):
              max_diverged_frac=FULL_DIVERGED_FRAC, image_b=group_samples(parts))
 
 
-@pytest.mark.parametrize("mode", ["host", "device", "groups"])
+@pytest.mark.parametrize("mode", ["host", "device", "groups", "host-groups"])
 def test_layers32_ragged_full_size_every_unit(ss, oracle_impl, mode):
     """The 32-layer ragged workload at full size (B=16, lengths U[8k, 64k],
     k=128, 30% cache per layer, 8 drifting steps): every step runs all 32
@@ -608,15 +608,17 @@ def test_layers32_ragged_full_size_every_unit(ss, oracle_impl, mode):
     layers, two of which read DRAM records shared with an earlier layer.
     The automatic groups of each schedule: each layer's step in turn with
     the resolve on host threads (host) or on the GPU (device), and the
-    groups pipelined across layers in one call per step (groups,
-    ss_decode_step_dev, bench.py's default for this workload)."""
+    groups pipelined across layers in one call per step with the resolve on
+    the GPU (groups, ss_decode_step_dev) or on host threads (host-groups,
+    ss_decode_step)."""
     from paper_2509_24626_amd import harness as H
     cfg = synth.get(3)
     seed = 0
     nblk = (synth.gen.lengths(cfg, seed) // cfg.blk).astype(np.int32)
     log = lambda m: print("[gpu]", m, flush=True)
-    dev_cache = mode != "host"
-    parts = H.default_parts(cfg.B, "groups" if mode == "groups" else "layers")
+    dev_cache = mode in ("device", "groups")
+    grouped = mode in ("groups", "host-groups")
+    parts = H.default_parts(cfg.B, "groups" if grouped else "layers")
     pool, layers, n = H.build_hier_model(cfg, seed, nblk, progress=log, parts=parts, dev_cache=dev_cache)
     try:
         print(f"[gpu] {cfg.name}: {n} of {cfg.layers} layers with their own DRAM records", flush=True)
@@ -626,7 +628,7 @@ def test_layers32_ragged_full_size_every_unit(ss, oracle_impl, mode):
         tracks = {l: ParTrack(oracle_impl, cfg, layers[l], pool, range(cfg.B), f"layer {l}",
                               image_b=group_samples(layers[0].part_sizes)) for l in followed}
         for t in range(cfg.steps + 1):
-            if mode == "groups":
+            if grouped:
                 H.decode_step_groups(layers, t, [qs[l][t][1] for l in range(cfg.layers)])
             else:
                 for l, L in enumerate(layers):

@@ -1,7 +1,8 @@
-"""The decode step with the sequence groups pipelined across layers
-(ss_decode_step_dev, one call per step) against each layer's step in turn
-(ss_decode_layer_dev), whose parity with the oracle the hierarchical tests
-establish unit by unit.  Both take the same kernels over the same groups,
+"""The decode step with the sequence groups pipelined across layers (one
+call per step: ss_decode_step_dev with the slot tables resolved on the GPU,
+ss_decode_step with them resolved on host threads) against each layer's
+step in turn (ss_decode_layer_dev, ss_decode_layer), whose parity with the
+oracle the hierarchical tests establish unit by unit.  Both take the same kernels over the same groups,
 so every layer's selection, slots and attention output must be identical
 bit for bit, and so must the block caches after the run.
 
@@ -40,10 +41,10 @@ def small_cfg(B=12, layers=4):
                                layers=layers, ctx_range=(1024, 8192), steps=3)
 
 
-def build(cfg, seed, parts):
+def build(cfg, seed, parts, dev=True):
     from paper_2509_24626_amd import harness as H
     nblk = (synth.gen.lengths(cfg, seed) // cfg.blk).astype(np.int32)
-    pool, layers, n = H.build_hier_model(cfg, seed, nblk, parts=parts, dev_cache=True)
+    pool, layers, n = H.build_hier_model(cfg, seed, nblk, parts=parts, dev_cache=dev)
     assert n == cfg.layers
     return pool, layers
 
@@ -63,18 +64,23 @@ def _stream_of(handle):
     return torch.cuda.ExternalStream(handle) if handle else torch.cuda.default_stream()
 
 
-@pytest.mark.parametrize("B,layers,parts", [(12, 4, 1), (12, 4, 4), (12, 4, 6), (12, 4, [2, 3, 5, 2]), (13, 3, 4),
-                                            (12, 1, 4)])
-def test_groups_schedule_equals_layer_by_layer(ss, B, layers, parts):
+@pytest.mark.parametrize("B,layers,parts,resolve", [
+    (12, 4, 1, "device"), (12, 4, 4, "device"), (12, 4, 6, "device"), (12, 4, [2, 3, 5, 2], "device"),
+    (13, 3, 4, "device"), (12, 1, 4, "device"),
+    (12, 4, 1, "host"), (12, 4, 4, "host"), (12, 4, 6, "host"), (12, 4, [2, 3, 5, 2], "host"), (13, 3, 4, "host"),
+    (12, 1, 4, "host")])
+def test_groups_schedule_equals_layer_by_layer(ss, B, layers, parts, resolve):
     """Groups pipelined across layers, with the between-layer callback, give
-    the per-layer path's results bit for bit at every step and layer; 6
-    groups share the four streams, the uneven groups put groups of different
-    sizes on one stream's attention workspace, 13 sequences do not divide
-    into the groups evenly, and a single layer makes no callback."""
+    the per-layer path's results bit for bit at every step and layer, with
+    the slot tables on the GPU or on the host; 6 groups share the four
+    streams, the uneven groups put groups of different sizes on one stream's
+    attention workspace, 13 sequences do not divide into the groups evenly,
+    and a single layer makes no callback."""
     from paper_2509_24626_amd import harness as H
     cfg, seed = small_cfg(B=B, layers=layers), 3
-    pa, A = build(cfg, seed, parts)
-    pb, Bm = build(cfg, seed, parts)
+    dev = resolve == "device"
+    pa, A = build(cfg, seed, parts, dev)
+    pb, Bm = build(cfg, seed, parts, dev)
     try:
         base = [H.query_stream(cfg, seed, l, cfg.steps) for l in range(cfg.layers)]
         qa = [torch.empty_like(base[l][0][1]) for l in range(cfg.layers)]
@@ -100,9 +106,14 @@ def test_groups_schedule_equals_layer_by_layer(ss, B, layers, parts):
                 assert torch.equal(A[l].slots, Bm[l].slots), where
                 assert torch.equal(qa[l], qb[l]), where
                 assert torch.equal(A[l].out, Bm[l].out), where
-                ca, _, ea = A[l].dev_miss_rows()
-                cb, _, eb = Bm[l].dev_miss_rows()
-                assert ea == eb == 0 and np.array_equal(ca, cb), where
+                if dev:
+                    ca, _, ea = A[l].dev_miss_rows()
+                    cb, _, eb = Bm[l].dev_miss_rows()
+                    assert ea == eb == 0 and np.array_equal(ca, cb), where
+                else:  # the layer's miss rows, compact in group order on both paths
+                    n = A[l].last_n_miss
+                    assert n == Bm[l].last_n_miss, where
+                    assert np.array_equal(A[l].miss_h.numpy()[:n], Bm[l].miss_h.numpy()[:n]), where
         P = Bm[0].parts
         ends = np.cumsum(Bm[0].part_sizes)
         want = [(l, int(e - n), int(e)) for l in range(cfg.layers - 1) for e, n in zip(ends, Bm[0].part_sizes)]
@@ -112,23 +123,28 @@ def test_groups_schedule_equals_layer_by_layer(ss, B, layers, parts):
             n = A[l].total_slots
             sa, la = np.empty(n, np.int32), np.empty(n, np.int64)
             sb, lb = np.empty(n, np.int32), np.empty(n, np.int64)
-            ss.ss_dev_cache_export(A[l].dev, sa, la)
-            ss.ss_dev_cache_export(Bm[l].dev, sb, lb)
+            if dev:
+                ss.ss_dev_cache_export(A[l].dev, sa, la)
+                ss.ss_dev_cache_export(Bm[l].dev, sb, lb)
+                assert ss.ss_dev_cache_total_misses(A[l].dev) == ss.ss_dev_cache_total_misses(Bm[l].dev)
+            else:
+                ss.ss_cache_export(A[l].handle, sa, la)
+                ss.ss_cache_export(Bm[l].handle, sb, lb)
             assert np.array_equal(sa, sb) and np.array_equal(la, lb), f"cache of layer {l}"
-            assert ss.ss_dev_cache_total_misses(A[l].dev) == ss.ss_dev_cache_total_misses(Bm[l].dev)
     finally:
         close(pa, A)
         close(pb, Bm)
 
 
-def test_groups_schedule_without_callback_and_events(ss):
+@pytest.mark.parametrize("resolve", ["device", "host"])
+def test_groups_schedule_without_callback_and_events(ss, resolve):
     """Without a callback the queries are taken as given: the results equal
     the per-layer path's; the gather timing events of every (layer, group)
     complete, each interval inside the step."""
     from paper_2509_24626_amd import harness as H
     cfg, seed = small_cfg(B=16, layers=3), 5
-    pa, A = build(cfg, seed, 4)
-    pb, Bm = build(cfg, seed, 4)
+    pa, A = build(cfg, seed, 4, resolve == "device")
+    pb, Bm = build(cfg, seed, 4, resolve == "device")
     try:
         qs = [H.query_stream(cfg, seed, l, cfg.steps) for l in range(cfg.layers)]
         P = Bm[0].parts
@@ -155,7 +171,8 @@ def test_groups_schedule_without_callback_and_events(ss):
         close(pb, Bm)
 
 
-def test_groups_schedule_callback_error_and_checks(ss):
+@pytest.mark.parametrize("resolve", ["device", "host"])
+def test_groups_schedule_callback_error_and_checks(ss, resolve):
     """An exception in the callback stops the call and is raised; what was
     enqueued finishes, the caller's stream is ordered after it, and the next
     step runs.  A step call made from inside the callback is refused.  Layers
@@ -163,7 +180,8 @@ def test_groups_schedule_callback_error_and_checks(ss):
     rejected before anything is enqueued."""
     from paper_2509_24626_amd import harness as H
     cfg, seed = small_cfg(layers=3), 7
-    pool, Ls = build(cfg, seed, 4)
+    dev = resolve == "device"
+    pool, Ls = build(cfg, seed, 4, dev)
     try:
         qs = [H.query_stream(cfg, seed, l, cfg.steps) for l in range(cfg.layers)]
 
@@ -183,20 +201,26 @@ def test_groups_schedule_callback_error_and_checks(ss):
         torch.cuda.synchronize()
         H.decode_step_groups(Ls, 1, [qs[l][1][1] for l in range(cfg.layers)])
         torch.cuda.synchronize()
-        for L in Ls:
-            _, _, err = L.dev_miss_rows()
-            assert err == 0
+        if dev:
+            for L in Ls:
+                _, _, err = L.dev_miss_rows()
+                assert err == 0
+
+        def call(bufs):
+            q2, o2 = [qs[0][2][1], qs[1][2][1]], [Ls[0].out, Ls[1].out]
+            if dev:
+                ss.ss_decode_step_dev(bufs, [Ls[0].dev, Ls[1].dev], 2, q2, o2)
+            else:
+                ss.ss_decode_step(bufs, 2, q2, o2)
 
         b = ss.ss_layer_buffers.from_buffer_copy(Ls[1].buffers)
         b.k = cfg.k // 2
         with pytest.raises(ss.SparseServeError, match="shape differs"):
-            ss.ss_decode_step_dev([Ls[0].buffers, b], [Ls[0].dev, Ls[1].dev], 2, [qs[0][2][1], qs[1][2][1]],
-                                  [Ls[0].out, Ls[1].out])
+            call([Ls[0].buffers, b])
         b = ss.ss_layer_buffers.from_buffer_copy(Ls[1].buffers)
         b.attn_ws_bytes = Ls[1].ws_bytes // 4 * 3  # three of the four regions
         with pytest.raises(ss.SparseServeError, match="workspace"):
-            ss.ss_decode_step_dev([Ls[0].buffers, b], [Ls[0].dev, Ls[1].dev], 2, [qs[0][2][1], qs[1][2][1]],
-                                  [Ls[0].out, Ls[1].out])
+            call([Ls[0].buffers, b])
         torch.cuda.synchronize()
     finally:
         close(pool, Ls)
