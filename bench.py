@@ -674,10 +674,10 @@ KERNEL_SOURCES = {
 # 2,4,10,20,18,8,2, host resolve
 _KEY = ["hier-b64-ctx128k-blk16-k128-cache25", 0, 20, [2, 4, 10, 20, 18, 8, 2], "host"]
 TRAFFIC = {
-    "gather": {"key": _KEY, "digest": "4b25a462025388cd", "bytes": 245799274, "fetch": 123711850,
+    "gather": {"key": _KEY, "digest": "fc3ee5fdc0ce0be4", "bytes": 245801680, "fetch": 123714256,
               "write": 122087424},
-    "score": {"key": _KEY, "digest": "c9510f2bf97a7ac5", "bytes": 2168519167, "fetch": 2151712735,
-              "write": 16806432},
+    "score": {"key": _KEY, "digest": "c9510f2bf97a7ac5", "bytes": 2168521631, "fetch": 2151712671,
+              "write": 16808960},
     "topk": {"key": _KEY, "digest": "1d38913edab606c6", "bytes": 17217148, "fetch": 16955004,
               "write": 262144},
     "attention": {"key": _KEY, "digest": "9e23bba1c2251224", "bytes": 539142308, "fetch": 538093732,
