@@ -224,3 +224,44 @@ def test_groups_schedule_callback_error_and_checks(ss, resolve):
         torch.cuda.synchronize()
     finally:
         close(pool, Ls)
+
+
+def test_host_groups_schedule_wait_deadline(ss):
+    """With the host resolve, a wait for a selection that passes the deadline
+    (ss_set_host_wait_timeout) returns SS_ERR_TIMEOUT before any slot table
+    changed: the caller's stream is held busy by ordinary work queued before
+    the step (four fp32 8192^3 products) against a 2 ms deadline.  After
+    synchronising, the next steps equal those of a model that never saw the
+    failed call."""
+    from paper_2509_24626_amd import harness as H
+    cfg, seed = small_cfg(layers=2), 9
+    pa, A = build(cfg, seed, 4, False)
+    pb, Bm = build(cfg, seed, 4, False)
+    try:
+        qs = [H.query_stream(cfg, seed, l, cfg.steps) for l in range(cfg.layers)]
+        for M in (A, Bm):
+            H.decode_step_groups(M, 0, [qs[l][0][1] for l in range(cfg.layers)])
+        torch.cuda.synchronize()
+        x = torch.randn(8192, 8192, device="cuda")
+        torch.cuda.synchronize()
+        ss.ss_set_host_wait_timeout(2)
+        try:
+            for _ in range(4):
+                x = x @ x * 1e-4
+            with pytest.raises(ss.SparseServeError) as e:
+                H.decode_step_groups(Bm, 1, [qs[l][1][1] for l in range(cfg.layers)])
+            assert e.value.status == ss.SS_ERR_TIMEOUT, str(e.value)
+            assert "step 1" in str(e.value)
+        finally:
+            ss.ss_set_host_wait_timeout(0)
+        torch.cuda.synchronize()
+        for t in (1, 2):
+            for M in (A, Bm):
+                H.decode_step_groups(M, t, [qs[l][t][1] for l in range(cfg.layers)])
+            torch.cuda.synchronize()
+            for l in range(cfg.layers):
+                assert torch.equal(A[l].slots, Bm[l].slots) and torch.equal(A[l].out, Bm[l].out), (t, l)
+                assert A[l].last_n_miss == Bm[l].last_n_miss, (t, l)
+    finally:
+        close(pa, A)
+        close(pb, Bm)
