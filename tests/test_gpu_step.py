@@ -265,3 +265,31 @@ def test_host_groups_schedule_wait_deadline(ss):
     finally:
         close(pa, A)
         close(pb, Bm)
+
+
+@pytest.mark.parametrize("resolve", ["device", "host"])
+def test_groups_schedule_gqa7_blk8(ss, resolve):
+    """The GQA-7 shape (28 query / 4 KV heads, blocks of 8 tokens, k = 512,
+    15% cache, drift 0.6) over three layers with ragged lengths U[2k, 16k]:
+    the groups schedule equals layer-by-layer calls bit for bit."""
+    from paper_2509_24626_amd import harness as H
+    cfg = dataclasses.replace(synth.get(4), name="layers3-gqa7-b7-ragged2k16k-blk8-k512-cache15", B=7, layers=3,
+                              ctx=0, ctx_range=(2048, 16384), steps=3)
+    seed, dev = 4, resolve == "device"
+    pa, A = build(cfg, seed, 3, dev)
+    pb, Bm = build(cfg, seed, 3, dev)
+    try:
+        qs = [H.query_stream(cfg, seed, l, cfg.steps) for l in range(cfg.layers)]
+        for t in range(cfg.steps + 1):
+            for l, L in enumerate(A):
+                L.step(t, qs[l][t][1])
+            H.decode_step_groups(Bm, t, [qs[l][t][1] for l in range(cfg.layers)])
+            torch.cuda.synchronize()
+            for l in range(cfg.layers):
+                where = f"step {t} layer {l}"
+                assert torch.equal(A[l].sel, Bm[l].sel), where
+                assert torch.equal(A[l].slots, Bm[l].slots), where
+                assert torch.equal(A[l].out, Bm[l].out), where
+    finally:
+        close(pa, A)
+        close(pb, Bm)
